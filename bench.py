@@ -1,0 +1,186 @@
+"""Benchmark: training frames/s of one learner step on one MI355X.
+
+A step is the whole learner step of H-ADPSGD for one mini-batch: BLSTM
+forward, softmax cross-entropy forward/backward, BPTT, and the fused ADPSGD
+update (which also refreshes the bf16 operand copy), all through the C ABI.
+Inputs are seeded synthetic tensors with the paper's shapes, resident in HBM
+before timing starts.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload full_b128]
+
+Prints one JSON line.  Only one GPU is supported: the learner step is one
+GPU's share of the paper's system."""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "training frames/sec per GPU (BLSTM fwd+bwd+update); MFMA util %, HBM GB/s %"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3      # MI355X dense fp32 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def kernel_work(name, c, n_params):
+    """Algorithmic work of all launches of kernel `name` in one step:
+    (bound, amount, unit, launches).  FLOPs count 2 per multiply-add of the
+    products the step needs; bytes count each tensor read or written once."""
+    L, D, H, P, K, T, B = (c[k] for k in "LDHPKTB")
+    M = T * B
+    es = 2 if c["precision"] == "bf16" else 4
+    Dl = [D] + [2 * H] * (L - 1)
+    if name == "gemm_gx":
+        return "mfma", sum(2 * 2 * M * 4 * H * d for d in Dl), "flop", L
+    if name in ("lstm_rec_fwd", "lstm_rec_bwd"):
+        return "mfma", L * (T - 1) * 2 * 2 * B * 4 * H * H, "flop", L * T
+    if name == "gemm_dwih":
+        return "mfma", sum(2 * 2 * 4 * H * d * M for d in Dl), "flop", L
+    if name == "gemm_dwhh":
+        return "mfma", L * 2 * 2 * 4 * H * H * (T - 1) * B, "flop", L
+    if name == "gemm_dx":
+        return "mfma", (L - 1) * 2 * M * 2 * H * 8 * H, "flop", L - 1
+    if name == "gemm_z":
+        return "mfma", 2 * M * P * 2 * H, "flop", 1
+    if name in ("gemm_logits", "gemm_dws", "gemm_dz"):
+        return "mfma", 2 * M * K * P, "flop", 1
+    if name in ("gemm_dwl", "gemm_dy"):
+        return "mfma", 2 * M * P * 2 * H, "flop", 1
+    if name == "softmax_ce_rows":
+        Kp = (K + 7) // 8 * 8
+        return "hbm", 2 * M * Kp * es + 8 * M, "byte", 1
+    if name == "adpsgd_update":
+        return "hbm", n_params * (4 * 4 + (2 if es == 2 else 0)), "byte", 1
+    return None
+
+
+def peak_for(bound, precision):
+    if bound == "hbm":
+        return PEAK_HBM_GBS, "GB/s"
+    return (PEAK_BF16_TFLOPS if precision == "bf16" else PEAK_FP32_TFLOPS), "TFLOP/s"
+
+
+def cpu_baseline(cfg, budget_s=12.0):
+    """The float64 oracle on the host cores, on a bounded slice of the same
+    workload: the full layer dimensions with B=16 sequences, whole steps
+    (gradient + update) repeated until the time budget is spent."""
+    import numpy as np
+    from oracle import blstm_ref as ref
+    from paper_1907_05701_amd import inputs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count()
+    Bs = min(16, cfg["B"])
+    dims = ref.Dims(L=cfg["L"], D=cfg["D"], H=cfg["H"], P=cfg["P"], K=cfg["K"], T=cfg["T"], B=Bs)
+    n = ref.param_count(dims)
+    theta = inputs.params(n)
+    peer = inputs.peer(theta)
+    x = inputs.features(dims.T, Bs, dims.D)
+    lab = inputs.labels(dims.T, Bs, dims.K, dist=cfg["label_dist"])
+    steps, t0 = 0, time.perf_counter()
+    while True:
+        g = ref.learner_gradient(theta, dims, x, lab)
+        ref.adpsgd_update(theta, peer, g["grad"], cfg["lr"])
+        steps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or steps >= 50:
+            break
+    return {"value": round(steps * dims.T * Bs / el, 2), "unit": "frames/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{steps} float64 oracle step(s) (gradient + update) at the workload's layer "
+                      f"dimensions with B={Bs} of {cfg['B']} sequences, {el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="full_b128")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--breakdown", action="store_true", help="per-kernel times to stderr")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one learner on one GPU; --gpus {args.gpus} is not supported "
+              "(the multi-GPU exchange of the paper is not part of this library)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1907_05701_amd import binding as bd
+    from paper_1907_05701_amd import inputs
+    from paper_1907_05701_amd.step import LearnerStep
+
+    cfg = dict(inputs.CONFIGS[args.workload])
+    if "R" in cfg:
+        raise SystemExit("the update-only workload is measured by the update test, not here")
+    shape = {k: cfg[k] for k in "LDHPKTB"}
+    st = LearnerStep(**shape, precision=cfg["precision"])
+    theta = inputs.params(st.n)
+    st.load(theta, inputs.features(cfg["T"], cfg["B"], cfg["D"]),
+            inputs.labels(cfg["T"], cfg["B"], cfg["K"], dist=cfg["label_dist"]), inputs.peer(theta))
+    lr = cfg["lr"]
+    frames = cfg["T"] * cfg["B"]
+
+    for _ in range(args.warmup):
+        st.step(lr)
+    torch.cuda.synchronize()
+    # find the dominant kernel on one extra untimed step
+    bd.blstm_timing_begin("")
+    st.step(lr)
+    per = bd.blstm_timing_end()
+    torch.cuda.synchronize()
+    ranked = sorted(per.items(), key=lambda kv: -kv[1][1])
+    if args.breakdown:
+        tot = sum(v[1] for v in per.values())
+        for name, (cnt, ms) in ranked:
+            print(f"  {name:22s} {cnt:5d} launches {ms * 1e3:10.1f} us {100 * ms / tot:5.1f}%",
+                  file=sys.stderr)
+    dominant = next(n for n, _ in ranked if kernel_work(n, cfg, st.n) is not None)
+
+    # timed region: K steps, the dominant kernel bracketed by HIP events on
+    # the stream it runs on
+    torch.cuda.synchronize()
+    bd.blstm_timing_begin(dominant)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        st.step(lr)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    dom = bd.blstm_timing_end()[dominant]
+    loss = float(st.loss.cpu()[0])
+
+    ms_per_step = elapsed * 1e3 / args.steps
+    value = frames * args.steps / elapsed
+    bound, amount, unit, launches_per_step = kernel_work(dominant, cfg, st.n)
+    n_launch, total_ms = dom
+    per_launch = amount / launches_per_step
+    avg_s = total_ms / n_launch / 1e3
+    achieved = per_launch / avg_s / (1e9 if bound == "hbm" else 1e12)
+    peak, punit = peak_for(bound, cfg["precision"])
+    roofline = {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": punit,
+                "frac": round(achieved / peak, 5), "traffic": None, "kernel": dominant,
+                "avg_launch_us": round(avg_s * 1e6, 3),
+                "algorithmic_per_launch": per_launch, "algorithmic_unit": unit}
+    out = {"metric": METRIC, "value": round(value, 1), "unit": "frames/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": cfg["precision"], "data": "synthetic",
+           "config": {"workload": args.workload, **shape, "frames_per_step": frames,
+                      "params": st.n, "label_dist": cfg["label_dist"]},
+           "loss_last_step": loss, "roofline": roofline}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,112 @@
+// Shared definitions of the learner-step library: element types, the gfx950
+// MFMA wrappers, the flat parameter layout, workspace layout, error and
+// kernel-timing plumbing.  Everything here is written for CDNA4 (gfx950,
+// 64-lane wavefronts) only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "adpsgd_blstm.h"
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+#define MAX_LAYERS 16
+#define MAX_REPLICAS 16
+
+// ---------------------------------------------------------------------------
+// Element conversion.  float -> bf16 is round-to-nearest-even (the compiler
+// lowers the cast to gfx950's v_cvt_pk_bf16_f32, which rounds that way).
+// ---------------------------------------------------------------------------
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf16)v; }
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(bf16 v) { return (float)v; }
+
+// ---------------------------------------------------------------------------
+// MFMA 16x16 tiles.  For both element types lane l supplies row (l % 16) of
+// the A block and column (l % 16) of the B block, and the k values it
+// supplies are the same set for A and B; lane l receives C rows
+// 4*(l/16) .. 4*(l/16)+3 of column l % 16.
+//   bf16 : v_mfma_f32_16x16x32_bf16, 8 consecutive k per lane (one 16-byte read)
+//   float: v_mfma_f32_16x16x4_f32,   1 k per lane
+// ---------------------------------------------------------------------------
+template <typename T> struct Mfma;
+template <> struct Mfma<bf16> {
+  static constexpr int KPL = 8;
+  static constexpr int KSTEP = 32;
+  typedef bf16x8 frag;
+  __device__ static __forceinline__ f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ frag zero() { return frag{}; }
+};
+template <> struct Mfma<float> {
+  static constexpr int KPL = 1;
+  static constexpr int KSTEP = 4;
+  typedef float frag;
+  __device__ static __forceinline__ f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ frag zero() { return 0.0f; }
+};
+
+// Fast transcendental helpers for the LSTM cell (float32 throughout).
+__device__ __forceinline__ float sigmoidf_(float a) { return 1.0f / (1.0f + __expf(-a)); }
+__device__ __forceinline__ float tanhf_(float a) { return tanhf(a); }
+
+// ---------------------------------------------------------------------------
+// Host side: layout of the flat parameter vector and of the workspaces.
+// ---------------------------------------------------------------------------
+struct Layout {
+  int L, D, H, P, K, T, B, prec;
+  int64_t M;          // frames per mini-batch, T*B
+  int Dp0;            // layer-0 input width padded to a multiple of 8
+  int Kp;             // logits row pitch, K padded to a multiple of 8
+  size_t es;          // bytes per activation element (2 for bf16, 4 for float)
+  int64_t n;          // parameter count
+  // parameter offsets in elements
+  int64_t Wih[MAX_LAYERS][2], Whh[MAX_LAYERS][2], bih[MAX_LAYERS][2], bhh[MAX_LAYERS][2];
+  int64_t Wl, bl, Ws, bs;
+  // act_ws byte offsets
+  size_t X0, Y[MAX_LAYERS], G[MAX_LAYERS], C[MAX_LAYERS], GX, DYa, DYb, DC, WT, CSP, SKP;
+  size_t act_bytes;
+  // head_ws byte offsets
+  size_t Z, S, RL, DZ, DZT, HCSP, HSKP;
+  size_t head_bytes;
+  size_t ytop_bytes;
+  // split-K factors of the weight/input-gradient GEMMs (1 = direct store)
+  int sp_dWih[MAX_LAYERS], sp_dWhh, sp_dX[MAX_LAYERS], sp_dz, sp_dWs, sp_dWl, sp_dy;
+  int layer_in(int l) const { return l == 0 ? D : 2 * H; }
+  int layer_in_pitch(int l) const { return l == 0 ? Dp0 : 2 * H; }
+};
+
+// Fills *lo; returns BLSTM_OK or an error code (message set).
+int make_layout(const blstm_dims* d, Layout* lo);
+
+// Split-K factor for an output of Mo x No tiles of BMt x BNt with a reduction
+// of Kr over BK-deep tiles: 1 when the grid already fills the chip.
+int plan_splits(int64_t Mo, int64_t No, int64_t Kr, int BMt, int BNt, int BK, int batches);
+
+// Error reporting (thread-local message).
+int blstm_fail(int code, const char* fmt, ...);
+int blstm_check_launch(const char* what);
+
+// Kernel timing hooks; see blstm_timing_begin in the public header.
+extern bool g_timing_on;
+int timing_pre(const char* name, hipStream_t s);
+void timing_post(int slot, hipStream_t s);
+
+#define BLSTM_LAUNCH(name, kernel, grid, block, shmem, stream, ...)                     \
+  do {                                                                                 \
+    int _slot = g_timing_on ? timing_pre(name, stream) : -1;                           \
+    hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);               \
+    if (_slot >= 0) timing_post(_slot, stream);                                        \
+  } while (0)
+
+__host__ __device__ static inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+__host__ __device__ static inline int64_t rup(int64_t a, int64_t b) { return cdiv(a, b) * b; }

@@ -1,0 +1,267 @@
+// LDS-tiled MFMA GEMM used for every all-frames contraction of the step:
+// the gate input projection, the bottleneck and softmax-layer products and
+// all weight-gradient / input-gradient products.
+//
+// C[z][m][n] = sum_k A[z][m][k] * B[z][k][n], accumulated in float32, with
+//   - each operand either K-contiguous ("KC": element (mn, k) at row(mn) + k)
+//     or MN-contiguous ("MNC": element (mn, k) at row(k) + mn), so that
+//     transposed products (dW = da^T x, dx = da W) need no transposed copies;
+//   - a row-address map per operand (plain, segmented for the two LSTM
+//     directions stored apart, or gate-interleaved);
+//   - optional split-K over blockIdx.z (partial sums reduced afterwards in a
+//     fixed order, so results are deterministic);
+//   - an epilogue functor that receives the wave's accumulator tile.
+//
+// Block tile BM x BN x BK, WM x WN waves of 64 lanes, each wave owning a
+// (BM/WM) x (BN/WN) tile of 16x16 MFMA blocks.  Global tiles are staged in
+// registers, written to a double-buffered LDS tile laid out as
+// [BK/KPL][BMN + pad][KPL] so that one MFMA fragment is one aligned LDS read.
+#pragma once
+
+#include "common.hpp"
+
+struct Opnd {
+  const void* base;
+  int64_t ld;         // elements between consecutive index rows
+  int64_t zstride;    // elements between batch entries
+  int64_t seg;        // > 0: rows come in segments of `seg` rows ...
+  int64_t segstride;  // ... whose starts are `segstride` elements apart
+  int32_t ilH;        // > 0: gate-interleaved rows (16 units x 4 gates per 64 rows)
+  int32_t ext;        // extent of the contiguous dimension (elements)
+  int64_t rows;       // extent of the row index; rows beyond it read as zero
+};
+
+static inline Opnd opnd(const void* base, int64_t ld, int32_t ext, int64_t rows,
+                        int64_t zstride = 0) {
+  Opnd o;
+  o.base = base; o.ld = ld; o.zstride = zstride; o.seg = 0; o.segstride = 0;
+  o.ilH = 0; o.ext = ext; o.rows = rows;
+  return o;
+}
+
+template <typename T>
+__device__ __forceinline__ const T* opnd_row(const Opnd& o, int z, int64_t r) {
+  const T* p = (const T*)o.base + (int64_t)z * o.zstride;
+  if (o.ilH > 0) r = ((r >> 4) & 3) * (int64_t)o.ilH + (r >> 6) * 16 + (r & 15);
+  if (o.seg > 0) return p + (r / o.seg) * o.segstride + (r % o.seg) * o.ld;
+  return p + r * o.ld;
+}
+
+template <int BYTES> struct VecOf;
+template <> struct VecOf<16> { typedef uint4 type; };
+template <> struct VecOf<8> { typedef uint2 type; };
+
+template <typename T> struct LdsPad { static constexpr int rows = 1; };
+template <> struct LdsPad<float> { static constexpr int rows = 4; };
+
+// Global -> register -> LDS staging of one operand tile.
+template <typename T, int BMN, int BK, int NT, bool KC, int VEC>
+struct TileLoader {
+  static constexpr int KPL = Mfma<T>::KPL;
+  static constexpr int PADR = LdsPad<T>::rows;
+  typedef typename VecOf<VEC * (int)sizeof(T)>::type V;
+  static constexpr int CPR = KC ? BK / VEC : BMN / VEC;   // chunks per global row
+  static constexpr int CH = KC ? BMN * CPR : BK * CPR;
+  static constexpr int PER = (CH + NT - 1) / NT;
+  static_assert(KPL == 1 || VEC <= KPL || !KC, "bf16 K-contiguous chunk must fit a k-group");
+  V r[PER];
+
+  __device__ __forceinline__ void load(const Opnd& o, int z, int64_t mn0, int64_t k0,
+                                       int64_t kend, int tid) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int c = tid + p * NT;
+      V v = {};
+      if (CH % NT == 0 || c < CH) {
+        const int rr = c / CPR, cc = c % CPR;
+        if (KC) {
+          const int64_t row = mn0 + rr, k = k0 + (int64_t)cc * VEC;
+          const int64_t kmax = min((int64_t)o.ext, (kend + VEC - 1) / VEC * VEC);
+          if (row < o.rows && k + VEC <= kmax) v = *(const V*)(opnd_row<T>(o, z, row) + k);
+        } else {
+          const int64_t k = k0 + rr, mn = mn0 + (int64_t)cc * VEC;
+          if (k < kend && k < o.rows && mn + VEC <= o.ext) v = *(const V*)(opnd_row<T>(o, z, k) + mn);
+        }
+      }
+      r[p] = v;
+    }
+  }
+
+  __device__ __forceinline__ void store(T* lds, int tid) const {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int c = tid + p * NT;
+      if (CH % NT != 0 && c >= CH) continue;
+      const int rr = c / CPR, cc = c % CPR;
+      if (KC) {
+        const int kl = cc * VEC;
+        if (KPL == 8) {
+          *(V*)&lds[((kl / 8) * (BMN + PADR) + rr) * 8 + (kl % 8)] = r[p];
+        } else {
+          const T* e = (const T*)&r[p];
+#pragma unroll
+          for (int i = 0; i < VEC; ++i) lds[(kl + i) * (BMN + PADR) + rr] = e[i];
+        }
+      } else {
+        const int ml = cc * VEC;
+        if (KPL == 8) {
+          const T* e = (const T*)&r[p];
+#pragma unroll
+          for (int i = 0; i < VEC; ++i) lds[((rr / 8) * (BMN + PADR) + ml + i) * 8 + (rr % 8)] = e[i];
+        } else {
+          *(V*)&lds[rr * (BMN + PADR) + ml] = r[p];
+        }
+      }
+    }
+  }
+};
+
+template <typename T, int BM, int BN, int BK, int WM, int WN, bool AKC, bool BKC, int VA, int VB,
+          class Epi>
+__global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const Opnd A, const Opnd B, int64_t M,
+                                                            int64_t N, int64_t K, int64_t ksplit,
+                                                            int splits, const Epi epi) {
+  typedef Mfma<T> MT;
+  constexpr int NT = WM * WN * 64;
+  constexpr int KPL = MT::KPL;
+  constexpr int PADR = LdsPad<T>::rows;
+  constexpr int SA = (BK / KPL) * (BM + PADR) * KPL;
+  constexpr int SB = (BK / KPL) * (BN + PADR) * KPL;
+  constexpr int FM = BM / WM / 16, FN = BN / WN / 16;
+  __shared__ __attribute__((aligned(16))) T lds[2][SA + SB];
+
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wm = wid % WM, wn = wid / WM;
+  const int z = blockIdx.z / splits, sp = blockIdx.z % splits;
+  const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
+  const int64_t kbeg = (int64_t)sp * ksplit;
+  const int64_t kend = min(K, kbeg + ksplit);
+  const int ntiles = kend > kbeg ? (int)((kend - kbeg + BK - 1) / BK) : 0;
+
+  f32x4 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (ntiles > 0) {
+    TileLoader<T, BM, BK, NT, AKC, VA> la;
+    TileLoader<T, BN, BK, NT, BKC, VB> lb;
+    la.load(A, z, m0, kbeg, kend, tid);
+    lb.load(B, z, n0, kbeg, kend, tid);
+    la.store(&lds[0][0], tid);
+    lb.store(&lds[0][SA], tid);
+    __syncthreads();
+    for (int it = 0; it < ntiles; ++it) {
+      const int cur = it & 1;
+      const bool more = it + 1 < ntiles;
+      if (more) {
+        la.load(A, z, m0, kbeg + (int64_t)(it + 1) * BK, kend, tid);
+        lb.load(B, z, n0, kbeg + (int64_t)(it + 1) * BK, kend, tid);
+      }
+      const T* lA = &lds[cur][0];
+      const T* lB = &lds[cur][SA];
+#pragma unroll
+      for (int ks = 0; ks < BK / MT::KSTEP; ++ks) {
+        const int kg = ks * (MT::KSTEP / KPL) + (lane >> 4);
+        typename MT::frag a[FM], b[FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+          a[i] = *(const typename MT::frag*)&lA[(kg * (BM + PADR) + wm * (BM / WM) + i * 16 + (lane & 15)) * KPL];
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          b[j] = *(const typename MT::frag*)&lB[(kg * (BN + PADR) + wn * (BN / WN) + j * 16 + (lane & 15)) * KPL];
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) acc[i][j] = MT::mma(a[i], b[j], acc[i][j]);
+      }
+      if (more) {
+        la.store(&lds[cur ^ 1][0], tid);
+        lb.store(&lds[cur ^ 1][SA], tid);
+      }
+      __syncthreads();
+    }
+  }
+  epi.template apply<FM, FN>(z, sp, m0 + wm * (BM / WM), n0 + wn * (BN / WN), acc, lane);
+}
+
+// Plain store epilogue: out[z][sp][m][n] = acc + bias[z][n] + bias2[z][n].
+template <typename TO>
+struct EpiStore {
+  TO* out;
+  int64_t ld, zstride, sstride;
+  const float* bias;
+  const float* bias2;
+  int64_t bias_zstride;
+  int64_t M, N;
+  template <int FM, int FN>
+  __device__ __forceinline__ void apply(int z, int sp, int64_t mw, int64_t nw, f32x4 (&acc)[FM][FN],
+                                        int lane) const {
+    TO* o = out + (int64_t)z * zstride + (int64_t)sp * sstride;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int64_t n = nw + j * 16 + (lane & 15);
+      if (n >= N) continue;
+      float bv = 0.f;
+      if (bias) bv += bias[(int64_t)z * bias_zstride + n];
+      if (bias2) bv += bias2[(int64_t)z * bias_zstride + n];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t m = mw + i * 16 + (lane >> 4) * 4 + r;
+          if (m < M) o[m * ld + n] = from_f32<TO>(acc[i][j][r] + bv);
+        }
+    }
+  }
+};
+
+template <typename TO>
+static inline EpiStore<TO> epi_store(TO* out, int64_t ld, int64_t M, int64_t N, int64_t zstride = 0,
+                                     int64_t sstride = 0, const float* bias = nullptr,
+                                     const float* bias2 = nullptr, int64_t bias_zstride = 0) {
+  EpiStore<TO> e;
+  e.out = out; e.ld = ld; e.zstride = zstride; e.sstride = sstride;
+  e.bias = bias; e.bias2 = bias2; e.bias_zstride = bias_zstride; e.M = M; e.N = N;
+  return e;
+}
+
+// Tile configurations per element type.
+template <typename T> struct GemmCfg;
+template <> struct GemmCfg<bf16> {
+  static constexpr int BM = 128, BN = 128, BK = 64, WM = 2, WN = 2;
+};
+template <> struct GemmCfg<float> {
+  static constexpr int BM = 64, BN = 64, BK = 16, WM = 2, WN = 2;
+};
+
+template <typename T, bool AKC, bool BKC, int VA, int VB, class Epi>
+static inline void gemm_launch(const char* name, hipStream_t s, const Opnd& A, const Opnd& B,
+                               int64_t M, int64_t N, int64_t K, int batches, int splits,
+                               const Epi& epi) {
+  typedef GemmCfg<T> C;
+  const int64_t ksplit = splits > 1 ? rup(cdiv(K, splits), C::BK) : (K > 0 ? K : 1);
+  dim3 grid((unsigned)cdiv(N, C::BN), (unsigned)cdiv(M, C::BM), (unsigned)(batches * splits));
+  BLSTM_LAUNCH(name, (gemm_kernel<T, C::BM, C::BN, C::BK, C::WM, C::WN, AKC, BKC, VA, VB, Epi>),
+               grid, dim3(C::WM * C::WN * 64), 0, s, A, B, M, N, K, ksplit, splits, epi);
+}
+
+// Fixed-order split-K reduction: dst[z][m][n] = sum_s part[z][s][m][n]
+// (part rows are N wide), optionally also a low-precision copy.
+template <typename TC>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* part, int splits, int batches,
+                                                            int64_t M, int64_t N, float* dst,
+                                                            int64_t ld, int64_t dst_zstride,
+                                                            TC* dstc, int64_t ldc) {
+  const int64_t total = (int64_t)batches * M * N;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t z = idx / (M * N), rem = idx % (M * N), m = rem / N, n = rem % N;
+    const float* p = part + (z * splits) * M * N + rem;
+    float s = p[0];
+    for (int k = 1; k < splits; ++k) s += p[(int64_t)k * M * N];
+    dst[z * dst_zstride + m * ld + n] = s;
+    if (dstc) dstc[m * ldc + n] = from_f32<TC>(s);
+  }
+}

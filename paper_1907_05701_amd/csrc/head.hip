@@ -1,0 +1,151 @@
+// Output head of the acoustic model (Section 5.2): a linear bottleneck
+// z = W_l y + b_l (no nonlinearity), a softmax layer s = W_s z + b_s over the
+// context-dependent HMM states, and the frame cross-entropy averaged over the
+// mini-batch (eqs. 1-2, 4), together with its backward pass.
+//
+// The logits are produced once by an MFMA GEMM with the bias fused in; one
+// workgroup per frame then computes max and sum-of-exponentials with an
+// online (running-max) reduction across 64-lane wavefronts, the frame loss,
+// and overwrites the logits in place with ds = scale * (softmax - onehot),
+// which feeds the three backward GEMMs (dW_s, dz, and via dz dW_l and dy).
+#include <math.h>
+
+#include "common.hpp"
+#include "gemm.hpp"
+#include "reduce.hpp"
+
+__device__ __forceinline__ void lse_combine(float& m, float& s, float m2, float s2) {
+  const float mx = fmaxf(m, m2);
+  const float a = s > 0.f ? s * __expf(m - mx) : 0.f;
+  const float b = s2 > 0.f ? s2 * __expf(m2 - mx) : 0.f;
+  m = mx;
+  s = a + b;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void softmax_ce_rows_kernel(T* __restrict__ S, int K, int Kp,
+                                                              const int32_t* __restrict__ labels,
+                                                              float scale, float* __restrict__ rowloss) {
+  const int64_t m = blockIdx.x;
+  T* s = S + m * Kp;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  float mx = -INFINITY, sm = 0.f;
+  for (int k = tid; k < K; k += 256) {
+    const float v = to_f32(s[k]);
+    if (v > mx) {
+      sm = sm * __expf(mx - v) + 1.f;
+      mx = v;
+    } else {
+      sm += __expf(v - mx);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const float m2 = __shfl_xor(mx, off);
+    const float s2 = __shfl_xor(sm, off);
+    lse_combine(mx, sm, m2, s2);
+  }
+  __shared__ float wm[4], ws[4], sh_lse, sh_sl;
+  if (lane == 0) { wm[wid] = mx; ws[wid] = sm; }
+  __syncthreads();
+  if (tid == 0) {
+    float M0 = wm[0], S0 = ws[0];
+    for (int w = 1; w < 4; ++w) lse_combine(M0, S0, wm[w], ws[w]);
+    const float lse = M0 + __logf(S0);
+    const int lab = labels[m];
+    // an out-of-range label is not read (the loss becomes NaN instead)
+    const float sl = (lab >= 0 && lab < K) ? to_f32(s[lab]) : __int_as_float(0x7fc00000);
+    sh_lse = lse;
+    sh_sl = sl;
+    rowloss[m] = lse - sl;
+  }
+  __syncthreads();
+  const float lse = sh_lse;
+  const int lab = labels[m];
+  for (int k = tid; k < Kp; k += 256) {
+    float g = 0.f;
+    if (k < K) g = scale * (__expf(to_f32(s[k]) - lse) - (k == lab ? 1.f : 0.f));
+    s[k] = from_f32<T>(g);
+  }
+}
+
+// loss = scale * sum of per-frame losses, in a fixed order.
+__global__ __launch_bounds__(256) void loss_sum_kernel(const float* __restrict__ rowloss, int64_t M,
+                                                       float scale, float* __restrict__ loss) {
+  __shared__ float buf[256];
+  float s = 0.f;
+  for (int64_t i = threadIdx.x; i < M; i += 256) s += rowloss[i];
+  buf[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) buf[threadIdx.x] += buf[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *loss = scale * buf[0];
+}
+
+template <typename T> struct VecH { static constexpr int v = 8; };
+template <> struct VecH<float> { static constexpr int v = 4; };
+
+template <typename T>
+static int head_impl(const Layout& lo, const float* theta, const T* W, const T* ytop,
+                     const int32_t* labels, float scale, float* loss, float* dytop, float* grad,
+                     char* hws, hipStream_t s) {
+  constexpr int V = VecH<T>::v;
+  const int64_t M = lo.M;
+  const int P = lo.P, K = lo.K, Kp = lo.Kp, H2 = 2 * lo.H;
+  T* Z = (T*)(hws + lo.Z);
+  T* S = (T*)(hws + lo.S);
+  float* RL = (float*)(hws + lo.RL);
+  float* DZ = (float*)(hws + lo.DZ);
+  T* DZT = (T*)(hws + lo.DZT);
+  float* csp = (float*)(hws + lo.HCSP);
+  float* part = (float*)(hws + lo.HSKP);
+
+  // z = y W_l^T + b_l
+  gemm_launch<T, true, true, V, V>("gemm_z", s, opnd(ytop, H2, H2, M), opnd(W + lo.Wl, H2, H2, P), M,
+                                   P, H2, 1, 1, epi_store<T>(Z, P, M, P, 0, 0, theta + lo.bl));
+  // s = z W_s^T + b_s
+  gemm_launch<T, true, true, V, V>("gemm_logits", s, opnd(Z, P, P, M), opnd(W + lo.Ws, P, P, K), M,
+                                   K, P, 1, 1, epi_store<T>(S, Kp, M, K, 0, 0, theta + lo.bs));
+  // per-frame loss and ds (in place)
+  BLSTM_LAUNCH("softmax_ce_rows", softmax_ce_rows_kernel<T>, dim3((unsigned)M), dim3(256), 0, s, S, K,
+               Kp, labels, scale, RL);
+  BLSTM_LAUNCH("loss_sum", loss_sum_kernel, dim3(1), dim3(256), 0, s, RL, M, scale, loss);
+  // db_s = sum over frames of ds
+  colsum<T>("colsum_dbs", s, S, M, K, Kp, csp, K, 0, grad + lo.bs, nullptr);
+  // dW_s = ds^T z
+  gemm_f32<T, false, false, V, V>("gemm_dws", s, opnd(S, Kp, Kp, M), opnd(Z, P, P, M), K, P, M, 1,
+                                  lo.sp_dWs, grad + lo.Ws, P, 0, part);
+  // dz = ds W_s (float32 and a low-precision copy for the next products)
+  gemm_f32<T, true, false, V, V>("gemm_dz", s, opnd(S, Kp, Kp, M), opnd(W + lo.Ws, P, P, K), M, P, K,
+                                 1, lo.sp_dz, DZ, P, 0, part, DZT, P);
+  // db_l = sum over frames of dz
+  colsum<float>("colsum_dbl", s, DZ, M, P, P, csp, P, 0, grad + lo.bl, nullptr);
+  // dW_l = dz^T y
+  gemm_f32<T, false, false, V, V>("gemm_dwl", s, opnd(DZT, P, P, M), opnd(ytop, H2, H2, M), P, H2, M,
+                                  1, lo.sp_dWl, grad + lo.Wl, H2, 0, part);
+  // dy = dz W_l
+  gemm_f32<T, true, false, V, V>("gemm_dy", s, opnd(DZT, P, P, M), opnd(W + lo.Wl, H2, H2, P), M, H2,
+                                 P, 1, lo.sp_dy, dytop, H2, 0, part);
+  return blstm_check_launch("softmax_ce_fwd_bwd");
+}
+
+extern "C" int softmax_ce_fwd_bwd(const blstm_dims* dims, const float* theta, const void* theta_lp,
+                                  const void* y_top, const int32_t* labels, float loss_scale,
+                                  float* loss, float* dy_top, float* grad, void* head_ws,
+                                  hipStream_t stream) {
+  Layout lo;
+  int rc = make_layout(dims, &lo);
+  if (rc) return rc;
+  if (!theta || !y_top || !labels || !loss || !dy_top || !grad || !head_ws)
+    return blstm_fail(BLSTM_EINVAL, "softmax_ce_fwd_bwd: NULL pointer");
+  if (lo.M > 0x7fffffff) return blstm_fail(BLSTM_EUNSUPPORTED, "too many frames");
+  if (lo.prec == BLSTM_BF16) {
+    if (!theta_lp) return blstm_fail(BLSTM_EINVAL, "softmax_ce_fwd_bwd: theta_lp is NULL (bf16)");
+    return head_impl<bf16>(lo, theta, (const bf16*)theta_lp, (const bf16*)y_top, labels, loss_scale,
+                           loss, dy_top, grad, (char*)head_ws, stream);
+  }
+  return head_impl<float>(lo, theta, theta, (const float*)y_top, labels, loss_scale, loss, dy_top,
+                          grad, (char*)head_ws, stream);
+}

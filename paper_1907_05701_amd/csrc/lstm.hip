@@ -1,0 +1,376 @@
+// Bidirectional LSTM stack: forward pass and back-propagation through time
+// (Section 5.2 of the paper: 6 bidirectional layers, 512 cells per direction,
+// 21-frame non-overlapping chunks; the cell is PyTorch's nn.LSTM: gates
+// i, f, g, o, no peepholes, two biases; each chunk starts at h = c = 0).
+//
+// Per layer the forward is
+//   1. one all-frames MFMA GEMM for the input projection of both directions,
+//      G_x = X W_ih^T + b_ih + b_hh  ([T*B] x [2 * 4H]);
+//   2. T recurrent steps, each one launch that advances BOTH directions:
+//      a = G_x[t] + h_prev W_hh^T, then the fused gates and cell update.
+// The backward runs T reverse-time steps (dh_rec = da_next W_hh, fused gate
+// derivatives), then all-frames MFMA GEMMs for dW_ih, dW_hh, dx and a
+// column sum for the biases.
+//
+// Recurrent-step kernels: one workgroup owns 16 batch rows x 16 hidden units
+// of one direction; its four waves split the reduction dimension, feed MFMA
+// fragments straight from global memory (the step's operands are small and
+// L2-resident) and combine their partial sums through LDS in a fixed order,
+// so the step is latency-bound rather than bandwidth-bound.
+#include "common.hpp"
+#include "gemm.hpp"
+#include "reduce.hpp"
+
+template <typename T>
+__device__ __forceinline__ typename Mfma<T>::frag load_frag(const T* p);
+template <>
+__device__ __forceinline__ bf16x8 load_frag<bf16>(const bf16* p) {
+  return *(const bf16x8*)p;
+}
+template <>
+__device__ __forceinline__ float load_frag<float>(const float* p) {
+  return *p;
+}
+
+// --------------------------------------------------------------------------
+// Forward recurrent step.
+// --------------------------------------------------------------------------
+template <typename T>
+struct RecFwdArgs {
+  T* Y;              // layer output [M][2H]; h_prev is read from row tp, h written at row t
+  const T* Whh0;     // W_hh of the forward direction [4H][H]
+  const T* Whh1;     // W_hh of the reverse direction
+  const T* Gx;       // input projection incl. both biases [M][8H]
+  float* C;          // cell states [M][2H]
+  T* G;              // saved activated gates i, f, g, o [M][8H]
+  int Tn, B, H, tau;
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void lstm_rec_fwd_step(const RecFwdArgs<T> a) {
+  typedef Mfma<T> MT;
+  const int q = blockIdx.x, rb = blockIdx.y, d = blockIdx.z;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int H = a.H, B = a.B;
+  const int t = d ? a.Tn - 1 - a.tau : a.tau;
+  const int tp = d ? t + 1 : t - 1;
+  f32x4 acc[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (a.tau > 0) {
+    const T* Wd = d ? a.Whh1 : a.Whh0;
+    const int bl = rb * 16 + (lane & 15);
+    const bool rowok = bl < B;
+    const T* arow = a.Y + ((int64_t)tp * B + (rowok ? bl : 0)) * 2 * H + (int64_t)d * H;
+    const T* brow[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) brow[g] = Wd + ((int64_t)g * H + q * 16 + (lane & 15)) * H;
+    const int koff = (lane >> 4) * MT::KPL;
+    const int nks = H / MT::KSTEP;
+#pragma unroll 4
+    for (int ks = w; ks < nks; ks += 4) {
+      const int k = ks * MT::KSTEP + koff;
+      typename MT::frag af = rowok ? load_frag<T>(arow + k) : MT::zero();
+      typename MT::frag bf[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) bf[g] = load_frag<T>(brow[g] + k);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) acc[g] = MT::mma(af, bf[g], acc[g]);
+    }
+  }
+
+  __shared__ f32x4 red[3][4][64];
+  if (w > 0) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) red[w - 1][g][lane] = acc[g];
+  }
+  __syncthreads();
+  if (w != 0) return;
+#pragma unroll
+  for (int ww = 0; ww < 3; ++ww)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) acc[g] += red[ww][g][lane];
+
+  const int u = q * 16 + (lane & 15);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int b = rb * 16 + (lane >> 4) * 4 + r;
+    if (b >= B) continue;
+    const int64_t row = (int64_t)t * B + b;
+    const T* gx = a.Gx + row * 8 * H + (int64_t)d * 4 * H + u;
+    const float ai = acc[0][r] + to_f32(gx[0]);
+    const float af = acc[1][r] + to_f32(gx[H]);
+    const float ag = acc[2][r] + to_f32(gx[2 * H]);
+    const float ao = acc[3][r] + to_f32(gx[3 * H]);
+    const float ig = sigmoidf_(ai), fg = sigmoidf_(af), gg = tanhf_(ag), og = sigmoidf_(ao);
+    const float cp = a.tau > 0 ? a.C[((int64_t)tp * B + b) * 2 * H + (int64_t)d * H + u] : 0.f;
+    const float c = fg * cp + ig * gg;
+    const float h = og * tanhf_(c);
+    a.C[row * 2 * H + (int64_t)d * H + u] = c;
+    a.Y[row * 2 * H + (int64_t)d * H + u] = from_f32<T>(h);
+    T* gs = a.G + row * 8 * H + (int64_t)d * 4 * H + u;
+    gs[0] = from_f32<T>(ig);
+    gs[H] = from_f32<T>(fg);
+    gs[2 * H] = from_f32<T>(gg);
+    gs[3 * H] = from_f32<T>(og);
+  }
+}
+
+// --------------------------------------------------------------------------
+// Backward recurrent step (BPTT).
+// --------------------------------------------------------------------------
+template <typename T>
+struct RecBwdArgs {
+  T* DA;             // gate pre-activation gradients [M][8H]; read at t_next, written at t
+  const T* WT0;      // W_hh^T of the forward direction [H][4H]
+  const T* WT1;      // W_hh^T of the reverse direction
+  const float* DY;   // gradient reaching the layer output [M][2H]
+  const T* G;        // saved gates [M][8H]
+  const float* C;    // saved cell states [M][2H]
+  float* DC;         // carried cell gradient [2][B][H]
+  int Tn, B, H, tau;
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void lstm_rec_bwd_step(const RecBwdArgs<T> a) {
+  typedef Mfma<T> MT;
+  const int q = blockIdx.x, rb = blockIdx.y, d = blockIdx.z;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int H = a.H, B = a.B, Tn = a.Tn;
+  const int t = d ? a.tau : Tn - 1 - a.tau;
+  const int tn = d ? t - 1 : t + 1;   // processed just before t in this pass
+  const int tp = d ? t + 1 : t - 1;   // forward-pass predecessor of t
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (a.tau > 0) {
+    const T* WT = d ? a.WT1 : a.WT0;
+    const int bl = rb * 16 + (lane & 15);
+    const bool rowok = bl < B;
+    const T* arow = a.DA + ((int64_t)tn * B + (rowok ? bl : 0)) * 8 * H + (int64_t)d * 4 * H;
+    const T* brow = WT + ((int64_t)q * 16 + (lane & 15)) * 4 * H;
+    const int koff = (lane >> 4) * MT::KPL;
+    const int nks = 4 * H / MT::KSTEP;
+#pragma unroll 4
+    for (int ks = w; ks < nks; ks += 4) {
+      const int k = ks * MT::KSTEP + koff;
+      typename MT::frag af = rowok ? load_frag<T>(arow + k) : MT::zero();
+      acc = MT::mma(af, load_frag<T>(brow + k), acc);
+    }
+  }
+
+  __shared__ f32x4 red[3][64];
+  if (w > 0) red[w - 1][lane] = acc;
+  __syncthreads();
+  if (w != 0) return;
+#pragma unroll
+  for (int ww = 0; ww < 3; ++ww) acc += red[ww][lane];
+
+  const int u = q * 16 + (lane & 15);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int b = rb * 16 + (lane >> 4) * 4 + r;
+    if (b >= B) continue;
+    const int64_t row = (int64_t)t * B + b;
+    const float dh = acc[r] + a.DY[row * 2 * H + (int64_t)d * H + u];
+    const T* gs = a.G + row * 8 * H + (int64_t)d * 4 * H + u;
+    const float ig = to_f32(gs[0]), fg = to_f32(gs[H]), gg = to_f32(gs[2 * H]), og = to_f32(gs[3 * H]);
+    const float c = a.C[row * 2 * H + (int64_t)d * H + u];
+    const float cp = (tp >= 0 && tp < Tn) ? a.C[((int64_t)tp * B + b) * 2 * H + (int64_t)d * H + u] : 0.f;
+    float* dcp = a.DC + ((int64_t)d * B + b) * H + u;
+    const float dcn = a.tau > 0 ? *dcp : 0.f;
+    const float tc = tanhf_(c);
+    const float dc = dh * og * (1.f - tc * tc) + dcn;
+    *dcp = dc * fg;
+    T* da = a.DA + row * 8 * H + (int64_t)d * 4 * H + u;
+    da[0] = from_f32<T>(dc * gg * ig * (1.f - ig));
+    da[H] = from_f32<T>(dc * cp * fg * (1.f - fg));
+    da[2 * H] = from_f32<T>(dc * ig * (1.f - gg * gg));
+    da[3 * H] = from_f32<T>(dh * tc * og * (1.f - og));
+  }
+}
+
+// --------------------------------------------------------------------------
+// Small helpers: feature conversion, W_hh transposition, column sums.
+// --------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void convert_input_kernel(const float* __restrict__ x, int64_t M,
+                                                            int D, int Dp, T* __restrict__ X) {
+  const int64_t total = M * Dp;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t m = i / Dp;
+    const int k = (int)(i % Dp);
+    X[i] = from_f32<T>(k < D ? x[m * D + k] : 0.f);
+  }
+}
+
+// out[z][c][r] = in_z[r][c] for 2L matrices of R = 4H rows and C = H columns.
+struct TransposeSrc {
+  const void* p[2 * MAX_LAYERS];
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_kernel(TransposeSrc src, int R, int C, T* out) {
+  __shared__ T tile[32][33];
+  const T* in = (const T*)src.p[blockIdx.z];
+  T* o = out + (int64_t)blockIdx.z * R * C;
+  const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int i = ty; i < 32; i += 8) {
+    const int r = r0 + i, c = c0 + tx;
+    if (r < R && c < C) tile[i][tx] = in[(int64_t)r * C + c];
+  }
+  __syncthreads();
+  for (int i = ty; i < 32; i += 8) {
+    const int c = c0 + i, r = r0 + tx;
+    if (r < R && c < C) o[(int64_t)c * R + r] = tile[tx][i];
+  }
+}
+
+
+// --------------------------------------------------------------------------
+// Host entry points.
+// --------------------------------------------------------------------------
+template <typename T> struct VecW { static constexpr int v = 8; };   // 16-byte chunks
+template <> struct VecW<float> { static constexpr int v = 4; };
+
+template <typename T>
+static int fwd_impl(const Layout& lo, const float* theta, const T* W, const float* x, char* ws,
+                    T* ytop, hipStream_t s) {
+  constexpr int V = VecW<T>::v;
+  const int64_t M = lo.M;
+  const int H = lo.H, B = lo.B;
+  T* X0 = (T*)(ws + lo.X0);
+  T* GX = (T*)(ws + lo.GX);
+  {
+    const int64_t total = M * lo.Dp0;
+    const unsigned grid = (unsigned)std::min<int64_t>(cdiv(total, 256), 16384);
+    BLSTM_LAUNCH("convert_input", convert_input_kernel<T>, dim3(grid), dim3(256), 0, s, x, M, lo.D,
+                 lo.Dp0, X0);
+  }
+  for (int l = 0; l < lo.L; ++l) {
+    const T* Xl = l == 0 ? X0 : (const T*)(ws + lo.Y[l - 1]);
+    const int Dl = lo.layer_in(l), Dpl = lo.layer_in_pitch(l);
+    T* Yl = l == lo.L - 1 ? ytop : (T*)(ws + lo.Y[l]);
+    T* Gl = (T*)(ws + lo.G[l]);
+    float* Cl = (float*)(ws + lo.C[l]);
+    // G_x = X W_ih^T + b_ih + b_hh for both directions (batch z = direction)
+    const Opnd A = opnd(Xl, Dpl, Dpl, M);
+    const Opnd Bw = opnd(W + lo.Wih[l][0], Dl, Dl, 4 * H, lo.Wih[l][1] - lo.Wih[l][0]);
+    const auto epi = epi_store<T>(GX, 8 * H, M, 4 * H, 4 * H, 0, theta + lo.bih[l][0],
+                                  theta + lo.bhh[l][0], lo.bih[l][1] - lo.bih[l][0]);
+    if (Dl % V == 0)
+      gemm_launch<T, true, true, V, V>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
+    else
+      gemm_launch<T, true, true, V, 4>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
+    RecFwdArgs<T> ra;
+    ra.Y = Yl; ra.Whh0 = W + lo.Whh[l][0]; ra.Whh1 = W + lo.Whh[l][1]; ra.Gx = GX; ra.C = Cl;
+    ra.G = Gl; ra.Tn = lo.T; ra.B = B; ra.H = H;
+    const dim3 grid(H / 16, (unsigned)cdiv(B, 16), 2);
+    for (int tau = 0; tau < lo.T; ++tau) {
+      ra.tau = tau;
+      BLSTM_LAUNCH("lstm_rec_fwd", lstm_rec_fwd_step<T>, grid, dim3(256), 0, s, ra);
+    }
+  }
+  return blstm_check_launch("blstm_fwd");
+}
+
+template <typename T>
+static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const float* dytop,
+                    float* grad, hipStream_t s) {
+  constexpr int V = VecW<T>::v;
+  const int64_t M = lo.M;
+  const int H = lo.H, B = lo.B, Tn = lo.T;
+  T* WT = (T*)(ws + lo.WT);
+  T* DA = (T*)(ws + lo.GX);
+  float* DC = (float*)(ws + lo.DC);
+  float* part = (float*)(ws + lo.SKP);
+  float* csp = (float*)(ws + lo.CSP);
+  {
+    TransposeSrc src;
+    for (int i = 0; i < 2 * MAX_LAYERS; ++i) src.p[i] = nullptr;
+    for (int l = 0; l < lo.L; ++l)
+      for (int d = 0; d < 2; ++d) src.p[2 * l + d] = W + lo.Whh[l][d];
+    BLSTM_LAUNCH("transpose_whh", transpose_kernel<T>,
+                 dim3((unsigned)cdiv(H, 32), (unsigned)cdiv(4 * H, 32), 2 * lo.L), dim3(256), 0, s,
+                 src, 4 * H, H, WT);
+  }
+  const float* dY = dytop;
+  for (int l = lo.L - 1; l >= 0; --l) {
+    const T* Xl = l == 0 ? (const T*)(ws + lo.X0) : (const T*)(ws + lo.Y[l - 1]);
+    const int Dl = lo.layer_in(l), Dpl = lo.layer_in_pitch(l);
+    const T* Yl = l == lo.L - 1 ? ytop : (const T*)(ws + lo.Y[l]);
+    const T* Gl = (const T*)(ws + lo.G[l]);
+    const float* Cl = (const float*)(ws + lo.C[l]);
+    // BPTT over the chunk, both directions per launch
+    RecBwdArgs<T> rb;
+    rb.DA = DA; rb.WT0 = WT + (int64_t)(2 * l) * 4 * H * H; rb.WT1 = WT + (int64_t)(2 * l + 1) * 4 * H * H;
+    rb.DY = dY; rb.G = Gl; rb.C = Cl; rb.DC = DC; rb.Tn = Tn; rb.B = B; rb.H = H;
+    const dim3 grid(H / 16, (unsigned)cdiv(B, 16), 2);
+    for (int tau = 0; tau < Tn; ++tau) {
+      rb.tau = tau;
+      BLSTM_LAUNCH("lstm_rec_bwd", lstm_rec_bwd_step<T>, grid, dim3(256), 0, s, rb);
+    }
+    // dW_ih[d] = da_d^T X_l  (4H x D_l, reduction over all frames)
+    {
+      const Opnd A = opnd(DA, 8 * H, 4 * H, M, 4 * H);
+      const Opnd Bx = opnd(Xl, Dpl, Dpl, M);
+      gemm_f32<T, false, false, V, V>("gemm_dwih", s, A, Bx, 4 * H, Dl, M, 2, lo.sp_dWih[l],
+                                      grad + lo.Wih[l][0], Dl, lo.Wih[l][1] - lo.Wih[l][0], part);
+    }
+    // dW_hh[d] = sum_t da_d[t]^T h_d[t_prev]: frames shifted by one step, the
+    // forward direction pairing t with t-1 and the reverse direction t with t+1
+    {
+      const int64_t Kr = (int64_t)(Tn - 1) * B;
+      const Opnd A = opnd(DA + (int64_t)B * 8 * H, 8 * H, 4 * H, Kr, 4 * H - (int64_t)B * 8 * H);
+      const Opnd Bh = opnd(Yl, 2 * H, H, Kr, (int64_t)B * 2 * H + H);
+      gemm_f32<T, false, false, V, V>("gemm_dwhh", s, A, Bh, 4 * H, H, Kr, 2, lo.sp_dWhh,
+                                      grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part);
+    }
+    // db_ih = db_hh = sum over frames of da
+    colsum<T>("colsum_db", s, DA, M, 8 * H, 8 * H, csp, 4 * H, lo.bih[l][1] - lo.bih[l][0],
+              grad + lo.bih[l][0], grad + lo.bhh[l][0]);
+    // dX_l = sum_d da_d W_ih[d]  (the gradient reaching the layer below)
+    if (l > 0) {
+      const Opnd A = opnd(DA, 8 * H, 8 * H, M);
+      Opnd Bw = opnd(W + lo.Wih[l][0], Dl, Dl, 8 * H);
+      Bw.seg = 4 * H;
+      Bw.segstride = lo.Wih[l][1] - lo.Wih[l][0];
+      float* dst = (dY == (const float*)(ws + lo.DYa)) ? (float*)(ws + lo.DYb) : (float*)(ws + lo.DYa);
+      gemm_f32<T, true, false, V, V>("gemm_dx", s, A, Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst, Dl, 0,
+                                     part);
+      dY = dst;
+    }
+  }
+  return blstm_check_launch("blstm_bwd");
+}
+
+extern "C" int blstm_fwd(const blstm_dims* dims, const float* theta, const void* theta_lp,
+                         const float* x, void* act_ws, void* y_top, hipStream_t stream) {
+  Layout lo;
+  int rc = make_layout(dims, &lo);
+  if (rc) return rc;
+  if (!theta || !x || !act_ws || !y_top) return blstm_fail(BLSTM_EINVAL, "blstm_fwd: NULL pointer");
+  if (lo.prec == BLSTM_BF16) {
+    if (!theta_lp) return blstm_fail(BLSTM_EINVAL, "blstm_fwd: theta_lp is NULL (bf16)");
+    return fwd_impl<bf16>(lo, theta, (const bf16*)theta_lp, x, (char*)act_ws, (bf16*)y_top, stream);
+  }
+  return fwd_impl<float>(lo, theta, theta, x, (char*)act_ws, (float*)y_top, stream);
+}
+
+extern "C" int blstm_bwd(const blstm_dims* dims, const float* theta, const void* theta_lp,
+                         void* act_ws, const void* y_top, const float* dy_top, float* grad,
+                         hipStream_t stream) {
+  Layout lo;
+  int rc = make_layout(dims, &lo);
+  if (rc) return rc;
+  if (!theta || !act_ws || !y_top || !dy_top || !grad)
+    return blstm_fail(BLSTM_EINVAL, "blstm_bwd: NULL pointer");
+  if (lo.prec == BLSTM_BF16) {
+    if (!theta_lp) return blstm_fail(BLSTM_EINVAL, "blstm_bwd: theta_lp is NULL (bf16)");
+    return bwd_impl<bf16>(lo, (const bf16*)theta_lp, (char*)act_ws, (const bf16*)y_top, dy_top, grad,
+                          stream);
+  }
+  return bwd_impl<float>(lo, theta, (char*)act_ws, (const float*)y_top, dy_top, grad, stream);
+}
