@@ -39,8 +39,10 @@ def kernel_work(name, c, n_params):
     Dl = [D] + [2 * H] * (L - 1)
     if name == "gemm_gx":
         return "mfma", sum(2 * 2 * M * 4 * H * d for d in Dl), "flop", L
-    if name in ("lstm_rec_fwd", "lstm_rec_bwd"):
-        return "mfma", L * (T - 1) * 2 * 2 * B * 4 * H * H, "flop", L * T
+    if name in ("lstm_rec_fwd", "lstm_rec_bwd", "lstm_rec_fwd_persist", "lstm_rec_bwd_persist"):
+        # the recurrent products h_prev W_hh^T (forward) or da W_hh (BPTT);
+        # the first step of each direction has no previous state
+        return "mfma", L * (T - 1) * 2 * 2 * B * 4 * H * H, "flop", None
     if name == "gemm_dwih":
         return "mfma", sum(2 * 2 * 4 * H * d * M for d in Dl), "flop", L
     if name == "gemm_dwhh":
@@ -108,6 +110,8 @@ def main():
     ap.add_argument("--workload", default="full_b128")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="per-kernel times to stderr")
+    ap.add_argument("--mode", choices=("graph", "eager"), default="graph",
+                    help="replay the timed steps as one HIP graph, or launch them one by one")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one learner on one GPU; --gpus {args.gpus} is not supported "
@@ -133,7 +137,9 @@ def main():
     for _ in range(args.warmup):
         st.step(lr)
     torch.cuda.synchronize()
-    # find the dominant kernel on one extra untimed step
+    # find the dominant kernel on one extra untimed step, run the way the
+    # timed steps run (in graph mode: captured, with its event records, and
+    # replayed)
     bd.blstm_timing_begin("")
     st.step(lr)
     per = bd.blstm_timing_end()
@@ -147,22 +153,42 @@ def main():
     dominant = next(n for n, _ in ranked if kernel_work(n, cfg, st.n) is not None)
 
     # timed region: K steps, the dominant kernel bracketed by HIP events on
-    # the stream it runs on
-    torch.cuda.synchronize()
-    bd.blstm_timing_begin(dominant)
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        st.step(lr)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
+    # the stream it runs on.  In graph mode the K steps (with their event
+    # records) are captured once and replayed as one graph.
+    if args.mode == "graph":
+        warm = st.capture(lr, steps=1)
+        for _ in range(max(args.warmup, 1)):
+            warm.replay()
+        torch.cuda.synchronize()
+        graph = st.capture(lr, steps=args.steps)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        graph.replay()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+    else:
+        torch.cuda.synchronize()
+        bd.blstm_timing_begin(dominant)
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            st.step(lr)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+    if args.mode == "graph":
+        # event records inside a graph carry no timestamps: time the dominant
+        # kernel on eager steps right after the timed replay
+        bd.blstm_timing_begin(dominant)
+        for _ in range(args.steps):
+            st.step(lr)
+        torch.cuda.synchronize()
     dom = bd.blstm_timing_end()[dominant]
     loss = float(st.loss.cpu()[0])
 
     ms_per_step = elapsed * 1e3 / args.steps
     value = frames * args.steps / elapsed
-    bound, amount, unit, launches_per_step = kernel_work(dominant, cfg, st.n)
+    bound, amount, unit, _ = kernel_work(dominant, cfg, st.n)
     n_launch, total_ms = dom
-    per_launch = amount / launches_per_step
+    per_launch = amount * args.steps / n_launch
     avg_s = total_ms / n_launch / 1e3
     achieved = per_launch / avg_s / (1e9 if bound == "hbm" else 1e12)
     peak, punit = peak_for(bound, cfg["precision"])
@@ -174,7 +200,7 @@ def main():
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": cfg["precision"], "data": "synthetic",
-           "config": {"workload": args.workload, **shape, "frames_per_step": frames,
+           "config": {"workload": args.workload, **shape, "frames_per_step": frames, "mode": args.mode,
                       "params": st.n, "label_dist": cfg["label_dist"]},
            "loss_last_step": loss, "roofline": roofline}
     if not args.no_cpu_baseline:

@@ -112,6 +112,7 @@ int make_layout(const blstm_dims* d, Layout* lo) {
     if (L.sp_dX[l] > 1) skp = std::max(skp, (size_t)L.sp_dX[l] * M * Dl * 4);
   }
   L.SKP = a; a = align256(a + skp);
+  L.SYNC = a; a = align256(a + 64 * 32 * 4 + 256);   // barrier counters + status word
   L.act_bytes = a;
 
   // head_ws

@@ -20,7 +20,7 @@ PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libadpsgd_blstm.so")
-SOURCES = ["abi.hip", "update.hip", "lstm.hip", "head.hip"]
+SOURCES = ["abi.hip", "update.hip", "lstm.hip", "lstm_persist.hip", "head.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

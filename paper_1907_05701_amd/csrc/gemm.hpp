@@ -55,19 +55,51 @@ template <typename T> struct LdsPad { static constexpr int rows = 1; };
 template <> struct LdsPad<float> { static constexpr int rows = 4; };
 
 // Global -> register -> LDS staging of one operand tile.
-template <typename T, int BMN, int BK, int NT, bool KC, int VEC>
+//
+// K-contiguous operands (and every float32 operand) move in VEC-element
+// chunks.  MN-contiguous bf16 operands move in 8x8 blocks (8 k rows of 8
+// consecutive mn): each thread loads the block's 8 rows, transposes it in
+// registers (pairs of bf16 per dword) and writes 8 aligned 16-byte LDS rows,
+// so the LDS tile has the same [k/8][mn][8] layout in both cases.  Block b
+// goes to thread b (k group = b % (BK/8)), which spreads one store
+// instruction over all LDS banks.  TOFF rotates the thread numbering so two
+// transposed operands are staged by different halves of the workgroup.
+template <typename T, int BMN, int BK, int NT, bool KC, int VEC, int TOFF = 0>
 struct TileLoader {
   static constexpr int KPL = Mfma<T>::KPL;
   static constexpr int PADR = LdsPad<T>::rows;
+  static constexpr bool XPOSE = !KC && KPL == 8;
   typedef typename VecOf<VEC * (int)sizeof(T)>::type V;
   static constexpr int CPR = KC ? BK / VEC : BMN / VEC;   // chunks per global row
-  static constexpr int CH = KC ? BMN * CPR : BK * CPR;
-  static constexpr int PER = (CH + NT - 1) / NT;
+  static constexpr int CH = XPOSE ? (BK / 8) * (BMN / 8) * 8 : (KC ? BMN * CPR : BK * CPR);
+  static constexpr int NB = (BK / 8) * (BMN / 8);          // 8x8 blocks (XPOSE)
+  static constexpr int NA = NB < NT ? NB : NT;              // threads with a block
+  static constexpr int BPT = NB < NT ? 1 : NB / NT;         // blocks per thread
+  static constexpr int PER = XPOSE ? 8 * BPT : (CH + NT - 1) / NT;
   static_assert(KPL == 1 || VEC <= KPL || !KC, "bf16 K-contiguous chunk must fit a k-group");
+  static_assert(!XPOSE || (VEC == 8 && NB % NA == 0), "transposed staging needs 8-wide chunks");
   V r[PER];
 
   __device__ __forceinline__ void load(const Opnd& o, int z, int64_t mn0, int64_t k0,
                                        int64_t kend, int tid) {
+    if (XPOSE) {
+      const int t = (tid + TOFF) % NT;
+#pragma unroll
+      for (int p = 0; p < BPT; ++p) {
+        const int b = t + p * NA;
+        const int kg = b % (BK / 8), mc = b / (BK / 8);
+        const int64_t mn = mn0 + (int64_t)mc * 8;
+        const bool mnok = t < NA && mn + 8 <= o.ext;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int64_t k = k0 + kg * 8 + i;
+          V v = {};
+          if (mnok && k < kend && k < o.rows) v = *(const V*)(opnd_row<T>(o, z, k) + mn);
+          r[p * 8 + i] = v;
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int c = tid + p * NT;
@@ -88,6 +120,30 @@ struct TileLoader {
   }
 
   __device__ __forceinline__ void store(T* lds, int tid) const {
+    if (XPOSE) {
+      const int t = (tid + TOFF) % NT;
+      if (t >= NA) return;
+#pragma unroll
+      for (int p = 0; p < BPT; ++p) {
+        const int b = t + p * NA;
+        const int kg = b % (BK / 8), mc = b / (BK / 8);
+        const uint4* in = (const uint4*)&r[p * 8];
+        // out row j (mn = 8*mc + j) holds k = 8*kg .. 8*kg+7; dword w packs
+        // k = 2w (low half) and 2w+1 (high half)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          uint32_t o4[4];
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const uint32_t lo = ((const uint32_t*)&in[2 * w])[j / 2];
+            const uint32_t hi = ((const uint32_t*)&in[2 * w + 1])[j / 2];
+            o4[w] = (j & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+          }
+          *(uint4*)&lds[(kg * (BMN + PADR) + mc * 8 + j) * 8] = make_uint4(o4[0], o4[1], o4[2], o4[3]);
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int c = tid + p * NT;
@@ -104,13 +160,7 @@ struct TileLoader {
         }
       } else {
         const int ml = cc * VEC;
-        if (KPL == 8) {
-          const T* e = (const T*)&r[p];
-#pragma unroll
-          for (int i = 0; i < VEC; ++i) lds[((rr / 8) * (BMN + PADR) + ml + i) * 8 + (rr % 8)] = e[i];
-        } else {
-          *(V*)&lds[rr * (BMN + PADR) + ml] = r[p];
-        }
+        *(V*)&lds[rr * (BMN + PADR) + ml] = r[p];   // float32: [k][mn]
       }
     }
   }
@@ -145,8 +195,8 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const Opnd A, const 
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   if (ntiles > 0) {
-    TileLoader<T, BM, BK, NT, AKC, VA> la;
-    TileLoader<T, BN, BK, NT, BKC, VB> lb;
+    TileLoader<T, BM, BK, NT, AKC, VA, 0> la;
+    TileLoader<T, BN, BK, NT, BKC, VB, (!AKC && !BKC) ? NT / 2 : 0> lb;
     la.load(A, z, m0, kbeg, kend, tid);
     lb.load(B, z, n0, kbeg, kend, tid);
     la.store(&lds[0][0], tid);

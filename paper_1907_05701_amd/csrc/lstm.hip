@@ -17,8 +17,14 @@
 // fragments straight from global memory (the step's operands are small and
 // L2-resident) and combine their partial sums through LDS in a fixed order,
 // so the step is latency-bound rather than bandwidth-bound.
+#include <stdlib.h>
+#include <string.h>
+
+#include <type_traits>
+
 #include "common.hpp"
 #include "gemm.hpp"
+#include "lstm_persist.hpp"
 #include "reduce.hpp"
 
 template <typename T>
@@ -235,6 +241,35 @@ __global__ __launch_bounds__(256) void transpose_kernel(TransposeSrc src, int R,
 template <typename T> struct VecW { static constexpr int v = 8; };   // 16-byte chunks
 template <> struct VecW<float> { static constexpr int v = 4; };
 
+// The persistent kernels serve bf16 when the W_hh slice fits in LDS and the
+// stream is not being captured into a graph; the environment variable
+// ADPSGD_BLSTM_NO_PERSIST=1 forces the per-step kernels.
+template <typename T>
+static bool use_persistent(int H, hipStream_t s) {
+  if (!std::is_same<T, bf16>::value) return false;
+  // cooperative launches are not recorded into graphs: take the per-step
+  // kernels while the stream is being captured
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone) return false;
+  const char* env = getenv("ADPSGD_BLSTM_NO_PERSIST");
+  const bool off = env && atoi(env);
+  return !off && persist_supported(H);
+}
+
+static PersistArgs persist_args(const Layout& lo, const bf16* W, char* ws, int l) {
+  PersistArgs pa;
+  memset(&pa, 0, sizeof(pa));
+  pa.W = W;
+  pa.whh0 = lo.Whh[l][0];
+  pa.whh1 = lo.Whh[l][1];
+  pa.ctr = (unsigned*)(ws + lo.SYNC);
+  pa.status = (int*)(ws + lo.SYNC + PERSIST_CTR_BYTES);
+  pa.Tn = lo.T;
+  pa.B = lo.B;
+  pa.H = lo.H;
+  return pa;
+}
+
 template <typename T>
 static int fwd_impl(const Layout& lo, const float* theta, const T* W, const float* x, char* ws,
                     T* ytop, hipStream_t s) {
@@ -264,6 +299,12 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
       gemm_launch<T, true, true, V, V>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
     else
       gemm_launch<T, true, true, V, 4>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
+    if (use_persistent<T>(H, s)) {
+      PersistArgs pa = persist_args(lo, (const bf16*)W, ws, l);
+      pa.Y = (bf16*)Yl; pa.Gx = (const bf16*)GX; pa.C = Cl; pa.G = (bf16*)Gl;
+      if (persist_layer(false, pa, s) == hipSuccess) continue;
+      (void)hipGetLastError();   // cooperative launch refused: take the per-step path
+    }
     RecFwdArgs<T> ra;
     ra.Y = Yl; ra.Whh0 = W + lo.Whh[l][0]; ra.Whh1 = W + lo.Whh[l][1]; ra.Gx = GX; ra.C = Cl;
     ra.G = Gl; ra.Tn = lo.T; ra.B = B; ra.H = H;
@@ -287,7 +328,8 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
   float* DC = (float*)(ws + lo.DC);
   float* part = (float*)(ws + lo.SKP);
   float* csp = (float*)(ws + lo.CSP);
-  {
+  bool have_wt = false;   // W_hh^T copies for the per-step kernels, made on first use
+  auto make_wt = [&]() {
     TransposeSrc src;
     for (int i = 0; i < 2 * MAX_LAYERS; ++i) src.p[i] = nullptr;
     for (int l = 0; l < lo.L; ++l)
@@ -295,7 +337,8 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     BLSTM_LAUNCH("transpose_whh", transpose_kernel<T>,
                  dim3((unsigned)cdiv(H, 32), (unsigned)cdiv(4 * H, 32), 2 * lo.L), dim3(256), 0, s,
                  src, 4 * H, H, WT);
-  }
+    have_wt = true;
+  };
   const float* dY = dytop;
   for (int l = lo.L - 1; l >= 0; --l) {
     const T* Xl = l == 0 ? (const T*)(ws + lo.X0) : (const T*)(ws + lo.Y[l - 1]);
@@ -303,14 +346,24 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     const T* Yl = l == lo.L - 1 ? ytop : (const T*)(ws + lo.Y[l]);
     const T* Gl = (const T*)(ws + lo.G[l]);
     const float* Cl = (const float*)(ws + lo.C[l]);
-    // BPTT over the chunk, both directions per launch
-    RecBwdArgs<T> rb;
-    rb.DA = DA; rb.WT0 = WT + (int64_t)(2 * l) * 4 * H * H; rb.WT1 = WT + (int64_t)(2 * l + 1) * 4 * H * H;
-    rb.DY = dY; rb.G = Gl; rb.C = Cl; rb.DC = DC; rb.Tn = Tn; rb.B = B; rb.H = H;
-    const dim3 grid(H / 16, (unsigned)cdiv(B, 16), 2);
-    for (int tau = 0; tau < Tn; ++tau) {
-      rb.tau = tau;
-      BLSTM_LAUNCH("lstm_rec_bwd", lstm_rec_bwd_step<T>, grid, dim3(256), 0, s, rb);
+    // BPTT over the chunk, both directions at once
+    bool done = false;
+    if (use_persistent<T>(H, s)) {
+      PersistArgs pa = persist_args(lo, (const bf16*)W, ws, l);
+      pa.DA = (bf16*)DA; pa.DY = dY; pa.C = (float*)Cl; pa.G = (bf16*)Gl;
+      done = persist_layer(true, pa, s) == hipSuccess;
+      if (!done) (void)hipGetLastError();
+    }
+    if (!done) {
+      if (!have_wt) make_wt();
+      RecBwdArgs<T> rb;
+      rb.DA = DA; rb.WT0 = WT + (int64_t)(2 * l) * 4 * H * H; rb.WT1 = WT + (int64_t)(2 * l + 1) * 4 * H * H;
+      rb.DY = dY; rb.G = Gl; rb.C = Cl; rb.DC = DC; rb.Tn = Tn; rb.B = B; rb.H = H;
+      const dim3 grid(H / 16, (unsigned)cdiv(B, 16), 2);
+      for (int tau = 0; tau < Tn; ++tau) {
+        rb.tau = tau;
+        BLSTM_LAUNCH("lstm_rec_bwd", lstm_rec_bwd_step<T>, grid, dim3(256), 0, s, rb);
+      }
     }
     // dW_ih[d] = da_d^T X_l  (4H x D_l, reduction over all frames)
     {

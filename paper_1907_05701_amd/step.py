@@ -79,3 +79,12 @@ class LearnerStep:
         """The whole learner step: gradient, then the fused update."""
         self.gradient()
         self.update(lr, flags)
+
+    def capture(self, lr, steps=1, flags=0):
+        """Record `steps` learner steps into a HIP graph (replaying it runs
+        them again on the current buffers, i.e. continues training)."""
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(steps):
+                self.step(lr, flags)
+        return graph

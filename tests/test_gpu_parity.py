@@ -121,6 +121,22 @@ def test_full_model_dims_fp32_b8(gpu_lib):
                          dist="zipf", check_update=False)
 
 
+@pytest.mark.parametrize("B", [200, 300, 1100], ids=["mb2", "mb4", "mb8_two_chunks"])
+def test_recurrence_batch_regimes_bf16(gpu_lib, B):
+    """Batches large enough that each recurrent workgroup covers 2, 4 or 8
+    row blocks, and (B=1100) that the batch is processed in two chunks."""
+    run_step_and_compare(dict(L=1, D=40, H=512, P=32, K=50, T=3, B=B), "bf16", BF16_TOL, seed=11,
+                         check_update=False)
+
+
+def test_per_step_recurrence_path_bf16(gpu_lib, monkeypatch):
+    """The per-step recurrent kernels (used when the persistent ones do not
+    apply) on the full layer widths."""
+    monkeypatch.setenv("ADPSGD_BLSTM_NO_PERSIST", "1")
+    run_step_and_compare(dict(L=2, D=260, H=512, P=256, K=1000, T=6, B=24), "bf16", BF16_TOL, seed=12,
+                         check_update=False)
+
+
 # ------------------------------------------------------------ the update ---
 
 @pytest.mark.parametrize("flags", [0, 1, 2, 3])
@@ -226,7 +242,7 @@ def test_head_alone_on_given_hidden_states(gpu_lib, prec, tol):
     blocks, _ = ref.param_layout(dims)
     for key in ("W_l", "b_l", "W_s", "b_s"):
         off, shp = blocks[key]
-        assert rel(g[off:off + int(np.prod(shp))], grads[key]) <= tol, key
+        assert rel(g[off:off + int(np.prod(shp))], grads[key].reshape(-1)) <= tol, key
 
 
 def test_deterministic_across_runs(gpu_lib):
@@ -259,6 +275,38 @@ def test_timing_hooks_report_kernels(gpu_lib):
     bd.blstm_timing_begin("lstm_rec")
     st.gradient()
     got = bd.blstm_timing_end()
-    assert set(got) == {"lstm_rec_fwd", "lstm_rec_bwd"}
-    assert got["lstm_rec_fwd"][0] == 4 and got["lstm_rec_bwd"][0] == 4
+    assert set(got) == {"lstm_rec_fwd_persist", "lstm_rec_bwd_persist"}
+    assert got["lstm_rec_fwd_persist"][0] == 1 and got["lstm_rec_bwd_persist"][0] == 1
     assert all(v[1] > 0 for v in got.values())
+
+
+def test_graph_replays_match_eager_steps(gpu_lib, monkeypatch):
+    """A captured learner step replayed several times, with eager work and
+    synchronisation in between, gives bit-identical results to the same
+    number of eagerly launched steps (both on the per-step recurrent kernels,
+    which is what a captured step uses)."""
+    from paper_1907_05701_amd.step import LearnerStep
+    monkeypatch.setenv("ADPSGD_BLSTM_NO_PERSIST", "1")
+    shape = dict(L=2, D=260, H=128, P=64, K=3000, T=7, B=40)
+    dims = ref.Dims(**shape)
+    n = ref.param_count(dims)
+    theta = inputs.params(n)
+    x = inputs.features(dims.T, dims.B, dims.D)
+    lab = inputs.labels(dims.T, dims.B, dims.K, dist="zipf")
+    peer = inputs.peer(theta)
+    eager = LearnerStep(**shape, precision="bf16")
+    eager.load(theta, x, lab, peer)
+    replayed = LearnerStep(**shape, precision="bf16")
+    replayed.load(theta, x, lab, peer)
+    graph = replayed.capture(0.05)
+    torch.cuda.synchronize()
+    replayed.load(theta, x, lab, peer)          # capture ran nothing; start from the same state
+    for i in range(3):
+        eager.step(0.05)
+        graph.replay()
+        torch.cuda.synchronize()
+        _ = (eager.theta * 2.0).sum().item()       # unrelated eager work between replays
+        np.testing.assert_array_equal(replayed.theta.cpu().numpy(), eager.theta.cpu().numpy())
+        np.testing.assert_array_equal(replayed.loss.cpu().numpy(), eager.loss.cpu().numpy())
+        np.testing.assert_array_equal(replayed.grad.cpu().numpy(), eager.grad.cpu().numpy())
+        say(f"[graph] replay {i} matches, loss {float(eager.loss.cpu()[0]):.6f}")
