@@ -10,6 +10,7 @@
 
 #include "common.hpp"
 #include "gemm.hpp"
+#include "lstm_persist.hpp"
 
 static thread_local char g_err[512] = "";
 
@@ -112,7 +113,8 @@ int make_layout(const blstm_dims* d, Layout* lo) {
     if (L.sp_dX[l] > 1) skp = std::max(skp, (size_t)L.sp_dX[l] * M * Dl * 4);
   }
   L.SKP = a; a = align256(a + skp);
-  L.SYNC = a; a = align256(a + 64 * 32 * 4 + 256);   // barrier counters + status word
+  L.SYNC = a; a = align256(a + 256);                            // status word
+  L.XCH = a; a = align256(a + persist_xch_bytes(d->B, d->H));   // recurrent step exchange
   L.act_bytes = a;
 
   // head_ws

@@ -73,7 +73,7 @@ struct Layout {
   int64_t Wih[MAX_LAYERS][2], Whh[MAX_LAYERS][2], bih[MAX_LAYERS][2], bhh[MAX_LAYERS][2];
   int64_t Wl, bl, Ws, bs;
   // act_ws byte offsets
-  size_t X0, Y[MAX_LAYERS], G[MAX_LAYERS], C[MAX_LAYERS], GX, DYa, DYb, DC, WT, CSP, SKP, SYNC;
+  size_t X0, Y[MAX_LAYERS], G[MAX_LAYERS], C[MAX_LAYERS], GX, DYa, DYb, DC, WT, CSP, SKP, SYNC, XCH;
   size_t act_bytes;
   // head_ws byte offsets
   size_t Z, S, RL, DZ, DZT, HCSP, HSKP;

@@ -40,6 +40,13 @@ __device__ __forceinline__ float load_frag<float>(const float* p) {
 
 // --------------------------------------------------------------------------
 // Forward recurrent step.
+//
+// Workgroup (unit block q of 16 units, row block of 16*MBK rows, direction).
+// Wave w takes m-block w % MBK and the k-part w / MBK of the reduction; all
+// of its global loads (W_hh and h_prev fragments, and for the epilogue waves
+// the input projection and c_prev) are issued before any arithmetic, so a
+// step costs one memory round trip.  Partial sums of the k-parts meet in LDS
+// in a fixed order.
 // --------------------------------------------------------------------------
 template <typename T>
 struct RecFwdArgs {
@@ -52,32 +59,50 @@ struct RecFwdArgs {
   int Tn, B, H, tau;
 };
 
-template <typename T>
+template <typename T, int MBK>
 __global__ __launch_bounds__(256) void lstm_rec_fwd_step(const RecFwdArgs<T> a) {
   typedef Mfma<T> MT;
+  constexpr int KP = 4 / MBK;
   const int q = blockIdx.x, rb = blockIdx.y, d = blockIdx.z;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int mb = w % MBK, kp = w / MBK;
   const int H = a.H, B = a.B;
   const int t = d ? a.Tn - 1 - a.tau : a.tau;
   const int tp = d ? t + 1 : t - 1;
+  const int u = q * 16 + (lane & 15);
+  const bool epi = kp == 0;
+
+  // epilogue operands first: they do not depend on the reduction
+  float gx[4][4], cp[4];
+  if (epi) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      int b = rb * 16 * MBK + mb * 16 + (lane >> 4) * 4 + r;
+      b = b < B ? b : 0;
+      const T* p = a.Gx + ((int64_t)t * B + b) * 8 * H + (int64_t)d * 4 * H + u;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) gx[r][g] = to_f32(p[g * H]);
+      cp[r] = a.tau > 0 ? a.C[((int64_t)tp * B + b) * 2 * H + (int64_t)d * H + u] : 0.f;
+    }
+  }
+
   f32x4 acc[4];
 #pragma unroll
   for (int g = 0; g < 4; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
-
   if (a.tau > 0) {
     const T* Wd = d ? a.Whh1 : a.Whh0;
-    const int bl = rb * 16 + (lane & 15);
+    const int bl = rb * 16 * MBK + mb * 16 + (lane & 15);
     const bool rowok = bl < B;
     const T* arow = a.Y + ((int64_t)tp * B + (rowok ? bl : 0)) * 2 * H + (int64_t)d * H;
     const T* brow[4];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) brow[g] = Wd + ((int64_t)g * H + q * 16 + (lane & 15)) * H;
+    for (int g = 0; g < 4; ++g) brow[g] = Wd + ((int64_t)g * H + u) * H;
     const int koff = (lane >> 4) * MT::KPL;
     const int nks = H / MT::KSTEP;
-#pragma unroll 4
-    for (int ks = w; ks < nks; ks += 4) {
+#pragma unroll 8
+    for (int ks = kp; ks < nks; ks += KP) {
       const int k = ks * MT::KSTEP + koff;
-      typename MT::frag af = rowok ? load_frag<T>(arow + k) : MT::zero();
+      const typename MT::frag af = rowok ? load_frag<T>(arow + k) : MT::zero();
       typename MT::frag bf[4];
 #pragma unroll
       for (int g = 0; g < 4; ++g) bf[g] = load_frag<T>(brow[g] + k);
@@ -86,32 +111,26 @@ __global__ __launch_bounds__(256) void lstm_rec_fwd_step(const RecFwdArgs<T> a) 
     }
   }
 
-  __shared__ f32x4 red[3][4][64];
-  if (w > 0) {
+  __shared__ f32x4 red[KP - 1][MBK][4][64];
+  if (!epi) {
 #pragma unroll
-    for (int g = 0; g < 4; ++g) red[w - 1][g][lane] = acc[g];
+    for (int g = 0; g < 4; ++g) red[kp - 1][mb][g][lane] = acc[g];
   }
   __syncthreads();
-  if (w != 0) return;
+  if (!epi) return;
 #pragma unroll
-  for (int ww = 0; ww < 3; ++ww)
+  for (int j = 0; j < KP - 1; ++j)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) acc[g] += red[ww][g][lane];
+    for (int g = 0; g < 4; ++g) acc[g] += red[j][mb][g][lane];
 
-  const int u = q * 16 + (lane & 15);
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const int b = rb * 16 + (lane >> 4) * 4 + r;
+    const int b = rb * 16 * MBK + mb * 16 + (lane >> 4) * 4 + r;
     if (b >= B) continue;
     const int64_t row = (int64_t)t * B + b;
-    const T* gx = a.Gx + row * 8 * H + (int64_t)d * 4 * H + u;
-    const float ai = acc[0][r] + to_f32(gx[0]);
-    const float af = acc[1][r] + to_f32(gx[H]);
-    const float ag = acc[2][r] + to_f32(gx[2 * H]);
-    const float ao = acc[3][r] + to_f32(gx[3 * H]);
-    const float ig = sigmoidf_(ai), fg = sigmoidf_(af), gg = tanhf_(ag), og = sigmoidf_(ao);
-    const float cp = a.tau > 0 ? a.C[((int64_t)tp * B + b) * 2 * H + (int64_t)d * H + u] : 0.f;
-    const float c = fg * cp + ig * gg;
+    const float ig = sigmoidf_(acc[0][r] + gx[r][0]), fg = sigmoidf_(acc[1][r] + gx[r][1]);
+    const float gg = tanhf_(acc[2][r] + gx[r][2]), og = sigmoidf_(acc[3][r] + gx[r][3]);
+    const float c = fg * cp[r] + ig * gg;
     const float h = og * tanhf_(c);
     a.C[row * 2 * H + (int64_t)d * H + u] = c;
     a.Y[row * 2 * H + (int64_t)d * H + u] = from_f32<T>(h);
@@ -124,7 +143,8 @@ __global__ __launch_bounds__(256) void lstm_rec_fwd_step(const RecFwdArgs<T> a) 
 }
 
 // --------------------------------------------------------------------------
-// Backward recurrent step (BPTT).
+// Backward recurrent step (BPTT), same workgroup shape and load schedule:
+// dh_rec = da_next W_hh for 16 units, then the gate derivatives.
 // --------------------------------------------------------------------------
 template <typename T>
 struct RecBwdArgs {
@@ -138,59 +158,74 @@ struct RecBwdArgs {
   int Tn, B, H, tau;
 };
 
-template <typename T>
+template <typename T, int MBK>
 __global__ __launch_bounds__(256) void lstm_rec_bwd_step(const RecBwdArgs<T> a) {
   typedef Mfma<T> MT;
+  constexpr int KP = 4 / MBK;
   const int q = blockIdx.x, rb = blockIdx.y, d = blockIdx.z;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int mb = w % MBK, kp = w / MBK;
   const int H = a.H, B = a.B, Tn = a.Tn;
   const int t = d ? a.tau : Tn - 1 - a.tau;
   const int tn = d ? t - 1 : t + 1;   // processed just before t in this pass
   const int tp = d ? t + 1 : t - 1;   // forward-pass predecessor of t
-  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int u = q * 16 + (lane & 15);
+  const bool epi = kp == 0;
 
+  float dy[4], gt[4][4], cc[4], cpv[4], dcn[4];
+  if (epi) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      int b = rb * 16 * MBK + mb * 16 + (lane >> 4) * 4 + r;
+      b = b < B ? b : 0;
+      const int64_t row = (int64_t)t * B + b;
+      dy[r] = a.DY[row * 2 * H + (int64_t)d * H + u];
+      const T* gs = a.G + row * 8 * H + (int64_t)d * 4 * H + u;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) gt[r][g] = to_f32(gs[g * H]);
+      cc[r] = a.C[row * 2 * H + (int64_t)d * H + u];
+      cpv[r] = (tp >= 0 && tp < Tn) ? a.C[((int64_t)tp * B + b) * 2 * H + (int64_t)d * H + u] : 0.f;
+      dcn[r] = a.tau > 0 ? a.DC[((int64_t)d * B + b) * H + u] : 0.f;
+    }
+  }
+
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
   if (a.tau > 0) {
     const T* WT = d ? a.WT1 : a.WT0;
-    const int bl = rb * 16 + (lane & 15);
+    const int bl = rb * 16 * MBK + mb * 16 + (lane & 15);
     const bool rowok = bl < B;
     const T* arow = a.DA + ((int64_t)tn * B + (rowok ? bl : 0)) * 8 * H + (int64_t)d * 4 * H;
-    const T* brow = WT + ((int64_t)q * 16 + (lane & 15)) * 4 * H;
+    const T* brow = WT + (int64_t)u * 4 * H;
     const int koff = (lane >> 4) * MT::KPL;
     const int nks = 4 * H / MT::KSTEP;
-#pragma unroll 4
-    for (int ks = w; ks < nks; ks += 4) {
+#pragma unroll 16
+    for (int ks = kp; ks < nks; ks += KP) {
       const int k = ks * MT::KSTEP + koff;
-      typename MT::frag af = rowok ? load_frag<T>(arow + k) : MT::zero();
+      const typename MT::frag af = rowok ? load_frag<T>(arow + k) : MT::zero();
       acc = MT::mma(af, load_frag<T>(brow + k), acc);
     }
   }
 
-  __shared__ f32x4 red[3][64];
-  if (w > 0) red[w - 1][lane] = acc;
+  __shared__ f32x4 red[KP - 1][MBK][64];
+  if (!epi) red[kp - 1][mb][lane] = acc;
   __syncthreads();
-  if (w != 0) return;
+  if (!epi) return;
 #pragma unroll
-  for (int ww = 0; ww < 3; ++ww) acc += red[ww][lane];
+  for (int j = 0; j < KP - 1; ++j) acc += red[j][mb][lane];
 
-  const int u = q * 16 + (lane & 15);
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const int b = rb * 16 + (lane >> 4) * 4 + r;
+    const int b = rb * 16 * MBK + mb * 16 + (lane >> 4) * 4 + r;
     if (b >= B) continue;
     const int64_t row = (int64_t)t * B + b;
-    const float dh = acc[r] + a.DY[row * 2 * H + (int64_t)d * H + u];
-    const T* gs = a.G + row * 8 * H + (int64_t)d * 4 * H + u;
-    const float ig = to_f32(gs[0]), fg = to_f32(gs[H]), gg = to_f32(gs[2 * H]), og = to_f32(gs[3 * H]);
-    const float c = a.C[row * 2 * H + (int64_t)d * H + u];
-    const float cp = (tp >= 0 && tp < Tn) ? a.C[((int64_t)tp * B + b) * 2 * H + (int64_t)d * H + u] : 0.f;
-    float* dcp = a.DC + ((int64_t)d * B + b) * H + u;
-    const float dcn = a.tau > 0 ? *dcp : 0.f;
-    const float tc = tanhf_(c);
-    const float dc = dh * og * (1.f - tc * tc) + dcn;
-    *dcp = dc * fg;
+    const float ig = gt[r][0], fg = gt[r][1], gg = gt[r][2], og = gt[r][3];
+    const float dh = acc[r] + dy[r];
+    const float tc = tanhf_(cc[r]);
+    const float dc = dh * og * (1.f - tc * tc) + dcn[r];
+    a.DC[((int64_t)d * B + b) * H + u] = dc * fg;
     T* da = a.DA + row * 8 * H + (int64_t)d * 4 * H + u;
     da[0] = from_f32<T>(dc * gg * ig * (1.f - ig));
-    da[H] = from_f32<T>(dc * cp * fg * (1.f - fg));
+    da[H] = from_f32<T>(dc * cpv[r] * fg * (1.f - fg));
     da[2 * H] = from_f32<T>(dc * ig * (1.f - gg * gg));
     da[3 * H] = from_f32<T>(dh * tc * og * (1.f - og));
   }
@@ -241,19 +276,29 @@ __global__ __launch_bounds__(256) void transpose_kernel(TransposeSrc src, int R,
 template <typename T> struct VecW { static constexpr int v = 8; };   // 16-byte chunks
 template <> struct VecW<float> { static constexpr int v = 4; };
 
-// The persistent kernels serve bf16 when the W_hh slice fits in LDS and the
-// stream is not being captured into a graph; the environment variable
-// ADPSGD_BLSTM_NO_PERSIST=1 forces the per-step kernels.
+// Per-step kernels take 32 rows per workgroup when that still gives at least
+// one workgroup per compute unit (W_hh is then read half as often); this
+// pays off in the forward step only (measured on MI355X).
+static bool step_rows_32(int H, int B) { return (int64_t)(H / 16) * cdiv(B, 32) * 2 >= 256; }
+
+// Which recurrent kernels run.  Default (measured fastest on MI355X at the
+// paper's shapes): the persistent kernel for the forward pass and the
+// per-step kernels for BPTT.  ADPSGD_BLSTM_RECURRENCE=persistent uses the
+// persistent kernels for both passes, =per-step (or ADPSGD_BLSTM_NO_PERSIST=1)
+// none.  The persistent kernels need bf16, a W_hh slice that fits in LDS and
+// a stream that is not being captured into a graph (cooperative launches
+// are not recorded).
 template <typename T>
-static bool use_persistent(int H, hipStream_t s) {
+static bool use_persistent(int H, int steps, bool backward, hipStream_t s) {
   if (!std::is_same<T, bf16>::value) return false;
-  // cooperative launches are not recorded into graphs: take the per-step
-  // kernels while the stream is being captured
+  const char* off = getenv("ADPSGD_BLSTM_NO_PERSIST");
+  if (off && atoi(off)) return false;
+  const char* pol = getenv("ADPSGD_BLSTM_RECURRENCE");
+  if (pol && strcmp(pol, "per-step") == 0) return false;
+  if (backward && !(pol && strcmp(pol, "persistent") == 0)) return false;
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
   if (hipStreamIsCapturing(s, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone) return false;
-  const char* env = getenv("ADPSGD_BLSTM_NO_PERSIST");
-  const bool off = env && atoi(env);
-  return !off && persist_supported(H);
+  return persist_supported(H, steps);
 }
 
 static PersistArgs persist_args(const Layout& lo, const bf16* W, char* ws, int l) {
@@ -262,8 +307,8 @@ static PersistArgs persist_args(const Layout& lo, const bf16* W, char* ws, int l
   pa.W = W;
   pa.whh0 = lo.Whh[l][0];
   pa.whh1 = lo.Whh[l][1];
-  pa.ctr = (unsigned*)(ws + lo.SYNC);
-  pa.status = (int*)(ws + lo.SYNC + PERSIST_CTR_BYTES);
+  pa.X = (uint64_t*)(ws + lo.XCH);
+  pa.status = (int*)(ws + lo.SYNC);
   pa.Tn = lo.T;
   pa.B = lo.B;
   pa.H = lo.H;
@@ -299,7 +344,7 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
       gemm_launch<T, true, true, V, V>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
     else
       gemm_launch<T, true, true, V, 4>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
-    if (use_persistent<T>(H, s)) {
+    if (use_persistent<T>(H, lo.T, false, s)) {
       PersistArgs pa = persist_args(lo, (const bf16*)W, ws, l);
       pa.Y = (bf16*)Yl; pa.Gx = (const bf16*)GX; pa.C = Cl; pa.G = (bf16*)Gl;
       if (persist_layer(false, pa, s) == hipSuccess) continue;
@@ -308,10 +353,14 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
     RecFwdArgs<T> ra;
     ra.Y = Yl; ra.Whh0 = W + lo.Whh[l][0]; ra.Whh1 = W + lo.Whh[l][1]; ra.Gx = GX; ra.C = Cl;
     ra.G = Gl; ra.Tn = lo.T; ra.B = B; ra.H = H;
-    const dim3 grid(H / 16, (unsigned)cdiv(B, 16), 2);
+    const bool two = step_rows_32(H, B);
+    const dim3 grid(H / 16, (unsigned)cdiv(B, two ? 32 : 16), 2);
     for (int tau = 0; tau < lo.T; ++tau) {
       ra.tau = tau;
-      BLSTM_LAUNCH("lstm_rec_fwd", lstm_rec_fwd_step<T>, grid, dim3(256), 0, s, ra);
+      if (two)
+        BLSTM_LAUNCH("lstm_rec_fwd", (lstm_rec_fwd_step<T, 2>), grid, dim3(256), 0, s, ra);
+      else
+        BLSTM_LAUNCH("lstm_rec_fwd", (lstm_rec_fwd_step<T, 1>), grid, dim3(256), 0, s, ra);
     }
   }
   return blstm_check_launch("blstm_fwd");
@@ -348,7 +397,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     const float* Cl = (const float*)(ws + lo.C[l]);
     // BPTT over the chunk, both directions at once
     bool done = false;
-    if (use_persistent<T>(H, s)) {
+    if (use_persistent<T>(H, lo.T, true, s)) {
       PersistArgs pa = persist_args(lo, (const bf16*)W, ws, l);
       pa.DA = (bf16*)DA; pa.DY = dY; pa.C = (float*)Cl; pa.G = (bf16*)Gl;
       done = persist_layer(true, pa, s) == hipSuccess;
@@ -362,7 +411,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       const dim3 grid(H / 16, (unsigned)cdiv(B, 16), 2);
       for (int tau = 0; tau < Tn; ++tau) {
         rb.tau = tau;
-        BLSTM_LAUNCH("lstm_rec_bwd", lstm_rec_bwd_step<T>, grid, dim3(256), 0, s, rb);
+        BLSTM_LAUNCH("lstm_rec_bwd", (lstm_rec_bwd_step<T, 1>), grid, dim3(256), 0, s, rb);
       }
     }
     // dW_ih[d] = da_d^T X_l  (4H x D_l, reduction over all frames)

@@ -7,59 +7,100 @@
 // hidden units (two blocks of 16).  Its four waves are (unit block, half):
 // the half splits the reduction dimension when MB == 1 and the m-blocks
 // otherwise.  Per step a member
-//   forward : reads h_prev of its slice (all H units) from global memory,
-//             multiplies by its LDS-resident W_hh rows (4 gates x 32 units),
-//             adds the precomputed input projection and applies the cell;
-//             c stays in registers, h/c/gates are written for BPTT;
-//   backward: reads da of the previously processed step (all 4H gate
+//   forward : gathers h_prev of its slice (all H units), multiplies by its
+//             LDS-resident W_hh rows (4 gates x 32 units), adds the
+//             precomputed input projection and applies the cell; c stays in
+//             registers, h/c/gates are written for BPTT;
+//   backward: gathers da of the previously processed step (all 4H gate
 //             columns), multiplies by its LDS-resident W_hh columns to get
 //             dh_rec for its units, applies the gate derivatives (dc stays in
 //             registers) and writes da of this step.
-// Steps are separated by a per-group barrier: each wave drains its stores,
-// one thread per workgroup issues an agent-scope release fence and an atomic
-// arrival, and one thread spins (bounded) on the group counter and issues the
-// agent-scope acquire fence before the workgroup barrier releases the rest.  The launch is cooperative, so
-// all workgroups are co-resident; the spin bound only guarantees that every
-// wave exits even if that guarantee were broken (the status word is set).
-// Group g's members are workgroups g, g+NG, g+2NG, ... with NG a multiple of
-// 8, which keeps a group on one XCD when workgroups are dealt round-robin.
+//
+// Step-to-step exchange without barriers or cache maintenance.  The values
+// one member needs from the others (h, or da) are also published in an
+// exchange buffer as 8-byte words holding two bf16 values and the step
+// number + 1, written and read with agent-scope relaxed atomic stores and
+// loads.  Atomic accesses to one location are coherent across the whole
+// GPU, so a reader that sees the expected step number in a word also sees
+// that word's payload; readers simply poll the words they need (bounded; the
+// status word is set if a poll ever gives up).  Two slots alternate by step
+// parity: a member overwrites a slot only after it has consumed the next
+// step from every member, which those members produce only after they have
+// consumed the slot's current contents.  The buffer is cleared before each
+// launch, so no word from an earlier launch can carry a valid step number.
+// The launch is cooperative, so every member of a group is resident.
 #include "common.hpp"
 #include "lstm_persist.hpp"
 
 #define PU 32
-#define SPIN_LIMIT (1u << 22)
-#define CTR_STRIDE 32
+#define SPIN_LIMIT (1u << 18)
 
-// Arrival: every wave first waits until its own stores are complete at the
-// L2, the workgroup barrier joins the waves, and one thread then makes the
-// workgroup's writes visible at agent scope and counts the arrival.
-__device__ __forceinline__ void group_arrive(unsigned* ctr) {
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
+__device__ __forceinline__ uint64_t ll_load(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Wait: one thread spins on the counter, then invalidates this CU's caches
-// at agent scope before the barrier releases the other waves to read.
-__device__ __forceinline__ void group_wait(unsigned* ctr, unsigned target, int* status) {
-  if (threadIdx.x == 0) {
-    unsigned it = 0;
-    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-      __builtin_amdgcn_s_sleep(1);
-      if (++it > SPIN_LIMIT) {
-        __hip_atomic_store(status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        break;
-      }
+__device__ __forceinline__ void ll_store(uint64_t* p, uint32_t payload, uint32_t flag) {
+  __hip_atomic_store(p, ((uint64_t)flag << 32) | payload, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// two bf16 values in one dword, `lo` in the low half
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (bf16)lo) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)hi) << 16);
+}
+
+// MFMA A-fragments for k-steps ks0 .. ks0+nk-1 (nk <= KC) of MBW m-blocks,
+// gathered from exchange rows rp[m] (nullptr: row outside the batch, zeros).
+// Lane l takes row l % 16 and 8 k values = 4 words at word (ks*16 + (l/16)*4).
+template <int MBW, int KC>
+__device__ __forceinline__ void ll_fragments(const uint64_t* const (&rp)[MBW], int ks0, int nk,
+                                             uint32_t flag, int lane, bf16x8 (&af)[MBW][KC],
+                                             int* status) {
+  uint64_t w[MBW][KC][4];
+  const int woff = (lane >> 4) * 4;
+#pragma unroll
+  for (int m = 0; m < MBW; ++m)
+#pragma unroll
+    for (int kk = 0; kk < KC; ++kk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        w[m][kk][i] = (rp[m] && kk < nk) ? ll_load(rp[m] + (ks0 + kk) * 16 + woff + i)
+                                         : ((uint64_t)flag << 32);
+  for (unsigned it = 0;; ++it) {
+    bool bad = false;
+#pragma unroll
+    for (int m = 0; m < MBW; ++m)
+#pragma unroll
+      for (int kk = 0; kk < KC; ++kk)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) bad |= (uint32_t)(w[m][kk][i] >> 32) != flag;
+    if (!bad) break;
+    // give up after SPIN_LIMIT polls, or at once when any lane anywhere has
+    // given up before (then every later poll returns immediately too)
+    if (it > SPIN_LIMIT ||
+        ((it & 63) == 63 && __hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
+      __hip_atomic_store(status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      break;
     }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+    for (int m = 0; m < MBW; ++m)
+#pragma unroll
+      for (int kk = 0; kk < KC; ++kk)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if ((uint32_t)(w[m][kk][i] >> 32) != flag)
+            w[m][kk][i] = ll_load(rp[m] + (ks0 + kk) * 16 + woff + i);
   }
-  __syncthreads();
+#pragma unroll
+  for (int m = 0; m < MBW; ++m)
+#pragma unroll
+    for (int kk = 0; kk < KC; ++kk) {
+      const uint4 v = make_uint4((uint32_t)w[m][kk][0], (uint32_t)w[m][kk][1], (uint32_t)w[m][kk][2],
+                                 (uint32_t)w[m][kk][3]);
+      af[m][kk] = __builtin_bit_cast(bf16x8, v);
+    }
 }
-
-__device__ __forceinline__ bf16x8 ld16(const bf16* p) { return *(const bf16x8*)p; }
 
 // 8x8 bf16 transpose: in[i] holds row i (8 values); out[j] gets column j.
 __device__ __forceinline__ void transpose8x8(const uint4 (&in)[8], uint4 (&out)[8]) {
@@ -84,9 +125,10 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
   extern __shared__ __attribute__((aligned(16))) bf16 lds[];
   constexpr bool KSPLIT = MB == 1;
   constexpr int MBW = KSPLIT ? 1 : MB / 2;
+  constexpr int KC = MBW >= 4 ? 1 : 4 / MBW;   // k-steps gathered per poll
   constexpr int LDN = 128 + 1;   // LDS rows per k-group (128 gate rows + pad)
   const int H = a.H, B = a.B, Tn = a.Tn;
-  const int NM = H / PU, NG = 2 * a.NS;
+  const int NG = 2 * a.NS;
   const int g = blockIdx.x % NG, mem = blockIdx.x / NG;
   const int d = g & 1, s = g >> 1;
   const int u0 = mem * PU;
@@ -112,7 +154,8 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
   const int nks = H / 32;
   const int ks_beg = KSPLIT ? (wx ? nks / 2 : 0) : 0;
   const int ks_end = KSPLIT ? (wx ? nks : nks / 2) : nks;
-  unsigned* ctr = a.ctr + g * CTR_STRIDE;
+  const int wpr = H / 2;                        // exchange words per row
+  const int64_t slot_stride = (int64_t)2 * a.rows * wpr;
 
   float creg[MBW][4];
 #pragma unroll
@@ -122,7 +165,6 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
 
   for (int tau = 0; tau < Tn; ++tau) {
     const int t = d ? Tn - 1 - tau : tau;
-    const int tp = d ? t + 1 : t - 1;
     // input projection of this step for the epilogue (independent of h)
     float gx[MBW][4][4];
     if (epi) {
@@ -136,7 +178,6 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
           for (int q = 0; q < 4; ++q) gx[m][r][q] = (float)p[q * H];
         }
     }
-    if (tau > 0) group_wait(ctr, (unsigned)(NM * tau), a.status);
 
     f32x4 acc[MBW][4];
 #pragma unroll
@@ -144,27 +185,31 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) acc[m][q] = f32x4{0.f, 0.f, 0.f, 0.f};
     if (tau > 0) {
-      const bf16* arow[MBW];
-      bool rowok[MBW];
+      // h of the previous step, published with step number tau
+      const uint64_t* rp[MBW];
 #pragma unroll
       for (int m = 0; m < MBW; ++m) {
         const int row = rowbase + (mb0 + m) * 16 + (lane & 15);
-        rowok[m] = row < rend;
-        arow[m] = a.Y + ((int64_t)tp * B + (rowok[m] ? row : a.b0)) * 2 * H + (int64_t)d * H + (lane >> 4) * 8;
+        rp[m] = row < rend ? a.X + ((tau - 1) & 1) * slot_stride + ((int64_t)d * a.rows + (row - a.b0)) * wpr
+                           : nullptr;
       }
-#pragma unroll 4
-      for (int ks = ks_beg; ks < ks_end; ++ks) {
-        bf16x8 af[MBW];
+      for (int ks0 = ks_beg; ks0 < ks_end; ks0 += KC) {
+        const int nk = min(KC, ks_end - ks0);
+        bf16x8 af[MBW][KC];
+        ll_fragments<MBW, KC>(rp, ks0, nk, (uint32_t)tau, lane, af, a.status);
 #pragma unroll
-        for (int m = 0; m < MBW; ++m) af[m] = rowok[m] ? ld16(arow[m] + ks * 32) : bf16x8{};
-        const int kg = ks * 4 + (lane >> 4);
-        bf16x8 bfr[4];
+        for (int kk = 0; kk < KC; ++kk) {
+          if (kk >= nk) break;
+          const int kg = (ks0 + kk) * 4 + (lane >> 4);
+          bf16x8 bfr[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) bfr[q] = *(const bf16x8*)&lds[(kg * LDN + ub * 64 + q * 16 + (lane & 15)) * 8];
+          for (int q = 0; q < 4; ++q)
+            bfr[q] = *(const bf16x8*)&lds[(kg * LDN + ub * 64 + q * 16 + (lane & 15)) * 8];
 #pragma unroll
-        for (int m = 0; m < MBW; ++m)
+          for (int m = 0; m < MBW; ++m)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) acc[m][q] = Mfma<bf16>::mma(af[m], bfr[q], acc[m][q]);
+            for (int q = 0; q < 4; ++q) acc[m][q] = Mfma<bf16>::mma(af[m][kk], bfr[q], acc[m][q]);
+        }
       }
     }
     if (KSPLIT) {
@@ -179,12 +224,12 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
       }
     }
     if (epi) {
+      uint64_t* xo = a.X + (tau & 1) * slot_stride;
 #pragma unroll
       for (int m = 0; m < MBW; ++m)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int row = rowbase + (mb0 + m) * 16 + (lane >> 4) * 4 + r;
-          if (row >= rend) continue;
           const float ig = sigmoidf_(acc[m][0][r] + gx[m][r][0]);
           const float fg = sigmoidf_(acc[m][1][r] + gx[m][r][1]);
           const float gg = tanhf_(acc[m][2][r] + gx[m][r][2]);
@@ -192,6 +237,8 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
           const float c = fg * creg[m][r] + ig * gg;
           creg[m][r] = c;
           const float h = og * tanhf_(c);
+          const float h_next_unit = __shfl_xor(h, 1);   // lanes of one row, units u and u^1
+          if (row >= rend) continue;
           const int64_t fr = (int64_t)t * B + row;
           a.C[fr * 2 * H + (int64_t)d * H + unit] = c;
           a.Y[fr * 2 * H + (int64_t)d * H + unit] = (bf16)h;
@@ -200,146 +247,227 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
           gs[H] = (bf16)fg;
           gs[2 * H] = (bf16)gg;
           gs[3 * H] = (bf16)og;
+          if ((lane & 1) == 0)
+            ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 2, pack_bf16x2(h, h_next_unit),
+                     (uint32_t)(tau + 1));
         }
     }
-    group_arrive(ctr);
+    __syncthreads();   // the reduction buffer is reused by the next step
   }
 }
 
 // ---------------------------------------------------------------------------
 // Backward (BPTT).
+//
+// dh_rec[b][j] = sum over all 4H gate rows g of da[b][g] W_hh[g][j].  Member
+// m owns the 128 gate rows of its 32 units, so it computes the partial sums
+// P_m = da[:, own rows] W_hh[own rows, :] for ALL H units from data it
+// already holds (its own da, kept in LDS, and its W_hh rows, LDS-resident),
+// publishes P_m as exchange words, and gathers for its own 32 units the
+// partials of all members, summed in member order.  Per step a member thus
+// reads rows x 32 x H/32 values instead of rows x 4H.
 // ---------------------------------------------------------------------------
 template <int MB>
 __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
   extern __shared__ __attribute__((aligned(16))) bf16 lds[];
-  constexpr bool KSPLIT = MB == 1;
-  constexpr int MBW = KSPLIT ? 1 : MB / 2;
-  constexpr int LDN = PU + 1;    // LDS rows per k-group (32 units + pad)
+  constexpr int R = 16 * MB;            // rows of this member's slice
+  constexpr int ITEMS = 2 * MB;         // (row, unit) cell items per thread
   const int H = a.H, B = a.B, Tn = a.Tn;
   const int NM = H / PU, NG = 2 * a.NS;
   const int g = blockIdx.x % NG, mem = blockIdx.x / NG;
   const int d = g & 1, s = g >> 1;
   const int u0 = mem * PU;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int ub = w & 1, wx = w >> 1;
 
-  // W_hh columns of this member, transposed: LDS element (k = gate row, n = unit)
+  // LDS: W_hh of the 128 own gate rows, as the B operand [k/8][unit][8]
+  // (k = own row kk: gate (kk>>4)&3, unit u0 + (kk>>6)*16 + (kk&15));
+  // own da as the A operand [k/8][row][8]; gathered dh_rec [row][32] fp32.
+  bf16* wl = lds;
+  bf16* al = wl + (size_t)16 * (H + 1) * 8;
+  float* dhl = (float*)(al + (size_t)16 * (R + 1) * 8);
   const bf16* Wd = a.W + (d ? a.whh1 : a.whh0);
-  const int nblk = (4 * H / 8) * (PU / 8);
-  for (int b = tid; b < nblk; b += 256) {
-    const int kgrp = b / (PU / 8), nb = b % (PU / 8);
+  for (int b = tid; b < 16 * (H / 8); b += 256) {
+    const int kg = b % 16, jb = b / 16;
     uint4 in[8], out[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      in[i] = *(const uint4*)(Wd + (int64_t)(kgrp * 8 + i) * H + u0 + nb * 8);
+    for (int i = 0; i < 8; ++i) {
+      const int kk = kg * 8 + i;
+      const int64_t grow = (int64_t)((kk >> 4) & 3) * H + u0 + (kk >> 6) * 16 + (kk & 15);
+      in[i] = *(const uint4*)(Wd + grow * H + jb * 8);
+    }
     transpose8x8(in, out);
 #pragma unroll
-    for (int jj = 0; jj < 8; ++jj) *(uint4*)&lds[(kgrp * LDN + nb * 8 + jj) * 8] = out[jj];
+    for (int jj = 0; jj < 8; ++jj) *(uint4*)&wl[(kg * (H + 1) + jb * 8 + jj) * 8] = out[jj];
   }
-  f32x4* red = (f32x4*)(lds + (size_t)(4 * H / 8) * LDN * 8);
   __syncthreads();
 
   const int rend = a.b0 + a.rows;
-  const int rowbase = a.b0 + s * 16 * MB;
-  const int mb0 = KSPLIT ? 0 : wx * MBW;
-  const bool epi = !KSPLIT || wx == 0;
-  const int unit = u0 + ub * 16 + (lane & 15);
-  const int nks = 4 * H / 32;
-  const int ks_beg = KSPLIT ? (wx ? nks / 2 : 0) : 0;
-  const int ks_end = KSPLIT ? (wx ? nks : nks / 2) : nks;
-  unsigned* ctr = a.ctr + g * CTR_STRIDE;
-
-  float dcreg[MBW][4];
+  const int rowbase = a.b0 + s * R;
+  const int wpr = (H / 2) * NM;                  // exchange words per row
+  const int64_t slot_stride = (int64_t)2 * a.rows * wpr;
+  // cell items: unit cu = tid % 32, rows tid/32 + 8*i
+  const int cu = tid & 31;
+  float dcreg[ITEMS];
 #pragma unroll
-  for (int m = 0; m < MBW; ++m)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) dcreg[m][r] = 0.f;
+  for (int i = 0; i < ITEMS; ++i) dcreg[i] = 0.f;
 
   for (int tau = 0; tau < Tn; ++tau) {
     const int t = d ? tau : Tn - 1 - tau;
-    const int tn = d ? t - 1 : t + 1;
     const int tp = d ? t + 1 : t - 1;
     const bool has_prev = tp >= 0 && tp < Tn;
     // everything the cell derivative needs besides dh_rec
-    float dy[MBW][4], gt[MBW][4][4], cc[MBW][4], cp[MBW][4];
-    if (epi) {
+    float dy[ITEMS], gt[ITEMS][4], cc[ITEMS], cp[ITEMS];
 #pragma unroll
-      for (int m = 0; m < MBW; ++m)
+    for (int i = 0; i < ITEMS; ++i) {
+      int row = rowbase + (tid >> 5) + 8 * i;
+      row = row < rend ? row : a.b0;
+      const int64_t fr = (int64_t)t * B + row;
+      const int unit = u0 + cu;
+      dy[i] = a.DY[fr * 2 * H + (int64_t)d * H + unit];
+      cc[i] = a.C[fr * 2 * H + (int64_t)d * H + unit];
+      cp[i] = has_prev ? a.C[((int64_t)tp * B + row) * 2 * H + (int64_t)d * H + unit] : 0.f;
+      const bf16* gs = a.G + fr * 8 * H + (int64_t)d * 4 * H + unit;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          int row = rowbase + (mb0 + m) * 16 + (lane >> 4) * 4 + r;
-          row = row < rend ? row : a.b0;
-          const int64_t fr = (int64_t)t * B + row;
-          dy[m][r] = a.DY[fr * 2 * H + (int64_t)d * H + unit];
-          cc[m][r] = a.C[fr * 2 * H + (int64_t)d * H + unit];
-          cp[m][r] = has_prev ? a.C[((int64_t)tp * B + row) * 2 * H + (int64_t)d * H + unit] : 0.f;
-          const bf16* gs = a.G + fr * 8 * H + (int64_t)d * 4 * H + unit;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) gt[m][r][q] = (float)gs[q * H];
-        }
+      for (int q = 0; q < 4; ++q) gt[i][q] = (float)gs[q * H];
     }
-    if (tau > 0) group_wait(ctr, (unsigned)(NM * tau), a.status);
 
-    f32x4 acc[MBW];
-#pragma unroll
-    for (int m = 0; m < MBW; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // gather dh_rec for the own units: items (row, unit pair), pair = tid % 16
     if (tau > 0) {
-      const bf16* arow[MBW];
-      bool rowok[MBW];
+      const uint64_t* xs = a.X + ((tau - 1) & 1) * slot_stride;
 #pragma unroll
-      for (int m = 0; m < MBW; ++m) {
-        const int row = rowbase + (mb0 + m) * 16 + (lane & 15);
-        rowok[m] = row < rend;
-        arow[m] = a.DA + ((int64_t)tn * B + (rowok[m] ? row : a.b0)) * 8 * H + (int64_t)d * 4 * H + (lane >> 4) * 8;
-      }
-#pragma unroll 4
-      for (int ks = ks_beg; ks < ks_end; ++ks) {
-        bf16x8 af[MBW];
+      for (int i = 0; i < MB; ++i) {
+        const int r = (tid >> 4) + 16 * i;
+        const int p = tid & 15;
+        float lo = 0.f, hi = 0.f;
+        if (rowbase + r < rend) {
+          const uint64_t* src = xs + ((int64_t)d * a.rows + (rowbase + r - a.b0)) * wpr +
+                                (int64_t)(u0 / 2 + p) * NM;
+          uint64_t wv[PU / 2];
+          for (int m0 = 0; m0 < NM; m0 += PU / 2) {
+            const int nm = min(PU / 2, NM - m0);
 #pragma unroll
-        for (int m = 0; m < MBW; ++m) af[m] = rowok[m] ? ld16(arow[m] + ks * 32) : bf16x8{};
-        const int kg = ks * 4 + (lane >> 4);
-        const bf16x8 bfr = *(const bf16x8*)&lds[(kg * LDN + ub * 16 + (lane & 15)) * 8];
+            for (int k = 0; k < PU / 2; ++k) wv[k] = k < nm ? ll_load(src + m0 + k) : ((uint64_t)tau << 32);
+            for (unsigned it = 0;; ++it) {
+              bool bad = false;
 #pragma unroll
-        for (int m = 0; m < MBW; ++m) acc[m] = Mfma<bf16>::mma(af[m], bfr, acc[m]);
-      }
-    }
-    if (KSPLIT) {
-      if (wx == 1) red[ub * 64 + lane] = acc[0];
-      __syncthreads();
-      if (wx == 0) acc[0] += red[ub * 64 + lane];
-    }
-    if (epi) {
+              for (int k = 0; k < PU / 2; ++k) bad |= (uint32_t)(wv[k] >> 32) != (uint32_t)tau;
+              if (!bad) break;
+              if (it > SPIN_LIMIT ||
+                  ((it & 63) == 63 && __hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
+                __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                break;
+              }
+              __builtin_amdgcn_s_sleep(1);
 #pragma unroll
-      for (int m = 0; m < MBW; ++m)
+              for (int k = 0; k < PU / 2; ++k)
+                if ((uint32_t)(wv[k] >> 32) != (uint32_t)tau) wv[k] = ll_load(src + m0 + k);
+            }
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = rowbase + (mb0 + m) * 16 + (lane >> 4) * 4 + r;
-          if (row >= rend) continue;
-          const float ig = gt[m][r][0], fg = gt[m][r][1], gg = gt[m][r][2], og = gt[m][r][3];
-          const float dh = acc[m][r] + dy[m][r];
-          const float tc = tanhf_(cc[m][r]);
-          const float dc = dh * og * (1.f - tc * tc) + dcreg[m][r];
-          dcreg[m][r] = dc * fg;
-          bf16* da = a.DA + ((int64_t)t * B + row) * 8 * H + (int64_t)d * 4 * H + unit;
-          da[0] = (bf16)(dc * gg * ig * (1.f - ig));
-          da[H] = (bf16)(dc * cp[m][r] * fg * (1.f - fg));
-          da[2 * H] = (bf16)(dc * ig * (1.f - gg * gg));
-          da[3 * H] = (bf16)(dh * tc * og * (1.f - og));
+            for (int k = 0; k < PU / 2; ++k) {
+              if (k >= nm) break;
+              const uint32_t v = (uint32_t)wv[k];
+              lo += __builtin_bit_cast(float, v << 16);
+              hi += __builtin_bit_cast(float, v & 0xffff0000u);
+            }
+          }
         }
+        dhl[r * PU + 2 * p] = lo;
+        dhl[r * PU + 2 * p + 1] = hi;
+      }
+    } else {
+      for (int i = tid; i < R * PU; i += 256) dhl[i] = 0.f;
     }
-    group_arrive(ctr);
+    __syncthreads();
+
+    // cell derivatives; da goes to global memory (weight gradients) and to
+    // LDS (next partial product)
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      const int r = (tid >> 5) + 8 * i;
+      const int row = rowbase + r;
+      const float ig = gt[i][0], fg = gt[i][1], gg = gt[i][2], og = gt[i][3];
+      const float dh = dhl[r * PU + cu] + dy[i];
+      const float tc = tanhf_(cc[i]);
+      const float dc = dh * og * (1.f - tc * tc) + dcreg[i];
+      dcreg[i] = dc * fg;
+      float da[4];
+      da[0] = dc * gg * ig * (1.f - ig);
+      da[1] = dc * cp[i] * fg * (1.f - fg);
+      da[2] = dc * ig * (1.f - gg * gg);
+      da[3] = dh * tc * og * (1.f - og);
+      const bool ok = row < rend;
+      bf16* dst = a.DA + ((int64_t)t * B + (ok ? row : a.b0)) * 8 * H + (int64_t)d * 4 * H + u0 + cu;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const bf16 v = ok ? (bf16)da[q] : (bf16)0.f;
+        if (ok) dst[q * H] = v;
+        // own row kk = (cu >> 4)*64 + q*16 + (cu & 15)
+        const int kk = (cu >> 4) * 64 + q * 16 + (cu & 15);
+        al[((kk >> 3) * (R + 1) + r) * 8 + (kk & 7)] = v;
+      }
+    }
+    __syncthreads();
+
+    // P = da_own [R x 128] * W_own [128 x H]; 16-unit block nb goes to wave nb % 4
+    if (tau + 1 < Tn) {
+      const int NB = H / 16;
+      uint64_t* xo = a.X + (tau & 1) * slot_stride;
+      for (int base = 0; base < NB; base += 16) {
+        f32x4 acc[MB][4];
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          const int kg = ks * 4 + (lane >> 4);
+          bf16x8 af[MB], bfr[4];
+#pragma unroll
+          for (int m = 0; m < MB; ++m) af[m] = *(const bf16x8*)&al[(kg * (R + 1) + m * 16 + (lane & 15)) * 8];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int nb = base + w + 4 * j;
+            bfr[j] = nb < NB ? *(const bf16x8*)&wl[(kg * (H + 1) + nb * 16 + (lane & 15)) * 8] : bf16x8{};
+          }
+#pragma unroll
+          for (int m = 0; m < MB; ++m)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[m][j] = Mfma<bf16>::mma(af[m], bfr[j], acc[m][j]);
+        }
+        // publish: word (row, unit pair, member)
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float v = acc[m][j][r];
+              const float vn = __shfl_xor(v, 1);
+              const int row = rowbase + m * 16 + (lane >> 4) * 4 + r;
+              const int nb = base + w + 4 * j;
+              const int unit = nb * 16 + (lane & 15);
+              if ((lane & 1) == 0 && row < rend && nb < NB)
+                ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + (int64_t)(unit / 2) * NM + mem,
+                         pack_bf16x2(v, vn), (uint32_t)(tau + 1));
+            }
+      }
+    }
   }
 }
 
-__global__ void zero_u32_kernel(unsigned* p, int n) {
-  for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0u;
+__global__ __launch_bounds__(256) void clear_exchange_kernel(uint4* p, int64_t n16, int* status) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
+    p[i] = make_uint4(0u, 0u, 0u, 0u);
+  if (blockIdx.x == 0 && threadIdx.x == 0) *status = 0;
 }
 
 // ---------------------------------------------------------------------------
 // Host side.
 // ---------------------------------------------------------------------------
-size_t persist_lds_bytes(int H, bool backward) {
-  if (backward) return (size_t)(4 * H / 8) * (PU + 1) * 16 + 2 * 64 * 16;
+size_t persist_lds_bytes(int H, bool backward, int MB) {
+  if (backward)
+    return (size_t)16 * (H + 1) * 16 + (size_t)16 * (16 * MB + 1) * 16 + (size_t)16 * MB * PU * 4;
   return (size_t)(H / 8) * (128 + 1) * 16 + 8 * 64 * 16;
 }
 
@@ -352,20 +480,20 @@ static int persist_max_wg() {
   return cus;
 }
 
-bool persist_supported(int H) {
-  return H % PU == 0 && persist_lds_bytes(H, false) <= 160 * 1024 &&
-         persist_lds_bytes(H, true) <= 160 * 1024;
+bool persist_supported(int H, int T) {
+  return H % PU == 0 && T < (1 << 30) && persist_lds_bytes(H, false, 1) <= 160 * 1024 &&
+         persist_lds_bytes(H, true, 1) <= 160 * 1024;
 }
 
-template <int MB>
-static hipError_t launch_one(bool backward, PersistArgs a, hipStream_t s) {
-  const void* fn = backward ? (const void*)lstm_bwd_persist<MB> : (const void*)lstm_fwd_persist<MB>;
-  const size_t lds = persist_lds_bytes(a.H, backward);
+template <int MB, bool BWD>
+static hipError_t launch_one(PersistArgs a, hipStream_t s) {
+  const void* fn = BWD ? (const void*)lstm_bwd_persist<MB> : (const void*)lstm_fwd_persist<MB>;
+  const size_t lds = persist_lds_bytes(a.H, BWD, MB);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   const dim3 grid(2 * a.NS * (a.H / PU)), block(256);
   void* args[] = {&a};
-  const char* name = backward ? "lstm_rec_bwd_persist" : "lstm_rec_fwd_persist";
+  const char* name = BWD ? "lstm_rec_bwd_persist" : "lstm_rec_fwd_persist";
   const int slot = g_timing_on ? timing_pre(name, s) : -1;
   e = hipLaunchCooperativeKernel(fn, grid, block, args, (unsigned)lds, s);
   if (slot >= 0) timing_post(slot, s);
@@ -376,25 +504,31 @@ static hipError_t launch_one(bool backward, PersistArgs a, hipStream_t s) {
 // launch error (nothing was enqueued for the failing chunk in that case).
 hipError_t persist_layer(bool backward, PersistArgs a, hipStream_t s) {
   const int NM = a.H / PU;
-  const int max_ns = std::min(persist_max_wg() / (2 * NM), 32);
+  const int max_ns = std::min(persist_max_wg() / (2 * NM), PERSIST_MAX_SLICES);
   if (max_ns < 1) return hipErrorInvalidValue;
+  // rows per workgroup: as few as fill the chip, up to 8 row blocks (4 in
+  // the backward, whose LDS also holds its own da), more rows by chunking
+  const int mb_cap = backward ? 4 : 8;
   int MB = 1;
-  while (MB < 8 && (a.B + 16 * MB - 1) / (16 * MB) > max_ns) MB *= 2;
+  while (MB < mb_cap && (a.B + 16 * MB - 1) / (16 * MB) > max_ns) MB *= 2;
+  while (MB > 1 && persist_lds_bytes(a.H, backward, MB) > 160 * 1024) MB /= 2;
   const int chunk = std::min(a.B, max_ns * 16 * MB);
   for (int b0 = 0; b0 < a.B; b0 += chunk) {
     PersistArgs c = a;
     c.b0 = b0;
     c.rows = std::min(chunk, a.B - b0);
     c.NS = (c.rows + 16 * MB - 1) / (16 * MB);
-    // counters and the status word are contiguous
-    hipLaunchKernelGGL(zero_u32_kernel, dim3(1), dim3(256), 0, s, c.ctr, PERSIST_CTR_BYTES / 4 + 1);
+    // both exchange slots of this chunk start without any valid step number
+    const int64_t words = (int64_t)2 * 2 * c.rows * (c.H / 2) * (backward ? c.H / PU : 1);
+    const int64_t n16 = words / 2;
+    hipLaunchKernelGGL(clear_exchange_kernel, dim3((unsigned)std::min<int64_t>(cdiv(n16, 256), 2048)),
+                       dim3(256), 0, s, (uint4*)c.X, n16, c.status);
     hipError_t e;
-    switch (MB) {
-      case 1: e = launch_one<1>(backward, c, s); break;
-      case 2: e = launch_one<2>(backward, c, s); break;
-      case 4: e = launch_one<4>(backward, c, s); break;
-      default: e = launch_one<8>(backward, c, s); break;
-    }
+    if (backward)
+      e = MB == 1 ? launch_one<1, true>(c, s) : MB == 2 ? launch_one<2, true>(c, s) : launch_one<4, true>(c, s);
+    else
+      e = MB == 1 ? launch_one<1, false>(c, s) : MB == 2 ? launch_one<2, false>(c, s)
+                  : MB == 4 ? launch_one<4, false>(c, s) : launch_one<8, false>(c, s);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -12,17 +12,27 @@ struct PersistArgs {
   bf16* G;            // activated gates [M][8H] (forward writes, backward reads)
   bf16* DA;           // backward: gate pre-activation gradients [M][8H]
   const float* DY;    // backward: gradient reaching the layer output [M][2H]
-  unsigned* ctr;      // group counters (zeroed before each launch)
-  int* status;        // set to 1 if a barrier wait ever timed out
+  uint64_t* X;        // step-exchange words (see lstm_persist.hip), PERSIST_XCH_BYTES
+  int* status;        // cleared before each launch; 1 if a poll ever gave up
   int Tn, B, H;
   int b0, rows, NS;   // batch chunk handled by one launch (filled in by persist_layer)
 };
 
-// Largest number of groups' counters a launch uses (times CTR stride).
-#define PERSIST_CTR_BYTES (64 * 32 * 4)
+// At most this many batch slices of 16*MB rows per launch (MB <= 8), so one
+// launch covers at most PERSIST_MAX_SLICES*128 rows.
+#define PERSIST_MAX_SLICES 32
+#define PERSIST_MAX_ROWS (PERSIST_MAX_SLICES * 16 * 8)
+// Exchange buffer: 2 slots x 2 directions x rows x (H/2 unit pairs) x
+// (H/32 members) words of 8 bytes (the backward's partial sums; the forward
+// uses the first H/2 words per row).
+static inline size_t persist_xch_bytes(int B, int H) {
+  const size_t rows = B < PERSIST_MAX_ROWS ? B : PERSIST_MAX_ROWS;
+  const size_t members = H / 32 > 0 ? H / 32 : 1;
+  return (size_t)2 * 2 * rows * (H / 2) * members * 8;
+}
 
 // True if the persistent kernels can hold a W_hh slice for this H in LDS.
-bool persist_supported(int H);
+bool persist_supported(int H, int T);
 // Runs every step of one layer, both directions; hipSuccess or the error of
 // the cooperative launch that failed.
 hipError_t persist_layer(bool backward, PersistArgs a, hipStream_t s);

@@ -8,6 +8,7 @@ unrounded float32 inputs.  The update kernels follow the oracle's float32
 operation order exactly and are compared bit for bit; the bf16 operand copy
 is compared bit for bit with round-to-nearest-even."""
 
+import os
 import sys
 
 import numpy as np
@@ -275,8 +276,12 @@ def test_timing_hooks_report_kernels(gpu_lib):
     bd.blstm_timing_begin("lstm_rec")
     st.gradient()
     got = bd.blstm_timing_end()
-    assert set(got) == {"lstm_rec_fwd_persist", "lstm_rec_bwd_persist"}
-    assert got["lstm_rec_fwd_persist"][0] == 1 and got["lstm_rec_bwd_persist"][0] == 1
+    if os.environ.get("ADPSGD_BLSTM_NO_PERSIST") == "1":
+        assert set(got) == {"lstm_rec_fwd", "lstm_rec_bwd"}
+        assert got["lstm_rec_fwd"][0] == 4 and got["lstm_rec_bwd"][0] == 4
+    else:
+        assert set(got) == {"lstm_rec_fwd_persist", "lstm_rec_bwd_persist"}
+        assert got["lstm_rec_fwd_persist"][0] == 1 and got["lstm_rec_bwd_persist"][0] == 1
     assert all(v[1] > 0 for v in got.values())
 
 
