@@ -18,6 +18,8 @@
 // [BK/KPL][BMN + pad][KPL] so that one MFMA fragment is one aligned LDS read.
 #pragma once
 
+#include <type_traits>
+
 #include "common.hpp"
 
 struct Opnd {
@@ -167,7 +169,7 @@ struct TileLoader {
 };
 
 template <typename T, int BM, int BN, int BK, int WM, int WN, bool AKC, bool BKC, int VA, int VB,
-          class Epi>
+          class Epi, int STAGES = 1>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const Opnd A, const Opnd B, int64_t M,
                                                             int64_t N, int64_t K, int64_t ksplit,
                                                             int splits, const Epi epi) {
@@ -194,11 +196,33 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const Opnd A, const 
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (ntiles > 0) {
-    TileLoader<T, BM, BK, NT, AKC, VA, 0> la;
-    TileLoader<T, BN, BK, NT, BKC, VB, (!AKC && !BKC) ? NT / 2 : 0> lb;
-    la.load(A, z, m0, kbeg, kend, tid);
-    lb.load(B, z, n0, kbeg, kend, tid);
+  typedef TileLoader<T, BM, BK, NT, AKC, VA, 0> LA;
+  typedef TileLoader<T, BN, BK, NT, BKC, VB, (!AKC && !BKC) ? NT / 2 : 0> LB;
+  auto compute = [&](const T* lA, const T* lB) {
+#pragma unroll
+    for (int ks = 0; ks < BK / MT::KSTEP; ++ks) {
+      const int kg = ks * (MT::KSTEP / KPL) + (lane >> 4);
+      typename MT::frag a[FM], b[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        a[i] = *(const typename MT::frag*)&lA[(kg * (BM + PADR) + wm * (BM / WM) + i * 16 + (lane & 15)) * KPL];
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        b[j] = *(const typename MT::frag*)&lB[(kg * (BN + PADR) + wn * (BN / WN) + j * 16 + (lane & 15)) * KPL];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = MT::mma(a[i], b[j], acc[i][j]);
+    }
+  };
+  auto kat = [&](int j) { return kbeg + (int64_t)j * BK; };
+  if (STAGES == 1 && ntiles > 0) {
+    // one register stage: the global loads of tile i+1 are in flight while
+    // tile i is multiplied from LDS
+    LA la;
+    LB lb;
+    la.load(A, z, m0, kat(0), kend, tid);
+    lb.load(B, z, n0, kat(0), kend, tid);
     la.store(&lds[0][0], tid);
     lb.store(&lds[0][SA], tid);
     __syncthreads();
@@ -206,29 +230,58 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const Opnd A, const 
       const int cur = it & 1;
       const bool more = it + 1 < ntiles;
       if (more) {
-        la.load(A, z, m0, kbeg + (int64_t)(it + 1) * BK, kend, tid);
-        lb.load(B, z, n0, kbeg + (int64_t)(it + 1) * BK, kend, tid);
+        la.load(A, z, m0, kat(it + 1), kend, tid);
+        lb.load(B, z, n0, kat(it + 1), kend, tid);
       }
-      const T* lA = &lds[cur][0];
-      const T* lB = &lds[cur][SA];
-#pragma unroll
-      for (int ks = 0; ks < BK / MT::KSTEP; ++ks) {
-        const int kg = ks * (MT::KSTEP / KPL) + (lane >> 4);
-        typename MT::frag a[FM], b[FN];
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-          a[i] = *(const typename MT::frag*)&lA[(kg * (BM + PADR) + wm * (BM / WM) + i * 16 + (lane & 15)) * KPL];
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          b[j] = *(const typename MT::frag*)&lB[(kg * (BN + PADR) + wn * (BN / WN) + j * 16 + (lane & 15)) * KPL];
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-          for (int j = 0; j < FN; ++j) acc[i][j] = MT::mma(a[i], b[j], acc[i][j]);
-      }
+      compute(&lds[cur][0], &lds[cur][SA]);
       if (more) {
         la.store(&lds[cur ^ 1][0], tid);
         lb.store(&lds[cur ^ 1][SA], tid);
+      }
+      __syncthreads();
+    }
+  }
+  // two register stages: the global loads of tile i+2 are in flight while
+  // tile i is multiplied from LDS and tile i+1 is written to the other LDS
+  // buffer (two iterations of memory latency hidden, more registers)
+  if (STAGES == 2 && ntiles > 0) {
+    LA la0, la1;
+    LB lb0, lb1;
+    la0.load(A, z, m0, kat(0), kend, tid);
+    lb0.load(B, z, n0, kat(0), kend, tid);
+    la0.store(&lds[0][0], tid);
+    lb0.store(&lds[0][SA], tid);
+    if (ntiles > 1) {
+      la1.load(A, z, m0, kat(1), kend, tid);
+      lb1.load(B, z, n0, kat(1), kend, tid);
+    }
+    if (ntiles > 2) {
+      la0.load(A, z, m0, kat(2), kend, tid);
+      lb0.load(B, z, n0, kat(2), kend, tid);
+    }
+    __syncthreads();
+    for (int it = 0; it < ntiles; it += 2) {
+      // tile it is in LDS buffer 0; registers: stage 1 = tile it+1, stage 0 = tile it+2
+      compute(&lds[0][0], &lds[0][SA]);
+      if (it + 1 < ntiles) {
+        la1.store(&lds[1][0], tid);
+        lb1.store(&lds[1][SA], tid);
+      }
+      if (it + 3 < ntiles) {
+        la1.load(A, z, m0, kat(it + 3), kend, tid);
+        lb1.load(B, z, n0, kat(it + 3), kend, tid);
+      }
+      __syncthreads();
+      if (it + 1 >= ntiles) break;
+      // tile it+1 is in LDS buffer 1; stage 0 = tile it+2, stage 1 = tile it+3
+      compute(&lds[1][0], &lds[1][SA]);
+      if (it + 2 < ntiles) {
+        la0.store(&lds[0][0], tid);
+        lb0.store(&lds[0][SA], tid);
+      }
+      if (it + 4 < ntiles) {
+        la0.load(A, z, m0, kat(it + 4), kend, tid);
+        lb0.load(B, z, n0, kat(it + 4), kend, tid);
       }
       __syncthreads();
     }
@@ -277,7 +330,9 @@ static inline EpiStore<TO> epi_store(TO* out, int64_t ld, int64_t M, int64_t N, 
   return e;
 }
 
-// Tile configurations per element type.
+// Tile configurations.  bf16: 128x128 blocks with 64x64 wave tiles (66 KB of
+// LDS, two workgroups per CU so one hides the other's barrier stalls);
+// float32: 64x64 blocks.
 template <typename T> struct GemmCfg;
 template <> struct GemmCfg<bf16> {
   static constexpr int BM = 128, BN = 128, BK = 64, WM = 2, WN = 2;
@@ -285,16 +340,35 @@ template <> struct GemmCfg<bf16> {
 template <> struct GemmCfg<float> {
   static constexpr int BM = 64, BN = 64, BK = 16, WM = 2, WN = 2;
 };
+template <typename T, class C, bool AKC, bool BKC, int VA, int VB, class Epi, int STAGES = 1>
+static inline void gemm_launch_cfg(const char* name, hipStream_t s, const Opnd& A, const Opnd& B,
+                                   int64_t M, int64_t N, int64_t K, int batches, int splits,
+                                   const Epi& epi) {
+  const int64_t ksplit = splits > 1 ? rup(cdiv(K, splits), C::BK) : (K > 0 ? K : 1);
+  dim3 grid((unsigned)cdiv(N, C::BN), (unsigned)cdiv(M, C::BM), (unsigned)(batches * splits));
+  BLSTM_LAUNCH(name, (gemm_kernel<T, C::BM, C::BN, C::BK, C::WM, C::WN, AKC, BKC, VA, VB, Epi, STAGES>),
+               grid, dim3(C::WM * C::WN * 64), 0, s, A, B, M, N, K, ksplit, splits, epi);
+}
+
+// K-contiguous x K-contiguous bf16 products run 32-deep k-tiles (measured
+// faster at the learner-step shapes on MI355X); products with an
+// MN-contiguous operand keep 64-deep tiles so that the 8x8 transposed staging
+// keeps every thread busy.
+struct GemmCfgK32 {
+  static constexpr int BM = 128, BN = 128, BK = 32, WM = 2, WN = 2;
+};
 
 template <typename T, bool AKC, bool BKC, int VA, int VB, class Epi>
 static inline void gemm_launch(const char* name, hipStream_t s, const Opnd& A, const Opnd& B,
                                int64_t M, int64_t N, int64_t K, int batches, int splits,
                                const Epi& epi) {
-  typedef GemmCfg<T> C;
-  const int64_t ksplit = splits > 1 ? rup(cdiv(K, splits), C::BK) : (K > 0 ? K : 1);
-  dim3 grid((unsigned)cdiv(N, C::BN), (unsigned)cdiv(M, C::BM), (unsigned)(batches * splits));
-  BLSTM_LAUNCH(name, (gemm_kernel<T, C::BM, C::BN, C::BK, C::WM, C::WN, AKC, BKC, VA, VB, Epi>),
-               grid, dim3(C::WM * C::WN * 64), 0, s, A, B, M, N, K, ksplit, splits, epi);
+  if constexpr (std::is_same<T, bf16>::value && AKC && BKC) {
+    if (splits == 1) {
+      gemm_launch_cfg<T, GemmCfgK32, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits, epi);
+      return;
+    }
+  }
+  gemm_launch_cfg<T, GemmCfg<T>, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits, epi);
 }
 
 // Fixed-order split-K reduction: dst[z][m][n] = sum_s part[z][s][m][n]

@@ -10,6 +10,8 @@
 // which feeds the three backward GEMMs (dW_s, dz, and via dz dW_l and dy).
 #include <math.h>
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "gemm.hpp"
 #include "reduce.hpp"
@@ -69,6 +71,75 @@ __global__ __launch_bounds__(256) void softmax_ce_rows_kernel(T* __restrict__ S,
   }
 }
 
+// Single-pass variant for rows of up to 256*8*NV classes: each thread keeps
+// its NV 8-element vectors of the row in registers, so the logits are read
+// once and ds written once.
+template <typename T, int NV>
+__global__ __launch_bounds__(256) void softmax_ce_rows_reg_kernel(T* __restrict__ S, int K, int Kp,
+                                                                  const int32_t* __restrict__ labels,
+                                                                  float scale, float* __restrict__ rowloss) {
+  const int64_t m = blockIdx.x;
+  T* s = S + m * Kp;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int nvec = Kp / 8;
+  float v[NV][8];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = tid + 256 * i;
+    if (c < nvec) {
+      const uint4 raw = *(const uint4*)(s + (int64_t)c * 8);
+      const T* e = (const T*)&raw;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        v[i][j] = (c * 8 + j < K) ? to_f32(e[j]) : -INFINITY;
+        mx = fmaxf(mx, v[i][j]);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[i][j] = -INFINITY;
+    }
+  }
+  __shared__ float red[4], sh_lse;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+  if (lane == 0) red[wid] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  float sm = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sm += __expf(v[i][j] - mx);   // exp(-inf) = 0 for padding
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) sm += __shfl_xor(sm, off);
+  __syncthreads();
+  if (lane == 0) red[wid] = sm;
+  __syncthreads();
+  const int lab = labels[m];
+  if (tid == 0) {
+    const float lse = mx + __logf(red[0] + red[1] + red[2] + red[3]);
+    sh_lse = lse;
+    // an out-of-range label is not read (the loss becomes NaN instead)
+    rowloss[m] = lse - ((lab >= 0 && lab < K) ? to_f32(s[lab]) : __int_as_float(0x7fc00000));
+  }
+  __syncthreads();
+  const float lse = sh_lse;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = tid + 256 * i;
+    if (c >= nvec) continue;
+    uint4 out;
+    T* e = (T*)&out;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int k = c * 8 + j;
+      e[j] = from_f32<T>(k < K ? scale * (__expf(v[i][j] - lse) - (k == lab ? 1.f : 0.f)) : 0.f);
+    }
+    *(uint4*)(s + (int64_t)c * 8) = out;
+  }
+}
+
 // loss = scale * sum of per-frame losses, in a fixed order.
 __global__ __launch_bounds__(256) void loss_sum_kernel(const float* __restrict__ rowloss, int64_t M,
                                                        float scale, float* __restrict__ loss) {
@@ -109,8 +180,21 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
   gemm_launch<T, true, true, V, V>("gemm_logits", s, opnd(Z, P, P, M), opnd(W + lo.Ws, P, P, K), M,
                                    K, P, 1, 1, epi_store<T>(S, Kp, M, K, 0, 0, theta + lo.bs));
   // per-frame loss and ds (in place)
-  BLSTM_LAUNCH("softmax_ce_rows", softmax_ce_rows_kernel<T>, dim3((unsigned)M), dim3(256), 0, s, S, K,
-               Kp, labels, scale, RL);
+  {
+    // ds in place; rows of up to 32768 classes stay in registers (bf16, 16 B vectors)
+    const int nv = (int)cdiv(Kp / 8, 256);
+    const dim3 g((unsigned)M), b(256);
+    if (std::is_same<T, bf16>::value && nv <= 16) {
+      if (nv <= 1)
+        BLSTM_LAUNCH("softmax_ce_rows", (softmax_ce_rows_reg_kernel<bf16, 1>), g, b, 0, s, (bf16*)S, K, Kp, labels, scale, RL);
+      else if (nv <= 4)
+        BLSTM_LAUNCH("softmax_ce_rows", (softmax_ce_rows_reg_kernel<bf16, 4>), g, b, 0, s, (bf16*)S, K, Kp, labels, scale, RL);
+      else
+        BLSTM_LAUNCH("softmax_ce_rows", (softmax_ce_rows_reg_kernel<bf16, 16>), g, b, 0, s, (bf16*)S, K, Kp, labels, scale, RL);
+    } else {
+      BLSTM_LAUNCH("softmax_ce_rows", softmax_ce_rows_kernel<T>, g, b, 0, s, S, K, Kp, labels, scale, RL);
+    }
+  }
   BLSTM_LAUNCH("loss_sum", loss_sum_kernel, dim3(1), dim3(256), 0, s, RL, M, scale, loss);
   // db_s = sum over frames of ds
   colsum<T>("colsum_dbs", s, S, M, K, Kp, csp, K, 0, grad + lo.bs, nullptr);

@@ -285,9 +285,8 @@ static bool step_rows_32(int H, int B) { return (int64_t)(H / 16) * cdiv(B, 32) 
 // paper's shapes): the persistent kernel for the forward pass and the
 // per-step kernels for BPTT.  ADPSGD_BLSTM_RECURRENCE=persistent uses the
 // persistent kernels for both passes, =per-step (or ADPSGD_BLSTM_NO_PERSIST=1)
-// none.  The persistent kernels need bf16, a W_hh slice that fits in LDS and
-// a stream that is not being captured into a graph (cooperative launches
-// are not recorded).
+// none.  The persistent kernels need bf16 and a W_hh slice that fits in LDS;
+// inside stream capture they are recorded as cooperative kernel nodes.
 template <typename T>
 static bool use_persistent(int H, int steps, bool backward, hipStream_t s) {
   if (!std::is_same<T, bf16>::value) return false;
@@ -297,7 +296,13 @@ static bool use_persistent(int H, int steps, bool backward, hipStream_t s) {
   if (pol && strcmp(pol, "per-step") == 0) return false;
   if (backward && !(pol && strcmp(pol, "persistent") == 0)) return false;
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-  if (hipStreamIsCapturing(s, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone) return false;
+  if (hipStreamIsCapturing(s, &cap) != hipSuccess) return false;
+  if (cap != hipStreamCaptureStatusNone) {
+    // captured launches carry the cooperative attribute; ADPSGD_BLSTM_GRAPH_PERSIST=0
+    // keeps graphs on the per-step kernels
+    const char* g = getenv("ADPSGD_BLSTM_GRAPH_PERSIST");
+    if (g && !atoi(g)) return false;
+  }
   return persist_supported(H, steps);
 }
 

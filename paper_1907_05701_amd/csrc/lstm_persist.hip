@@ -29,6 +29,8 @@
 // consumed the slot's current contents.  The buffer is cleared before each
 // launch, so no word from an earlier launch can carry a valid step number.
 // The launch is cooperative, so every member of a group is resident.
+#include <string.h>
+
 #include "common.hpp"
 #include "lstm_persist.hpp"
 
@@ -495,7 +497,27 @@ static hipError_t launch_one(PersistArgs a, hipStream_t s) {
   void* args[] = {&a};
   const char* name = BWD ? "lstm_rec_bwd_persist" : "lstm_rec_fwd_persist";
   const int slot = g_timing_on ? timing_pre(name, s) : -1;
-  e = hipLaunchCooperativeKernel(fn, grid, block, args, (unsigned)lds, s);
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  e = hipStreamIsCapturing(s, &cap);
+  if (e != hipSuccess) return e;
+  if (cap == hipStreamCaptureStatusNone) {
+    e = hipLaunchCooperativeKernel(fn, grid, block, args, (unsigned)lds, s);
+  } else {
+    // recorded into a graph as a kernel node with the cooperative attribute
+    hipLaunchAttribute attr;
+    memset(&attr, 0, sizeof(attr));
+    attr.id = hipLaunchAttributeCooperative;
+    attr.val.cooperative = 1;
+    hipLaunchConfig_t cfg;
+    memset(&cfg, 0, sizeof(cfg));
+    cfg.gridDim = grid;
+    cfg.blockDim = block;
+    cfg.dynamicSmemBytes = lds;
+    cfg.stream = s;
+    cfg.attrs = &attr;
+    cfg.numAttrs = 1;
+    e = hipLaunchKernelExC(&cfg, fn, args);
+  }
   if (slot >= 0) timing_post(slot, s);
   return e;
 }

@@ -315,3 +315,33 @@ def test_graph_replays_match_eager_steps(gpu_lib, monkeypatch):
         np.testing.assert_array_equal(replayed.loss.cpu().numpy(), eager.loss.cpu().numpy())
         np.testing.assert_array_equal(replayed.grad.cpu().numpy(), eager.grad.cpu().numpy())
         say(f"[graph] replay {i} matches, loss {float(eager.loss.cpu()[0]):.6f}")
+
+
+def test_graph_replays_with_persistent_forward(gpu_lib, monkeypatch):
+    """Same as above with the persistent forward kernel recorded into the
+    graph as a cooperative node (bit-identical to eager persistent steps)."""
+    from paper_1907_05701_amd.step import LearnerStep
+    monkeypatch.delenv("ADPSGD_BLSTM_NO_PERSIST", raising=False)
+    monkeypatch.setenv("ADPSGD_BLSTM_RECURRENCE", "auto")
+    monkeypatch.setenv("ADPSGD_BLSTM_GRAPH_PERSIST", "1")
+    shape = dict(L=2, D=260, H=512, P=64, K=3000, T=7, B=40)
+    dims = ref.Dims(**shape)
+    n = ref.param_count(dims)
+    theta = inputs.params(n)
+    x = inputs.features(dims.T, dims.B, dims.D)
+    lab = inputs.labels(dims.T, dims.B, dims.K, dist="zipf")
+    peer = inputs.peer(theta)
+    eager = LearnerStep(**shape, precision="bf16")
+    eager.load(theta, x, lab, peer)
+    replayed = LearnerStep(**shape, precision="bf16")
+    replayed.load(theta, x, lab, peer)
+    graph = replayed.capture(0.05)
+    torch.cuda.synchronize()
+    replayed.load(theta, x, lab, peer)
+    for i in range(3):
+        eager.step(0.05)
+        graph.replay()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(replayed.theta.cpu().numpy(), eager.theta.cpu().numpy())
+        np.testing.assert_array_equal(replayed.y_top.float().cpu().numpy(), eager.y_top.float().cpu().numpy())
+        say(f"[graph+persistent] replay {i} matches, loss {float(eager.loss.cpu()[0]):.6f}")
