@@ -63,6 +63,45 @@ def kernel_work(name, c, n_params):
     return None
 
 
+def recorded_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel`, from the rocprofv3 FETCH_SIZE /
+    WRITE_SIZE counters recorded in profiles/traffic.json (each divided by
+    what the same counter reads for a plain device copy of known size).
+    None when no record matches this kernel and workload, or when the
+    kernel's source file has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    for r in rec.get("kernels", []):
+        if r["kernel"] != kernel or r["workload"] != workload:
+            continue
+        src = os.path.join(ROOT, r["source"])
+        if not os.path.exists(src):
+            return None
+        with open(src, "rb") as fh:
+            if hashlib.sha256(fh.read()).hexdigest() != r["source_sha256"]:
+                return None
+        return int((r["fetch_kib_per_dispatch"] / rec["copy_factor_fetch"]
+                    + r["write_kib_per_dispatch"] / rec["copy_factor_write"]) * 1024)
+    return None
+
+
+def calibrate_copy(mib):
+    """A plain device-to-device copy of `mib` MiB (one torch copy kernel),
+    run three times: the reference for scaling the HBM byte counters."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes": n * 4, "launches": 3}), flush=True)
+
+
 def peak_for(bound, precision):
     if bound == "hbm":
         return PEAK_HBM_GBS, "GB/s"
@@ -112,7 +151,12 @@ def main():
     ap.add_argument("--breakdown", action="store_true", help="per-kernel times to stderr")
     ap.add_argument("--mode", choices=("graph", "eager"), default="graph",
                     help="replay the timed steps as one HIP graph, or launch them one by one")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one learner on one GPU; --gpus {args.gpus} is not supported "
               "(the multi-GPU exchange of the paper is not part of this library)", file=sys.stderr)
@@ -193,7 +237,8 @@ def main():
     achieved = per_launch / avg_s / (1e9 if bound == "hbm" else 1e12)
     peak, punit = peak_for(bound, cfg["precision"])
     roofline = {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": punit,
-                "frac": round(achieved / peak, 5), "traffic": None, "kernel": dominant,
+                "frac": round(achieved / peak, 5), "traffic": recorded_traffic(dominant, args.workload),
+                "kernel": dominant,
                 "avg_launch_us": round(avg_s * 1e6, 3),
                 "algorithmic_per_launch": per_launch, "algorithmic_unit": unit}
     out = {"metric": METRIC, "value": round(value, 1), "unit": "frames/s", "n_gpus": 1,

@@ -139,10 +139,12 @@ const char* blstm_last_error(void);
 
 /* Optional kernel timing.  After blstm_timing_begin(prefix), every library
  * kernel whose name starts with prefix ("" = all) is bracketed by HIP events
- * on the stream it is launched on.  blstm_timing_end() waits for those
- * events, fills up to cap entries (one per kernel name: launches and summed
- * milliseconds), stores the number of names in *count and stops recording.
- * Host-side bookkeeping only; not thread-safe. */
+ * on the stream it is launched on; a run of consecutive launches of one
+ * per-time-step kernel shares one event pair (counted as that many
+ * launches).  blstm_timing_end() waits for those events, fills up to cap
+ * entries (one per kernel name: launches and summed milliseconds), stores
+ * the number of names in *count and stops recording.  Host-side bookkeeping
+ * only; not thread-safe. */
 typedef struct blstm_kernel_time {
   char name[48];
   int32_t launches;

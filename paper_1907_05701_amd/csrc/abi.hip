@@ -168,6 +168,7 @@ static std::string g_prefix;
 struct TimedLaunch {
   std::string name;
   hipEvent_t start, stop;
+  int launches;
 };
 static std::vector<TimedLaunch> g_launches;
 static std::vector<hipEvent_t> g_pool;
@@ -183,10 +184,13 @@ static hipEvent_t take_event() {
   return e;
 }
 
-int timing_pre(const char* name, hipStream_t s) {
+int timing_pre(const char* name, hipStream_t s) { return timing_pre_n(name, s, 1); }
+
+int timing_pre_n(const char* name, hipStream_t s, int launches) {
   if (strncmp(name, g_prefix.c_str(), g_prefix.size()) != 0) return -1;
   TimedLaunch t;
   t.name = name;
+  t.launches = launches;
   t.start = take_event();
   t.stop = take_event();
   if (!t.start || !t.stop) return -1;
@@ -226,7 +230,7 @@ extern "C" int blstm_timing_end(blstm_kernel_time* out, int32_t cap, int32_t* co
       snprintf(k.name, sizeof(k.name), "%s", t.name.c_str());
       agg.push_back(k);
     }
-    agg[i].launches += 1;
+    agg[i].launches += t.launches;
     agg[i].total_ms += ms;
   }
   if (count) *count = (int32_t)agg.size();

@@ -97,9 +97,30 @@ int blstm_fail(int code, const char* fmt, ...);
 int blstm_check_launch(const char* what);
 
 // Kernel timing hooks; see blstm_timing_begin in the public header.
-extern bool g_timing_on;
 int timing_pre(const char* name, hipStream_t s);
+extern bool g_timing_on;
+// one event pair around `launches` consecutive launches of one kernel
+int timing_pre_n(const char* name, hipStream_t s, int launches);
 void timing_post(int slot, hipStream_t s);
+
+// Times a run of consecutive launches of one kernel as a single event pair
+// (per-launch events would add their own gaps between back-to-back kernels).
+struct TimedRun {
+  int slot;
+  bool saved;
+  hipStream_t s;
+  TimedRun(const char* name, hipStream_t st, int launches) : s(st) {
+    extern bool g_timing_on;
+    saved = g_timing_on;
+    slot = g_timing_on ? timing_pre_n(name, st, launches) : -1;
+    g_timing_on = false;
+  }
+  ~TimedRun() {
+    extern bool g_timing_on;
+    g_timing_on = saved;
+    if (slot >= 0) timing_post(slot, s);
+  }
+};
 
 #define BLSTM_LAUNCH(name, kernel, grid, block, shmem, stream, ...)                     \
   do {                                                                                 \

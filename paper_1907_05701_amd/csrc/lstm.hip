@@ -360,6 +360,7 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
     ra.G = Gl; ra.Tn = lo.T; ra.B = B; ra.H = H;
     const bool two = step_rows_32(H, B);
     const dim3 grid(H / 16, (unsigned)cdiv(B, two ? 32 : 16), 2);
+    TimedRun timed("lstm_rec_fwd", s, lo.T);
     for (int tau = 0; tau < lo.T; ++tau) {
       ra.tau = tau;
       if (two)
@@ -414,6 +415,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       rb.DA = DA; rb.WT0 = WT + (int64_t)(2 * l) * 4 * H * H; rb.WT1 = WT + (int64_t)(2 * l + 1) * 4 * H * H;
       rb.DY = dY; rb.G = Gl; rb.C = Cl; rb.DC = DC; rb.Tn = Tn; rb.B = B; rb.H = H;
       const dim3 grid(H / 16, (unsigned)cdiv(B, 16), 2);
+      TimedRun timed("lstm_rec_bwd", s, Tn);
       for (int tau = 0; tau < Tn; ++tau) {
         rb.tau = tau;
         BLSTM_LAUNCH("lstm_rec_bwd", (lstm_rec_bwd_step<T, 1>), grid, dim3(256), 0, s, rb);
