@@ -97,6 +97,8 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   L.DYb = a; a = align256(a + (size_t)M * 2 * H * 4);
   L.DC = a; a = align256(a + (size_t)2 * d->B * H * 4);
   L.WT = a; a = align256(a + (size_t)2 * d->L * 4 * H * H * es);
+  // bf16: W_ih^T of layers 1.. (both directions side by side) for dX
+  L.WIT = a; a = align256(a + (es == 2 ? (size_t)(d->L - 1) * 2 * H * 8 * H * es : 0));
   L.CSP = a; a = align256(a + (size_t)64 * 8 * H * 4);
   // split-K plans and partial buffers of the backward GEMMs
   const int BMt = es == 2 ? GemmCfg<bf16>::BM : GemmCfg<float>::BM;
@@ -136,6 +138,9 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   L.sp_dy = plan_splits(M, 2 * H, P, BMt, BNt, BKt, 1);
   if (L.sp_dy > 1) hsk = std::max(hsk, (size_t)L.sp_dy * M * 2 * H * 4);
   L.HSKP = h; h = align256(h + hsk);
+  L.head_xposed = es == 2 && d->K % 8 == 0;
+  L.WST = h; h = align256(h + (L.head_xposed ? (size_t)P * d->K * es : 0));
+  L.WLT = h; h = align256(h + (L.head_xposed ? (size_t)2 * H * P * es : 0));
   L.head_bytes = h;
   L.ytop_bytes = (size_t)M * 2 * H * es;
   return BLSTM_OK;

@@ -73,10 +73,11 @@ struct Layout {
   int64_t Wih[MAX_LAYERS][2], Whh[MAX_LAYERS][2], bih[MAX_LAYERS][2], bhh[MAX_LAYERS][2];
   int64_t Wl, bl, Ws, bs;
   // act_ws byte offsets
-  size_t X0, Y[MAX_LAYERS], G[MAX_LAYERS], C[MAX_LAYERS], GX, DYa, DYb, DC, WT, CSP, SKP, SYNC, XCH;
+  size_t X0, Y[MAX_LAYERS], G[MAX_LAYERS], C[MAX_LAYERS], GX, DYa, DYb, DC, WT, WIT, CSP, SKP, SYNC, XCH;
   size_t act_bytes;
   // head_ws byte offsets
-  size_t Z, S, RL, DZ, DZT, HCSP, HSKP;
+  size_t Z, S, RL, DZ, DZT, HCSP, HSKP, WST, WLT;
+  bool head_xposed;   // bf16 with K % 8 == 0: dz and dy use transposed weight copies
   size_t head_bytes;
   size_t ytop_bytes;
   // split-K factors of the weight/input-gradient GEMMs (1 = direct store)

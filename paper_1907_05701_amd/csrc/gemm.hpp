@@ -363,10 +363,8 @@ static inline void gemm_launch(const char* name, hipStream_t s, const Opnd& A, c
                                int64_t M, int64_t N, int64_t K, int batches, int splits,
                                const Epi& epi) {
   if constexpr (std::is_same<T, bf16>::value && AKC && BKC) {
-    if (splits == 1) {
-      gemm_launch_cfg<T, GemmCfgK32, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits, epi);
-      return;
-    }
+    gemm_launch_cfg<T, GemmCfgK32, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits, epi);
+    return;
   }
   gemm_launch_cfg<T, GemmCfg<T>, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits, epi);
 }

@@ -25,6 +25,7 @@
 #include "common.hpp"
 #include "gemm.hpp"
 #include "lstm_persist.hpp"
+#include "xpose.hpp"
 #include "reduce.hpp"
 
 template <typename T>
@@ -383,17 +384,41 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
   float* DC = (float*)(ws + lo.DC);
   float* part = (float*)(ws + lo.SKP);
   float* csp = (float*)(ws + lo.CSP);
-  bool have_wt = false;   // W_hh^T copies for the per-step kernels, made on first use
-  auto make_wt = [&]() {
-    TransposeSrc src;
-    for (int i = 0; i < 2 * MAX_LAYERS; ++i) src.p[i] = nullptr;
-    for (int l = 0; l < lo.L; ++l)
-      for (int d = 0; d < 2; ++d) src.p[2 * l + d] = W + lo.Whh[l][d];
-    BLSTM_LAUNCH("transpose_whh", transpose_kernel<T>,
-                 dim3((unsigned)cdiv(H, 32), (unsigned)cdiv(4 * H, 32), 2 * lo.L), dim3(256), 0, s,
-                 src, 4 * H, H, WT);
-    have_wt = true;
+  constexpr bool lp = std::is_same<T, bf16>::value;
+  T* WIT = (T*)(ws + lo.WIT);
+  // Transposed operand copies (bf16): W_ih^T of layers 1.. with both
+  // directions side by side, so dX is one K-contiguous product over 8H, and
+  // W_hh^T for the per-step BPTT kernels.  One launch makes all of them.
+  bool have_wt = false;
+  auto make_copies = [&](bool wih, bool whh) {
+    if constexpr (lp) {
+      XposeJobs jobs;
+      int n = 0;
+      if (whh)
+        for (int l = 0; l < lo.L; ++l)
+          for (int d = 0; d < 2; ++d)
+            jobs.j[n++] = XposeJob{(const bf16*)(W + lo.Whh[l][d]), (bf16*)(WT + (int64_t)(2 * l + d) * 4 * H * H),
+                                   H, 4 * H, 4 * H, H};
+      if (wih)
+        for (int l = 1; l < lo.L; ++l)
+          for (int d = 0; d < 2; ++d)
+            jobs.j[n++] = XposeJob{(const bf16*)(W + lo.Wih[l][d]),
+                                   (bf16*)(WIT + (int64_t)(l - 1) * 2 * H * 8 * H + (int64_t)d * 4 * H),
+                                   2 * H, 8 * H, 4 * H, 2 * H};
+      transpose_bf16("transpose_w", s, jobs, n);
+    } else {
+      if (!whh) return;
+      TransposeSrc src;
+      for (int i = 0; i < 2 * MAX_LAYERS; ++i) src.p[i] = nullptr;
+      for (int l = 0; l < lo.L; ++l)
+        for (int d = 0; d < 2; ++d) src.p[2 * l + d] = W + lo.Whh[l][d];
+      BLSTM_LAUNCH("transpose_whh", transpose_kernel<T>,
+                   dim3((unsigned)cdiv(H, 32), (unsigned)cdiv(4 * H, 32), 2 * lo.L), dim3(256), 0, s,
+                   src, 4 * H, H, WT);
+    }
+    if (whh) have_wt = true;
   };
+  make_copies(lp && lo.L > 1, !use_persistent<T>(H, lo.T, true, s));
   const float* dY = dytop;
   for (int l = lo.L - 1; l >= 0; --l) {
     const T* Xl = l == 0 ? (const T*)(ws + lo.X0) : (const T*)(ws + lo.Y[l - 1]);
@@ -410,7 +435,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       if (!done) (void)hipGetLastError();
     }
     if (!done) {
-      if (!have_wt) make_wt();
+      if (!have_wt) make_copies(false, true);
       RecBwdArgs<T> rb;
       rb.DA = DA; rb.WT0 = WT + (int64_t)(2 * l) * 4 * H * H; rb.WT1 = WT + (int64_t)(2 * l + 1) * 4 * H * H;
       rb.DY = dY; rb.G = Gl; rb.C = Cl; rb.DC = DC; rb.Tn = Tn; rb.B = B; rb.H = H;
@@ -443,12 +468,18 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     // dX_l = sum_d da_d W_ih[d]  (the gradient reaching the layer below)
     if (l > 0) {
       const Opnd A = opnd(DA, 8 * H, 8 * H, M);
-      Opnd Bw = opnd(W + lo.Wih[l][0], Dl, Dl, 8 * H);
-      Bw.seg = 4 * H;
-      Bw.segstride = lo.Wih[l][1] - lo.Wih[l][0];
       float* dst = (dY == (const float*)(ws + lo.DYa)) ? (float*)(ws + lo.DYb) : (float*)(ws + lo.DYa);
-      gemm_f32<T, true, false, V, V>("gemm_dx", s, A, Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst, Dl, 0,
-                                     part);
+      if constexpr (lp) {
+        const Opnd Bw = opnd(WIT + (int64_t)(l - 1) * 2 * H * 8 * H, 8 * H, 8 * H, Dl);
+        gemm_f32<T, true, true, V, V>("gemm_dx", s, A, Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst, Dl, 0,
+                                      part);
+      } else {
+        Opnd Bw = opnd(W + lo.Wih[l][0], Dl, Dl, 8 * H);
+        Bw.seg = 4 * H;
+        Bw.segstride = lo.Wih[l][1] - lo.Wih[l][0];
+        gemm_f32<T, true, false, V, V>("gemm_dx", s, A, Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst, Dl, 0,
+                                       part);
+      }
       dY = dst;
     }
   }

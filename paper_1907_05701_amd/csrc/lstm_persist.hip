@@ -33,6 +33,7 @@
 
 #include "common.hpp"
 #include "lstm_persist.hpp"
+#include "xpose.hpp"
 
 #define PU 32
 #define SPIN_LIMIT (1u << 18)
@@ -102,21 +103,6 @@ __device__ __forceinline__ void ll_fragments(const uint64_t* const (&rp)[MBW], i
                                  (uint32_t)w[m][kk][3]);
       af[m][kk] = __builtin_bit_cast(bf16x8, v);
     }
-}
-
-// 8x8 bf16 transpose: in[i] holds row i (8 values); out[j] gets column j.
-__device__ __forceinline__ void transpose8x8(const uint4 (&in)[8], uint4 (&out)[8]) {
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    uint32_t o4[4];
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const uint32_t lo = ((const uint32_t*)&in[2 * w])[j / 2];
-      const uint32_t hi = ((const uint32_t*)&in[2 * w + 1])[j / 2];
-      o4[w] = (j & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
-    }
-    out[j] = make_uint4(o4[0], o4[1], o4[2], o4[3]);
-  }
 }
 
 // ---------------------------------------------------------------------------
