@@ -99,6 +99,12 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   L.WT = a; a = align256(a + (size_t)2 * d->L * 4 * H * H * es);
   // bf16: W_ih^T of layers 1.. (both directions side by side) for dX
   L.WIT = a; a = align256(a + (es == 2 ? (size_t)(d->L - 1) * 2 * H * 8 * H * es : 0));
+  // bf16: K-contiguous (transposed) layer inputs/outputs for the weight gradients
+  L.xpose_act = es == 2 && d->B % 8 == 0;
+  for (int i = 0; i < 2; ++i) {
+    L.YT[i] = a;
+    a = align256(a + (L.xpose_act ? (size_t)std::max<int64_t>(2 * H, L.Dp0) * M * es : 0));
+  }
   L.CSP = a; a = align256(a + (size_t)64 * 8 * H * 4);
   // split-K plans and partial buffers of the backward GEMMs
   const int BMt = es == 2 ? GemmCfg<bf16>::BM : GemmCfg<float>::BM;

@@ -350,24 +350,11 @@ static inline void gemm_launch_cfg(const char* name, hipStream_t s, const Opnd& 
                grid, dim3(C::WM * C::WN * 64), 0, s, A, B, M, N, K, ksplit, splits, epi);
 }
 
-// K-contiguous x K-contiguous bf16 products run 32-deep k-tiles (measured
-// faster at the learner-step shapes on MI355X); products with an
-// MN-contiguous operand keep 64-deep tiles so that the 8x8 transposed staging
-// keeps every thread busy.
+// K-contiguous x K-contiguous bf16 products that the direct-to-LDS kernel
+// cannot take (unaligned rows) run 32-deep k-tiles.
 struct GemmCfgK32 {
   static constexpr int BM = 128, BN = 128, BK = 32, WM = 2, WN = 2;
 };
-
-template <typename T, bool AKC, bool BKC, int VA, int VB, class Epi>
-static inline void gemm_launch(const char* name, hipStream_t s, const Opnd& A, const Opnd& B,
-                               int64_t M, int64_t N, int64_t K, int batches, int splits,
-                               const Epi& epi) {
-  if constexpr (std::is_same<T, bf16>::value && AKC && BKC) {
-    gemm_launch_cfg<T, GemmCfgK32, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits, epi);
-    return;
-  }
-  gemm_launch_cfg<T, GemmCfg<T>, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits, epi);
-}
 
 // Fixed-order split-K reduction: dst[z][m][n] = sum_s part[z][s][m][n]
 // (part rows are N wide), optionally also a low-precision copy.

@@ -14,7 +14,7 @@
 
 #include "common.hpp"
 #include "xpose.hpp"
-#include "gemm.hpp"
+#include "gemm_kc.hpp"
 #include "reduce.hpp"
 
 __device__ __forceinline__ void lse_combine(float& m, float& s, float m2, float s2) {

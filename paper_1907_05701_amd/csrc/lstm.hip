@@ -23,7 +23,7 @@
 #include <type_traits>
 
 #include "common.hpp"
-#include "gemm.hpp"
+#include "gemm_kc.hpp"
 #include "lstm_persist.hpp"
 #include "xpose.hpp"
 #include "reduce.hpp"
@@ -446,20 +446,44 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
         BLSTM_LAUNCH("lstm_rec_bwd", (lstm_rec_bwd_step<T, 1>), grid, dim3(256), 0, s, rb);
       }
     }
-    // dW_ih[d] = da_d^T X_l  (4H x D_l, reduction over all frames)
-    {
+    const int64_t Kr = (int64_t)(Tn - 1) * B;
+    bool dw_done = false;
+    if constexpr (lp) {
+      if (lo.xpose_act) {
+        // K-contiguous (frame-contiguous) copies for the weight gradients: da^T
+        // over G[l] (BPTT of this layer is done with it), X_l^T into the buffer
+        // that held Y_{l+1}^T; Y_l^T was made one layer up (or from y_top).
+        T* DAT = (T*)(ws + lo.G[l]);
+        T* YTl = (T*)(ws + lo.YT[l & 1]);
+        T* XTl = (T*)(ws + lo.YT[(l + 1) & 1]);
+        XposeJobs jobs;
+        int n = 0;
+        jobs.j[n++] = XposeJob{(const bf16*)DA, (bf16*)DAT, 8 * H, M, (int)M, 8 * H};
+        if (l == lo.L - 1) jobs.j[n++] = XposeJob{(const bf16*)Yl, (bf16*)YTl, 2 * H, M, (int)M, 2 * H};
+        jobs.j[n++] = XposeJob{(const bf16*)Xl, (bf16*)XTl, Dpl, M, (int)M, Dpl};
+        transpose_bf16("transpose_act", s, jobs, n);
+        // dW_ih[d] = da_d^T X_l  (4H x D_l, reduction over all frames)
+        gemm_f32<T, true, true, V, V>("gemm_dwih", s, opnd(DAT, M, (int)M, 4 * H, 4 * H * M),
+                                      opnd(XTl, M, (int)M, Dl), 4 * H, Dl, M, 2, lo.sp_dWih[l], grad + lo.Wih[l][0], Dl,
+                                      lo.Wih[l][1] - lo.Wih[l][0], part);
+        // dW_hh[d] = sum_t da_d[t]^T h_d[t_prev] (frames shifted as below)
+        gemm_f32<T, true, true, V, V>("gemm_dwhh", s, opnd(DAT + B, M, (int)Kr, 4 * H, 4 * H * M - B),
+                                      opnd(YTl, M, (int)Kr, H, (int64_t)H * M + B), 4 * H, H, Kr, 2, lo.sp_dWhh,
+                                      grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part);
+        dw_done = true;
+      }
+    }
+    if (!dw_done) {
+      // dW_ih[d] = da_d^T X_l  (4H x D_l, reduction over all frames)
       const Opnd A = opnd(DA, 8 * H, 4 * H, M, 4 * H);
       const Opnd Bx = opnd(Xl, Dpl, Dpl, M);
       gemm_f32<T, false, false, V, V>("gemm_dwih", s, A, Bx, 4 * H, Dl, M, 2, lo.sp_dWih[l],
                                       grad + lo.Wih[l][0], Dl, lo.Wih[l][1] - lo.Wih[l][0], part);
-    }
-    // dW_hh[d] = sum_t da_d[t]^T h_d[t_prev]: frames shifted by one step, the
-    // forward direction pairing t with t-1 and the reverse direction t with t+1
-    {
-      const int64_t Kr = (int64_t)(Tn - 1) * B;
-      const Opnd A = opnd(DA + (int64_t)B * 8 * H, 8 * H, 4 * H, Kr, 4 * H - (int64_t)B * 8 * H);
+      // dW_hh[d] = sum_t da_d[t]^T h_d[t_prev]: frames shifted by one step, the
+      // forward direction pairing t with t-1 and the reverse direction t with t+1
+      const Opnd Ad = opnd(DA + (int64_t)B * 8 * H, 8 * H, 4 * H, Kr, 4 * H - (int64_t)B * 8 * H);
       const Opnd Bh = opnd(Yl, 2 * H, H, Kr, (int64_t)B * 2 * H + H);
-      gemm_f32<T, false, false, V, V>("gemm_dwhh", s, A, Bh, 4 * H, H, Kr, 2, lo.sp_dWhh,
+      gemm_f32<T, false, false, V, V>("gemm_dwhh", s, Ad, Bh, 4 * H, H, Kr, 2, lo.sp_dWhh,
                                       grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part);
     }
     // db_ih = db_hh = sum over frames of da

@@ -3,7 +3,7 @@
 #pragma once
 
 #include "common.hpp"
-#include "gemm.hpp"
+#include "gemm_kc.hpp"
 
 #define COLSUM_CHUNKS 64
 
