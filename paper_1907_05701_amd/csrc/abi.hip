@@ -105,7 +105,9 @@ int make_layout(const blstm_dims* d, Layout* lo) {
     L.YT[i] = a;
     a = align256(a + (L.xpose_act ? (size_t)std::max<int64_t>(2 * H, L.Dp0) * M * es : 0));
   }
-  L.CSP = a; a = align256(a + (size_t)64 * 8 * H * 4);
+  L.DAT = a; a = align256(a + (L.xpose_act ? (size_t)M * 8 * H * es : 0));   // da^T [8H][M]
+  L.DBP = a; a = align256(a + (size_t)d->T * cdiv(d->B, 16) * 8 * H * 4);   // per-step bias partials
+  L.CSP = a; a = align256(a + (size_t)COLSUM_MAX_CHUNKS * 8 * H * 4);
   // split-K plans and partial buffers of the backward GEMMs
   const int BMt = es == 2 ? GemmCfg<bf16>::BM : GemmCfg<float>::BM;
   const int BNt = es == 2 ? GemmCfg<bf16>::BN : GemmCfg<float>::BN;
@@ -133,7 +135,7 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   L.RL = h; h = align256(h + (size_t)M * 4);
   L.DZ = h; h = align256(h + (size_t)M * P * 4);
   L.DZT = h; h = align256(h + (size_t)M * P * es);
-  L.HCSP = h; h = align256(h + (size_t)64 * std::max<int64_t>(L.Kp, P) * 4);
+  L.HCSP = h; h = align256(h + (size_t)COLSUM_MAX_CHUNKS * std::max<int64_t>(L.Kp, P) * 4);
   size_t hsk = 0;
   L.sp_dz = plan_splits(M, P, d->K, BMt, BNt, BKt, 1);
   hsk = std::max(hsk, (size_t)L.sp_dz * M * P * 4);  // dz always goes through partials

@@ -16,6 +16,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 #define MAX_LAYERS 16
 #define MAX_REPLICAS 16
+#define COLSUM_MAX_CHUNKS 256   // row ranges of the two-pass column sums
 
 // ---------------------------------------------------------------------------
 // Element conversion.  float -> bf16 is round-to-nearest-even (the compiler
@@ -73,7 +74,7 @@ struct Layout {
   int64_t Wih[MAX_LAYERS][2], Whh[MAX_LAYERS][2], bih[MAX_LAYERS][2], bhh[MAX_LAYERS][2];
   int64_t Wl, bl, Ws, bs;
   // act_ws byte offsets
-  size_t X0, Y[MAX_LAYERS], G[MAX_LAYERS], C[MAX_LAYERS], GX, DYa, DYb, DC, WT, WIT, YT[2], CSP, SKP, SYNC, XCH;
+  size_t X0, Y[MAX_LAYERS], G[MAX_LAYERS], C[MAX_LAYERS], GX, DYa, DYb, DC, WT, WIT, YT[2], DAT, DBP, CSP, SKP, SYNC, XCH;
   bool xpose_act;     // bf16 with B % 8 == 0: weight gradients from transposed activations
   size_t act_bytes;
   // head_ws byte offsets

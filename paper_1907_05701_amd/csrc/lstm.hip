@@ -156,6 +156,9 @@ struct RecBwdArgs {
   const T* G;        // saved gates [M][8H]
   const float* C;    // saved cell states [M][2H]
   float* DC;         // carried cell gradient [2][B][H]
+  T* DAT;            // optional: da also written frame-contiguous, [8H][M]
+  float* DBP;        // optional: per-(step, 16-row block) sums of da, [Tn][B/16][8H]
+  int64_t M;
   int Tn, B, H, tau;
 };
 
@@ -214,21 +217,51 @@ __global__ __launch_bounds__(256) void lstm_rec_bwd_step(const RecBwdArgs<T> a) 
 #pragma unroll
   for (int j = 0; j < KP - 1; ++j) acc += red[j][mb][lane];
 
+  float dav[4][4];   // [row r][gate]
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int b = rb * 16 * MBK + mb * 16 + (lane >> 4) * 4 + r;
-    if (b >= B) continue;
-    const int64_t row = (int64_t)t * B + b;
     const float ig = gt[r][0], fg = gt[r][1], gg = gt[r][2], og = gt[r][3];
     const float dh = acc[r] + dy[r];
     const float tc = tanhf_(cc[r]);
     const float dc = dh * og * (1.f - tc * tc) + dcn[r];
+    const bool ok = b < B;
+    dav[r][0] = ok ? dc * gg * ig * (1.f - ig) : 0.f;
+    dav[r][1] = ok ? dc * cpv[r] * fg * (1.f - fg) : 0.f;
+    dav[r][2] = ok ? dc * ig * (1.f - gg * gg) : 0.f;
+    dav[r][3] = ok ? dh * tc * og * (1.f - og) : 0.f;
+    if (!ok) continue;
+    const int64_t row = (int64_t)t * B + b;
     a.DC[((int64_t)d * B + b) * H + u] = dc * fg;
     T* da = a.DA + row * 8 * H + (int64_t)d * 4 * H + u;
-    da[0] = from_f32<T>(dc * gg * ig * (1.f - ig));
-    da[H] = from_f32<T>(dc * cpv[r] * fg * (1.f - fg));
-    da[2 * H] = from_f32<T>(dc * ig * (1.f - gg * gg));
-    da[3 * H] = from_f32<T>(dh * tc * og * (1.f - og));
+#pragma unroll
+    for (int g = 0; g < 4; ++g) da[g * H] = from_f32<T>(dav[r][g]);
+  }
+  const int b0 = rb * 16 * MBK + mb * 16 + (lane >> 4) * 4;
+  if (a.DAT && b0 < B) {
+    // 4 consecutive frames of one gate row: one 8-byte store (B % 4 == 0)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      T* p = a.DAT + ((int64_t)d * 4 * H + g * H + u) * a.M + (int64_t)t * B + b0;
+      if constexpr (sizeof(T) == 2) {
+        const bf16 v[4] = {(bf16)dav[0][g], (bf16)dav[1][g], (bf16)dav[2][g], (bf16)dav[3][g]};
+        *(uint2*)p = *(const uint2*)v;
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) p[r] = from_f32<T>(dav[r][g]);
+      }
+    }
+  }
+  if (a.DBP) {
+    // bias gradient partial: the 16 rows of this block, in a fixed order
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      float sg = (dav[0][g] + dav[1][g]) + (dav[2][g] + dav[3][g]);
+      sg += __shfl_xor(sg, 16);
+      sg += __shfl_xor(sg, 32);
+      if (lane < 16)
+        a.DBP[((int64_t)a.tau * gridDim.y * MBK + rb * MBK + mb) * 8 * H + (int64_t)d * 4 * H + g * H + u] = sg;
+    }
   }
 }
 
@@ -427,7 +460,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     const T* Gl = (const T*)(ws + lo.G[l]);
     const float* Cl = (const float*)(ws + lo.C[l]);
     // BPTT over the chunk, both directions at once
-    bool done = false;
+    bool done = false, step_fused = false;
     if (use_persistent<T>(H, lo.T, true, s)) {
       PersistArgs pa = persist_args(lo, (const bf16*)W, ws, l);
       pa.DA = (bf16*)DA; pa.DY = dY; pa.C = (float*)Cl; pa.G = (bf16*)Gl;
@@ -439,26 +472,31 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       RecBwdArgs<T> rb;
       rb.DA = DA; rb.WT0 = WT + (int64_t)(2 * l) * 4 * H * H; rb.WT1 = WT + (int64_t)(2 * l + 1) * 4 * H * H;
       rb.DY = dY; rb.G = Gl; rb.C = Cl; rb.DC = DC; rb.Tn = Tn; rb.B = B; rb.H = H;
+      rb.DAT = lo.xpose_act ? (T*)(ws + lo.DAT) : nullptr;
+      rb.DBP = (float*)(ws + lo.DBP);
+      rb.M = M;
       const dim3 grid(H / 16, (unsigned)cdiv(B, 16), 2);
       TimedRun timed("lstm_rec_bwd", s, Tn);
       for (int tau = 0; tau < Tn; ++tau) {
         rb.tau = tau;
         BLSTM_LAUNCH("lstm_rec_bwd", (lstm_rec_bwd_step<T, 1>), grid, dim3(256), 0, s, rb);
       }
+      step_fused = true;
     }
     const int64_t Kr = (int64_t)(Tn - 1) * B;
     bool dw_done = false;
     if constexpr (lp) {
       if (lo.xpose_act) {
         // K-contiguous (frame-contiguous) copies for the weight gradients: da^T
-        // over G[l] (BPTT of this layer is done with it), X_l^T into the buffer
-        // that held Y_{l+1}^T; Y_l^T was made one layer up (or from y_top).
-        T* DAT = (T*)(ws + lo.G[l]);
+        // (written by the per-step BPTT kernel, else transposed here), X_l^T
+        // into the buffer that held Y_{l+1}^T; Y_l^T was made one layer up (or
+        // from y_top).
+        T* DAT = (T*)(ws + lo.DAT);
         T* YTl = (T*)(ws + lo.YT[l & 1]);
         T* XTl = (T*)(ws + lo.YT[(l + 1) & 1]);
         XposeJobs jobs;
         int n = 0;
-        jobs.j[n++] = XposeJob{(const bf16*)DA, (bf16*)DAT, 8 * H, M, (int)M, 8 * H};
+        if (!step_fused) jobs.j[n++] = XposeJob{(const bf16*)DA, (bf16*)DAT, 8 * H, M, (int)M, 8 * H};
         if (l == lo.L - 1) jobs.j[n++] = XposeJob{(const bf16*)Yl, (bf16*)YTl, 2 * H, M, (int)M, 2 * H};
         jobs.j[n++] = XposeJob{(const bf16*)Xl, (bf16*)XTl, Dpl, M, (int)M, Dpl};
         transpose_bf16("transpose_act", s, jobs, n);
@@ -487,8 +525,12 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
                                       grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part);
     }
     // db_ih = db_hh = sum over frames of da
-    colsum<T>("colsum_db", s, DA, M, 8 * H, 8 * H, csp, 4 * H, lo.bih[l][1] - lo.bih[l][0],
-              grad + lo.bih[l][0], grad + lo.bhh[l][0]);
+    if (step_fused)
+      colsum_parts("colsum_db", s, (const float*)(ws + lo.DBP), Tn * (int)cdiv(B, 16), 8 * H, 4 * H,
+                   lo.bih[l][1] - lo.bih[l][0], grad + lo.bih[l][0], grad + lo.bhh[l][0]);
+    else
+      colsum<T>("colsum_db", s, DA, M, 8 * H, 8 * H, csp, 4 * H, lo.bih[l][1] - lo.bih[l][0],
+                grad + lo.bih[l][0], grad + lo.bhh[l][0]);
     // dX_l = sum_d da_d W_ih[d]  (the gradient reaching the layer below)
     if (l > 0) {
       const Opnd A = opnd(DA, 8 * H, 8 * H, M);

@@ -5,45 +5,84 @@
 #include "common.hpp"
 #include "gemm_kc.hpp"
 
-#define COLSUM_CHUNKS 64
-
 // Column sums of an [M][N] matrix (row pitch ld) in two fixed-order passes:
-// COLSUM_CHUNKS row ranges each summed in order, then the ranges in order.
-template <typename T>
+// `chunks` row ranges each summed in order (VEC adjacent columns per thread,
+// one 16-byte load per row when the rows allow it), then the ranges in order.
+template <typename T, int VEC>
 __global__ __launch_bounds__(256) void colsum_partial_kernel(const T* __restrict__ X, int64_t M,
-                                                             int64_t N, int64_t ld,
+                                                             int64_t N, int64_t ld, int chunks,
                                                              float* __restrict__ part) {
-  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t c = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC;
   if (c >= N) return;
-  const int64_t rpc = cdiv(M, COLSUM_CHUNKS);
+  const int64_t rpc = cdiv(M, chunks);
   const int64_t r0 = (int64_t)blockIdx.y * rpc, r1 = min(M, r0 + rpc);
-  float s = 0.f;
-  for (int64_t r = r0; r < r1; ++r) s += to_f32(X[r * ld + c]);
-  part[(int64_t)blockIdx.y * N + c] = s;
+  float s[VEC];
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) s[v] = 0.f;
+  if constexpr (VEC == 1) {
+    for (int64_t r = r0; r < r1; ++r) s[0] += to_f32(X[r * ld + c]);
+  } else {
+    typedef typename VecOf<VEC * (int)sizeof(T)>::type V;
+#pragma unroll 4
+    for (int64_t r = r0; r < r1; ++r) {
+      const V x = *(const V*)(X + r * ld + c);
+      const T* e = (const T*)&x;
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) s[v] += to_f32(e[v]);
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) part[(int64_t)blockIdx.y * N + c + v] = s[v];
 }
 
+// Sum of `nparts` partial rows per column, in part order: four threads per
+// column each add a contiguous quarter, the quarters are added in order.
 // out1/out2 are written at (c / seg) * segstride + c % seg.
 __global__ __launch_bounds__(256) static void colsum_final_kernel(const float* __restrict__ part,
-                                                                  int64_t N, int64_t seg,
+                                                                  int nparts, int64_t N, int64_t seg,
                                                                   int64_t segstride, float* out1,
                                                                   float* out2) {
-  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= N) return;
-  float s = part[c];
-  for (int k = 1; k < COLSUM_CHUNKS; ++k) s += part[(int64_t)k * N + c];
+  __shared__ float q4[4][64];
+  const int cl = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int64_t c = (int64_t)blockIdx.x * 64 + cl;
+  const int per = (nparts + 3) / 4;
+  const int p0 = q * per, p1 = min(nparts, p0 + per);
+  float s = 0.f;
+  if (c < N) {
+#pragma unroll 8
+    for (int k = p0; k < p1; ++k) s += part[(int64_t)k * N + c];
+  }
+  q4[q][cl] = s;
+  __syncthreads();
+  if (q != 0 || c >= N) return;
+  const float t = ((q4[0][cl] + q4[1][cl]) + q4[2][cl]) + q4[3][cl];
   const int64_t o = (c / seg) * segstride + c % seg;
-  out1[o] = s;
-  if (out2) out2[o] = s;
+  out1[o] = t;
+  if (out2) out2[o] = t;
+}
+
+static inline void colsum_parts(const char* name, hipStream_t s, const float* part, int nparts, int64_t N,
+                                int64_t seg, int64_t segstride, float* out1, float* out2) {
+  BLSTM_LAUNCH(name, colsum_final_kernel, dim3((unsigned)cdiv(N, 64)), dim3(256), 0, s, part, nparts, N, seg,
+               segstride, out1, out2);
 }
 
 template <typename T>
 static inline void colsum(const char* name, hipStream_t s, const T* X, int64_t M, int64_t N,
                           int64_t ld, float* part, int64_t seg, int64_t segstride, float* out1,
                           float* out2) {
-  BLSTM_LAUNCH(name, colsum_partial_kernel<T>, dim3((unsigned)cdiv(N, 256), COLSUM_CHUNKS), dim3(256),
-               0, s, X, M, N, ld, part);
-  BLSTM_LAUNCH("colsum_final", colsum_final_kernel, dim3((unsigned)cdiv(N, 256)), dim3(256), 0, s,
-               part, N, seg, segstride, out1, out2);
+  constexpr int VEC = 16 / (int)sizeof(T);
+  const bool vec = N % VEC == 0 && ld % VEC == 0 && ((uintptr_t)X & 15) == 0;
+  const int64_t xb = cdiv(N, 256 * (vec ? VEC : 1));
+  int chunks = (int)std::min<int64_t>(COLSUM_MAX_CHUNKS, std::max<int64_t>(16, cdiv(2048, xb)));
+  chunks = (int)std::max<int64_t>(1, std::min<int64_t>(chunks, M));
+  if (vec)
+    BLSTM_LAUNCH(name, (colsum_partial_kernel<T, VEC>), dim3((unsigned)xb, (unsigned)chunks), dim3(256), 0, s, X,
+                 M, N, ld, chunks, part);
+  else
+    BLSTM_LAUNCH(name, (colsum_partial_kernel<T, 1>), dim3((unsigned)xb, (unsigned)chunks), dim3(256), 0, s, X, M,
+                 N, ld, chunks, part);
+  colsum_parts("colsum_final", s, part, chunks, N, seg, segstride, out1, out2);
 }
 
 // C = A B with a float32 destination (ld, dst_zstride per batch).  With
