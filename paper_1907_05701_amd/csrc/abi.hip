@@ -30,10 +30,15 @@ int blstm_check_launch(const char* what) {
 
 extern "C" const char* blstm_last_error(void) { return g_err; }
 
-int plan_splits(int64_t Mo, int64_t No, int64_t Kr, int BMt, int BNt, int BK, int batches) {
+// Split-K factor of a product with Mo x No outputs (per batch) and Kr-long
+// reductions: enough workgroups to cover the chip, at least 4 k-tiles per
+// split, below 256 tiles.  bf16 (direct-to-LDS kernel) aims at 256
+// workgroups (measured: more splits cost more in the partial reduction than
+// they gain), float32 at 512.
+int plan_splits(int64_t Mo, int64_t No, int64_t Kr, int BMt, int BNt, int BK, int batches, bool lp) {
   const int64_t tiles = cdiv(Mo, BMt) * cdiv(No, BNt) * batches;
   if (tiles >= 256) return 1;
-  int64_t s = cdiv(512, tiles);
+  int64_t s = cdiv(lp ? 256 : 512, tiles);
   const int64_t kt = cdiv(Kr, BK);
   s = std::min<int64_t>(s, std::max<int64_t>(kt / 4, 1));
   s = std::min<int64_t>(s, 16);
@@ -113,13 +118,13 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   const int BNt = es == 2 ? GemmCfg<bf16>::BN : GemmCfg<float>::BN;
   const int BKt = es == 2 ? GemmCfg<bf16>::BK : GemmCfg<float>::BK;
   size_t skp = 0;
-  L.sp_dWhh = plan_splits(4 * H, H, (int64_t)(d->T - 1) * d->B, BMt, BNt, BKt, 2);
+  L.sp_dWhh = plan_splits(4 * H, H, (int64_t)(d->T - 1) * d->B, BMt, BNt, BKt, 2, es == 2);
   if (L.sp_dWhh > 1) skp = std::max(skp, (size_t)L.sp_dWhh * 2 * 4 * H * H * 4);
   for (int l = 0; l < d->L; ++l) {
     const int64_t Dl = l == 0 ? d->D : 2 * H;
-    L.sp_dWih[l] = plan_splits(4 * H, Dl, M, BMt, BNt, BKt, 2);
+    L.sp_dWih[l] = plan_splits(4 * H, Dl, M, BMt, BNt, BKt, 2, es == 2);
     if (L.sp_dWih[l] > 1) skp = std::max(skp, (size_t)L.sp_dWih[l] * 2 * 4 * H * Dl * 4);
-    L.sp_dX[l] = l > 0 ? plan_splits(M, Dl, 8 * H, BMt, BNt, BKt, 1) : 1;
+    L.sp_dX[l] = l > 0 ? plan_splits(M, Dl, 8 * H, BMt, BNt, BKt, 1, es == 2) : 1;
     if (L.sp_dX[l] > 1) skp = std::max(skp, (size_t)L.sp_dX[l] * M * Dl * 4);
   }
   L.SKP = a; a = align256(a + skp);
@@ -137,13 +142,13 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   L.DZT = h; h = align256(h + (size_t)M * P * es);
   L.HCSP = h; h = align256(h + (size_t)COLSUM_MAX_CHUNKS * std::max<int64_t>(L.Kp, P) * 4);
   size_t hsk = 0;
-  L.sp_dz = plan_splits(M, P, d->K, BMt, BNt, BKt, 1);
+  L.sp_dz = plan_splits(M, P, d->K, BMt, BNt, BKt, 1, es == 2);
   hsk = std::max(hsk, (size_t)L.sp_dz * M * P * 4);  // dz always goes through partials
-  L.sp_dWs = plan_splits(d->K, P, M, BMt, BNt, BKt, 1);
+  L.sp_dWs = plan_splits(d->K, P, M, BMt, BNt, BKt, 1, es == 2);
   if (L.sp_dWs > 1) hsk = std::max(hsk, (size_t)L.sp_dWs * d->K * P * 4);
-  L.sp_dWl = plan_splits(P, 2 * H, M, BMt, BNt, BKt, 1);
+  L.sp_dWl = plan_splits(P, 2 * H, M, BMt, BNt, BKt, 1, es == 2);
   if (L.sp_dWl > 1) hsk = std::max(hsk, (size_t)L.sp_dWl * P * 2 * H * 4);
-  L.sp_dy = plan_splits(M, 2 * H, P, BMt, BNt, BKt, 1);
+  L.sp_dy = plan_splits(M, 2 * H, P, BMt, BNt, BKt, 1, es == 2);
   if (L.sp_dy > 1) hsk = std::max(hsk, (size_t)L.sp_dy * M * 2 * H * 4);
   L.HSKP = h; h = align256(h + hsk);
   L.head_xposed = es == 2 && d->K % 8 == 0;

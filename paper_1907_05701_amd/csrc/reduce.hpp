@@ -85,6 +85,29 @@ static inline void colsum(const char* name, hipStream_t s, const T* X, int64_t M
   colsum_parts("colsum_final", s, part, chunks, N, seg, segstride, out1, out2);
 }
 
+// The same reduction, 4 adjacent columns per thread: block (m, column block
+// of 256, batch), 64 threads.  Needs N, ld, ldc multiples of 4 and aligned
+// destinations.
+template <typename TC>
+__global__ __launch_bounds__(64) void splitk_reduce4_kernel(const float* __restrict__ part, int splits, int64_t M,
+                                                            int64_t N, float* dst, int64_t ld, int64_t dst_zstride,
+                                                            TC* dstc, int64_t ldc) {
+  const int64_t m = blockIdx.x, n = ((int64_t)blockIdx.y * 64 + threadIdx.x) * 4;
+  const int z = blockIdx.z;
+  if (n >= N) return;
+  const float* p = part + ((int64_t)z * splits * M + m) * N + n;
+  float4 acc = *(const float4*)p;
+  for (int k = 1; k < splits; ++k) {
+    const float4 v = *(const float4*)(p + (int64_t)k * M * N);
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  *(float4*)(dst + z * dst_zstride + m * ld + n) = acc;
+  if (dstc) {
+    TC* c = dstc + m * ldc + n;
+    c[0] = from_f32<TC>(acc.x); c[1] = from_f32<TC>(acc.y); c[2] = from_f32<TC>(acc.z); c[3] = from_f32<TC>(acc.w);
+  }
+}
+
 // C = A B with a float32 destination (ld, dst_zstride per batch).  With
 // splits > 1 (or when a low-precision copy dstc is wanted) the product goes
 // through split-K partials and the fixed-order reduction.
@@ -99,6 +122,12 @@ static inline void gemm_f32(const char* name, hipStream_t s, const Opnd& A, cons
   }
   gemm_launch<T, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits,
                                    epi_store<float>(part, N, M, N, (int64_t)splits * M * N, M * N));
+  if (N % 4 == 0 && ld % 4 == 0 && dst_zstride % 4 == 0 && ((uintptr_t)dst & 15) == 0 &&
+      (!dstc || (ldc % 4 == 0 && ((uintptr_t)dstc & 7) == 0))) {
+    BLSTM_LAUNCH("splitk_reduce", splitk_reduce4_kernel<T>, dim3((unsigned)M, (unsigned)cdiv(N, 256), batches),
+                 dim3(64), 0, s, part, splits, M, N, dst, ld, dst_zstride, dstc, ldc);
+    return;
+  }
   const int64_t total = (int64_t)batches * M * N;
   const unsigned grid = (unsigned)std::min<int64_t>(cdiv(total, 256), 8192);
   BLSTM_LAUNCH("splitk_reduce", splitk_reduce_kernel<T>, dim3(grid), dim3(256), 0, s, part, splits,
