@@ -110,8 +110,11 @@ int make_layout(const blstm_dims* d, Layout* lo) {
     L.YT[i] = a;
     a = align256(a + (L.xpose_act ? (size_t)std::max<int64_t>(2 * H, L.Dp0) * M * es : 0));
   }
-  L.DAT = a; a = align256(a + (L.xpose_act ? (size_t)M * 8 * H * es : 0));   // da^T [8H][M]
-  L.DBP = a; a = align256(a + (size_t)d->T * cdiv(d->B, 16) * 8 * H * 4);   // per-step bias partials
+  // da^T [8H][M] and per-step bias partials, two of each (alternating layers)
+  L.dat_bytes = align256(L.xpose_act ? (size_t)M * 8 * H * es : 0);
+  L.DAT = a; a += 2 * L.dat_bytes;
+  L.dbp_bytes = align256((size_t)d->T * cdiv(d->B, 16) * 8 * H * 4);
+  L.DBP = a; a += 2 * L.dbp_bytes;
   L.CSP = a; a = align256(a + (size_t)COLSUM_MAX_CHUNKS * 8 * H * 4);
   // split-K plans and partial buffers of the backward GEMMs
   const int BMt = es == 2 ? GemmCfg<bf16>::BM : GemmCfg<float>::BM;
@@ -128,6 +131,7 @@ int make_layout(const blstm_dims* d, Layout* lo) {
     if (L.sp_dX[l] > 1) skp = std::max(skp, (size_t)L.sp_dX[l] * M * Dl * 4);
   }
   L.SKP = a; a = align256(a + skp);
+  L.SKP2 = a; a = align256(a + skp);   // split-K partials of the side-stream products
   L.SYNC = a; a = align256(a + 256);                            // status word
   L.XCH = a; a = align256(a + persist_xch_bytes(d->B, d->H));   // recurrent step exchange
   L.act_bytes = a;

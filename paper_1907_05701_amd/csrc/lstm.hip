@@ -22,6 +22,8 @@
 
 #include <type_traits>
 
+#include <mutex>
+
 #include "common.hpp"
 #include "gemm_kc.hpp"
 #include "lstm_persist.hpp"
@@ -406,6 +408,38 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
   return blstm_check_launch("blstm_fwd");
 }
 
+// Side stream for the weight-gradient work of a layer, which then runs
+// concurrently with the BPTT of the layer below (it depends only on that
+// layer's da, which the per-step kernels write in their own buffer).  One
+// non-blocking stream at default priority and 2 events per layer, per device,
+// created on first use; used for eager calls only.  ADPSGD_BLSTM_OVERLAP=0
+// keeps everything on the caller's stream.
+struct SideStream {
+  hipStream_t st = nullptr;
+  hipEvent_t bptt_done[MAX_LAYERS] = {}, dw_done[MAX_LAYERS] = {};
+  bool ok = false, tried = false;
+};
+static SideStream* side_stream() {
+  static SideStream per_dev[64];
+  static std::mutex mu;
+  const char* env = getenv("ADPSGD_BLSTM_OVERLAP");
+  if (env && atoi(env) == 0) return nullptr;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  SideStream& ss = per_dev[dev];
+  if (!ss.tried) {
+    ss.tried = true;
+    bool ok = hipStreamCreateWithFlags(&ss.st, hipStreamNonBlocking) == hipSuccess;
+    for (int i = 0; ok && i < MAX_LAYERS; ++i)
+      ok = hipEventCreateWithFlags(&ss.bptt_done[i], hipEventDisableTiming) == hipSuccess &&
+           hipEventCreateWithFlags(&ss.dw_done[i], hipEventDisableTiming) == hipSuccess;
+    ss.ok = ok;
+    if (!ok) (void)hipGetLastError();
+  }
+  return ss.ok ? &ss : nullptr;
+}
+
 template <typename T>
 static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const float* dytop,
                     float* grad, hipStream_t s) {
@@ -452,8 +486,24 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     if (whh) have_wt = true;
   };
   make_copies(lp && lo.L > 1, !use_persistent<T>(H, lo.T, true, s));
+  // weight gradients on the side stream (bf16 per-step BPTT writing da^T):
+  // layer l's buffers (da^T, bias partials, split-K partials) alternate by
+  // layer parity, so BPTT of layer l waits only for the side work of l+2
+  SideStream* side = nullptr;
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cap) != hipSuccess) { (void)hipGetLastError(); cap = hipStreamCaptureStatusActive; }
+  // not under stream capture: replaying graphs with these parallel branches
+  // measured far slower on MI355X than the serial graph
+  if (lp && lo.xpose_act && cap == hipStreamCaptureStatusNone && !use_persistent<T>(H, lo.T, true, s))
+    side = side_stream();
+  hipStream_t ss = side ? side->st : s;
+  float* part_side = side ? (float*)(ws + lo.SKP2) : part;
   const float* dY = dytop;
   for (int l = lo.L - 1; l >= 0; --l) {
+    const int par = side ? (l & 1) : 0;
+    T* DATl = (T*)(ws + lo.DAT + par * lo.dat_bytes);
+    float* DBPl = (float*)(ws + lo.DBP + par * lo.dbp_bytes);
+    if (side && l + 2 < lo.L) (void)hipStreamWaitEvent(s, side->dw_done[l + 2], 0);
     const T* Xl = l == 0 ? (const T*)(ws + lo.X0) : (const T*)(ws + lo.Y[l - 1]);
     const int Dl = lo.layer_in(l), Dpl = lo.layer_in_pitch(l);
     const T* Yl = l == lo.L - 1 ? ytop : (const T*)(ws + lo.Y[l]);
@@ -472,8 +522,8 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       RecBwdArgs<T> rb;
       rb.DA = DA; rb.WT0 = WT + (int64_t)(2 * l) * 4 * H * H; rb.WT1 = WT + (int64_t)(2 * l + 1) * 4 * H * H;
       rb.DY = dY; rb.G = Gl; rb.C = Cl; rb.DC = DC; rb.Tn = Tn; rb.B = B; rb.H = H;
-      rb.DAT = lo.xpose_act ? (T*)(ws + lo.DAT) : nullptr;
-      rb.DBP = (float*)(ws + lo.DBP);
+      rb.DAT = lo.xpose_act ? DATl : nullptr;
+      rb.DBP = DBPl;
       rb.M = M;
       const dim3 grid(H / 16, (unsigned)cdiv(B, 16), 2);
       TimedRun timed("lstm_rec_bwd", s, Tn);
@@ -483,6 +533,10 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       }
       step_fused = true;
     }
+    if (side) {
+      (void)hipEventRecord(side->bptt_done[l], s);
+      (void)hipStreamWaitEvent(ss, side->bptt_done[l], 0);
+    }
     const int64_t Kr = (int64_t)(Tn - 1) * B;
     bool dw_done = false;
     if constexpr (lp) {
@@ -491,7 +545,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
         // (written by the per-step BPTT kernel, else transposed here), X_l^T
         // into the buffer that held Y_{l+1}^T; Y_l^T was made one layer up (or
         // from y_top).
-        T* DAT = (T*)(ws + lo.DAT);
+        T* DAT = DATl;
         T* YTl = (T*)(ws + lo.YT[l & 1]);
         T* XTl = (T*)(ws + lo.YT[(l + 1) & 1]);
         XposeJobs jobs;
@@ -499,15 +553,15 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
         if (!step_fused) jobs.j[n++] = XposeJob{(const bf16*)DA, (bf16*)DAT, 8 * H, M, (int)M, 8 * H};
         if (l == lo.L - 1) jobs.j[n++] = XposeJob{(const bf16*)Yl, (bf16*)YTl, 2 * H, M, (int)M, 2 * H};
         jobs.j[n++] = XposeJob{(const bf16*)Xl, (bf16*)XTl, Dpl, M, (int)M, Dpl};
-        transpose_bf16("transpose_act", s, jobs, n);
+        transpose_bf16("transpose_act", ss, jobs, n);
         // dW_ih[d] = da_d^T X_l  (4H x D_l, reduction over all frames)
-        gemm_f32<T, true, true, V, V>("gemm_dwih", s, opnd(DAT, M, (int)M, 4 * H, 4 * H * M),
+        gemm_f32<T, true, true, V, V>("gemm_dwih", ss, opnd(DAT, M, (int)M, 4 * H, 4 * H * M),
                                       opnd(XTl, M, (int)M, Dl), 4 * H, Dl, M, 2, lo.sp_dWih[l], grad + lo.Wih[l][0], Dl,
-                                      lo.Wih[l][1] - lo.Wih[l][0], part);
+                                      lo.Wih[l][1] - lo.Wih[l][0], part_side);
         // dW_hh[d] = sum_t da_d[t]^T h_d[t_prev] (frames shifted as below)
-        gemm_f32<T, true, true, V, V>("gemm_dwhh", s, opnd(DAT + B, M, (int)Kr, 4 * H, 4 * H * M - B),
+        gemm_f32<T, true, true, V, V>("gemm_dwhh", ss, opnd(DAT + B, M, (int)Kr, 4 * H, 4 * H * M - B),
                                       opnd(YTl, M, (int)Kr, H, (int64_t)H * M + B), 4 * H, H, Kr, 2, lo.sp_dWhh,
-                                      grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part);
+                                      grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part_side);
         dw_done = true;
       }
     }
@@ -526,11 +580,12 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     }
     // db_ih = db_hh = sum over frames of da
     if (step_fused)
-      colsum_parts("colsum_db", s, (const float*)(ws + lo.DBP), Tn * (int)cdiv(B, 16), 8 * H, 4 * H,
+      colsum_parts("colsum_db", ss, DBPl, Tn * (int)cdiv(B, 16), 8 * H, 4 * H,
                    lo.bih[l][1] - lo.bih[l][0], grad + lo.bih[l][0], grad + lo.bhh[l][0]);
     else
       colsum<T>("colsum_db", s, DA, M, 8 * H, 8 * H, csp, 4 * H, lo.bih[l][1] - lo.bih[l][0],
                 grad + lo.bih[l][0], grad + lo.bhh[l][0]);
+    if (side) (void)hipEventRecord(side->dw_done[l], ss);
     // dX_l = sum_d da_d W_ih[d]  (the gradient reaching the layer below)
     if (l > 0) {
       const Opnd A = opnd(DA, 8 * H, 8 * H, M);
@@ -549,6 +604,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       dY = dst;
     }
   }
+  if (side) (void)hipStreamWaitEvent(s, side->dw_done[0], 0);   // join before returning
   return blstm_check_launch("blstm_bwd");
 }
 
