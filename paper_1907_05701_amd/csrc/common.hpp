@@ -56,9 +56,14 @@ template <> struct Mfma<float> {
   __device__ static __forceinline__ frag zero() { return 0.0f; }
 };
 
-// Fast transcendental helpers for the LSTM cell (float32 throughout).
-__device__ __forceinline__ float sigmoidf_(float a) { return 1.0f / (1.0f + __expf(-a)); }
-__device__ __forceinline__ float tanhf_(float a) { return tanhf(a); }
+// Transcendental helpers for the LSTM cell (float32 throughout), on the
+// hardware exponential and reciprocal (v_exp_f32, v_rcp_f32: about 1 ulp
+// each): sigmoid(a) = 1 / (1 + e^-a), tanh(a) = 2 sigmoid(2a) - 1 (absolute
+// error a few 1e-7; both saturate correctly when e^-a over- or underflows).
+__device__ __forceinline__ float sigmoidf_(float a) { return __builtin_amdgcn_rcpf(1.0f + __expf(-a)); }
+__device__ __forceinline__ float tanhf_(float a) {
+  return 2.0f * __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * a)) - 1.0f;
+}
 
 // ---------------------------------------------------------------------------
 // Host side: layout of the flat parameter vector and of the workspaces.

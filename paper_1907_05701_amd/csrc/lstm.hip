@@ -102,15 +102,27 @@ __global__ __launch_bounds__(256) void lstm_rec_fwd_step(const RecFwdArgs<T> a) 
     for (int g = 0; g < 4; ++g) brow[g] = Wd + ((int64_t)g * H + u) * H;
     const int koff = (lane >> 4) * MT::KPL;
     const int nks = H / MT::KSTEP;
-#pragma unroll 8
-    for (int ks = kp; ks < nks; ks += KP) {
-      const int k = ks * MT::KSTEP + koff;
-      const typename MT::frag af = rowok ? load_frag<T>(arow + k) : MT::zero();
-      typename MT::frag bf[4];
+    // NB k-steps of loads in flight before the first product (a loop of
+    // load-then-multiply would wait one memory round trip per k-step)
+    constexpr int NB = 4;
+    for (int ks0 = kp; ks0 < nks; ks0 += NB * KP) {
+      typename MT::frag af[NB], bf[NB][4];
 #pragma unroll
-      for (int g = 0; g < 4; ++g) bf[g] = load_frag<T>(brow[g] + k);
+      for (int j = 0; j < NB; ++j) {
+        const int k = (ks0 + j * KP) * MT::KSTEP + koff;
+        if (ks0 + j * KP < nks) {
+          af[j] = load_frag<T>(arow + k);
 #pragma unroll
-      for (int g = 0; g < 4; ++g) acc[g] = MT::mma(af, bf[g], acc[g]);
+          for (int g = 0; g < 4; ++g) bf[j][g] = load_frag<T>(brow[g] + k);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+        if (ks0 + j * KP < nks) {
+          const typename MT::frag a0 = rowok ? af[j] : MT::zero();
+#pragma unroll
+          for (int g = 0; g < 4; ++g) acc[g] = MT::mma(a0, bf[j][g], acc[g]);
+        }
     }
   }
 
@@ -178,7 +190,41 @@ __global__ __launch_bounds__(256) void lstm_rec_bwd_step(const RecBwdArgs<T> a) 
   const int u = q * 16 + (lane & 15);
   const bool epi = kp == 0;
 
-  float dy[4], gt[4][4], cc[4], cpv[4], dcn[4];
+  // dh_rec of this 16x16 block over this wave's share of the 4H gate rows.
+  // A batch of NB k-steps of operand loads goes out before the first product
+  // (load-then-multiply would wait one memory round trip per k-step), and the
+  // cell-derivative inputs are loaded behind the first batch.
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  const bool prod = a.tau > 0;
+  const int bl = rb * 16 * MBK + mb * 16 + (lane & 15);
+  const bool rowok = bl < B;
+  const T* arow = a.DA + ((int64_t)tn * B + (rowok ? bl : 0)) * 8 * H + (int64_t)d * 4 * H;
+  const T* brow = (d ? a.WT1 : a.WT0) + (int64_t)u * 4 * H;
+  const int koff = (lane >> 4) * MT::KPL;
+  const int nks = 4 * H / MT::KSTEP;
+  constexpr int NB = 16;
+  typename MT::frag af[NB], bf[NB];
+  auto issue = [&](int ks0) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int k = (ks0 + j * KP) * MT::KSTEP + koff;
+      if (ks0 + j * KP < nks) {
+        af[j] = load_frag<T>(arow + k);
+        bf[j] = load_frag<T>(brow + k);
+      }
+    }
+  };
+  auto multiply = [&](int ks0) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      if (ks0 + j * KP < nks) acc = MT::mma(rowok ? af[j] : MT::zero(), bf[j], acc);
+  };
+  if (prod) issue(kp);
+
+  // everything the cell derivative needs besides dh_rec (gates stay bf16
+  // until used)
+  float dy[4], cc[4], cpv[4], dcn[4];
+  T graw[4][4];
   if (epi) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -188,27 +234,18 @@ __global__ __launch_bounds__(256) void lstm_rec_bwd_step(const RecBwdArgs<T> a) 
       dy[r] = a.DY[row * 2 * H + (int64_t)d * H + u];
       const T* gs = a.G + row * 8 * H + (int64_t)d * 4 * H + u;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) gt[r][g] = to_f32(gs[g * H]);
+      for (int g = 0; g < 4; ++g) graw[r][g] = gs[g * H];
       cc[r] = a.C[row * 2 * H + (int64_t)d * H + u];
       cpv[r] = (tp >= 0 && tp < Tn) ? a.C[((int64_t)tp * B + b) * 2 * H + (int64_t)d * H + u] : 0.f;
       dcn[r] = a.tau > 0 ? a.DC[((int64_t)d * B + b) * H + u] : 0.f;
     }
   }
 
-  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (a.tau > 0) {
-    const T* WT = d ? a.WT1 : a.WT0;
-    const int bl = rb * 16 * MBK + mb * 16 + (lane & 15);
-    const bool rowok = bl < B;
-    const T* arow = a.DA + ((int64_t)tn * B + (rowok ? bl : 0)) * 8 * H + (int64_t)d * 4 * H;
-    const T* brow = WT + (int64_t)u * 4 * H;
-    const int koff = (lane >> 4) * MT::KPL;
-    const int nks = 4 * H / MT::KSTEP;
-#pragma unroll 16
-    for (int ks = kp; ks < nks; ks += KP) {
-      const int k = ks * MT::KSTEP + koff;
-      const typename MT::frag af = rowok ? load_frag<T>(arow + k) : MT::zero();
-      acc = MT::mma(af, load_frag<T>(brow + k), acc);
+  if (prod) {
+    multiply(kp);
+    for (int ks0 = kp + NB * KP; ks0 < nks; ks0 += NB * KP) {
+      issue(ks0);
+      multiply(ks0);
     }
   }
 
@@ -223,7 +260,7 @@ __global__ __launch_bounds__(256) void lstm_rec_bwd_step(const RecBwdArgs<T> a) 
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int b = rb * 16 * MBK + mb * 16 + (lane >> 4) * 4 + r;
-    const float ig = gt[r][0], fg = gt[r][1], gg = gt[r][2], og = gt[r][3];
+    const float ig = to_f32(graw[r][0]), fg = to_f32(graw[r][1]), gg = to_f32(graw[r][2]), og = to_f32(graw[r][3]);
     const float dh = acc[r] + dy[r];
     const float tc = tanhf_(cc[r]);
     const float dc = dh * og * (1.f - tc * tc) + dcn[r];

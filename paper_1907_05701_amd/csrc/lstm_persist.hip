@@ -113,7 +113,7 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
   extern __shared__ __attribute__((aligned(16))) bf16 lds[];
   constexpr bool KSPLIT = MB == 1;
   constexpr int MBW = KSPLIT ? 1 : MB / 2;
-  constexpr int KC = MBW >= 4 ? 1 : 4 / MBW;   // k-steps gathered per poll
+  constexpr int KC = MBW >= 4 ? 2 : 8 / MBW;   // k-steps gathered per poll (all of a half when MB == 1)
   constexpr int LDN = 128 + 1;   // LDS rows per k-group (128 gate rows + pad)
   const int H = a.H, B = a.B, Tn = a.Tn;
   const int NG = 2 * a.NS;
@@ -151,20 +151,31 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) creg[m][r] = 0.f;
 
+  // input projection of a step (independent of h), loaded one step ahead so
+  // that its latency hides behind the previous step's exchange
+  bf16 gx[MBW][4][4], gxn[MBW][4][4];
+  auto load_gx = [&](int tt) {
+#pragma unroll
+    for (int m = 0; m < MBW; ++m)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rowbase + (mb0 + m) * 16 + (lane >> 4) * 4 + r;
+        const bf16* p = a.Gx + ((int64_t)tt * B + (row < rend ? row : a.b0)) * 8 * H + (int64_t)d * 4 * H + unit;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) gxn[m][r][q] = p[q * H];
+      }
+  };
+  if (epi) load_gx(d ? Tn - 1 : 0);
+
   for (int tau = 0; tau < Tn; ++tau) {
     const int t = d ? Tn - 1 - tau : tau;
-    // input projection of this step for the epilogue (independent of h)
-    float gx[MBW][4][4];
     if (epi) {
 #pragma unroll
       for (int m = 0; m < MBW; ++m)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = rowbase + (mb0 + m) * 16 + (lane >> 4) * 4 + r;
-          const bf16* p = a.Gx + ((int64_t)t * B + (row < rend ? row : a.b0)) * 8 * H + (int64_t)d * 4 * H + unit;
+        for (int r = 0; r < 4; ++r)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) gx[m][r][q] = (float)p[q * H];
-        }
+          for (int q = 0; q < 4; ++q) gx[m][r][q] = gxn[m][r][q];
     }
 
     f32x4 acc[MBW][4];
@@ -218,15 +229,20 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int row = rowbase + (mb0 + m) * 16 + (lane >> 4) * 4 + r;
-          const float ig = sigmoidf_(acc[m][0][r] + gx[m][r][0]);
-          const float fg = sigmoidf_(acc[m][1][r] + gx[m][r][1]);
-          const float gg = tanhf_(acc[m][2][r] + gx[m][r][2]);
-          const float og = sigmoidf_(acc[m][3][r] + gx[m][r][3]);
+          const float ig = sigmoidf_(acc[m][0][r] + (float)gx[m][r][0]);
+          const float fg = sigmoidf_(acc[m][1][r] + (float)gx[m][r][1]);
+          const float gg = tanhf_(acc[m][2][r] + (float)gx[m][r][2]);
+          const float og = sigmoidf_(acc[m][3][r] + (float)gx[m][r][3]);
           const float c = fg * creg[m][r] + ig * gg;
           creg[m][r] = c;
           const float h = og * tanhf_(c);
           const float h_next_unit = __shfl_xor(h, 1);   // lanes of one row, units u and u^1
           if (row >= rend) continue;
+          // publish h first: the other members wait for it, the saved
+          // activations below are only read after the launch
+          if ((lane & 1) == 0)
+            ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 2, pack_bf16x2(h, h_next_unit),
+                     (uint32_t)(tau + 1));
           const int64_t fr = (int64_t)t * B + row;
           a.C[fr * 2 * H + (int64_t)d * H + unit] = c;
           a.Y[fr * 2 * H + (int64_t)d * H + unit] = (bf16)h;
@@ -235,11 +251,9 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
           gs[H] = (bf16)fg;
           gs[2 * H] = (bf16)gg;
           gs[3 * H] = (bf16)og;
-          if ((lane & 1) == 0)
-            ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 2, pack_bf16x2(h, h_next_unit),
-                     (uint32_t)(tau + 1));
         }
     }
+    if (epi && tau + 1 < Tn) load_gx(d ? Tn - 2 - tau : tau + 1);
     __syncthreads();   // the reduction buffer is reused by the next step
   }
 }
