@@ -355,10 +355,9 @@ template <> struct VecW<float> { static constexpr int v = 4; };
 static bool step_rows_32(int H, int B) { return (int64_t)(H / 16) * cdiv(B, 32) * 2 >= 256; }
 
 // Which recurrent kernels run.  Default (measured fastest on MI355X at the
-// paper's shapes): the persistent kernel for the forward pass and the
-// per-step kernels for BPTT.  ADPSGD_BLSTM_RECURRENCE=persistent uses the
-// persistent kernels for both passes, =per-step (or ADPSGD_BLSTM_NO_PERSIST=1)
-// none.  The persistent kernels need bf16 and a W_hh slice that fits in LDS;
+// paper's shapes): the persistent kernels for both passes;
+// ADPSGD_BLSTM_RECURRENCE=per-step (or ADPSGD_BLSTM_NO_PERSIST=1) the
+// per-step kernels.  The persistent kernels need bf16 and a W_hh slice that fits in LDS;
 // inside stream capture they are recorded as cooperative kernel nodes.
 template <typename T>
 static bool use_persistent(int H, int steps, bool backward, hipStream_t s) {
@@ -367,7 +366,6 @@ static bool use_persistent(int H, int steps, bool backward, hipStream_t s) {
   if (off && atoi(off)) return false;
   const char* pol = getenv("ADPSGD_BLSTM_RECURRENCE");
   if (pol && strcmp(pol, "per-step") == 0) return false;
-  if (backward && !(pol && strcmp(pol, "persistent") == 0)) return false;
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
   if (hipStreamIsCapturing(s, &cap) != hipSuccess) return false;
   if (cap != hipStreamCaptureStatusNone) {
@@ -551,8 +549,12 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     if (use_persistent<T>(H, lo.T, true, s)) {
       PersistArgs pa = persist_args(lo, (const bf16*)W, ws, l);
       pa.DA = (bf16*)DA; pa.DY = dY; pa.C = (float*)Cl; pa.G = (bf16*)Gl;
+      pa.DAT = lo.xpose_act ? (bf16*)DATl : nullptr;
+      pa.DBP = DBPl;
+      pa.M = M;
       done = persist_layer(true, pa, s) == hipSuccess;
       if (!done) (void)hipGetLastError();
+      step_fused = done;
     }
     if (!done) {
       if (!have_wt) make_copies(false, true);

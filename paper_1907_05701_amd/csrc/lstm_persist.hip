@@ -267,7 +267,10 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
 // already holds (its own da, kept in LDS, and its W_hh rows, LDS-resident),
 // publishes P_m as exchange words, and gathers for its own 32 units the
 // partials of all members, summed in member order.  Per step a member thus
-// reads rows x 32 x H/32 values instead of rows x 4H.
+// reads rows x 32 x H/32 values instead of rows x 4H.  Exchange words are
+// member-major within a row (member m's H/2 words contiguous), so a member
+// publishes whole cache lines and a reader takes 128 contiguous bytes of each
+// member.
 // ---------------------------------------------------------------------------
 template <int MB>
 __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
@@ -318,7 +321,8 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
     const int tp = d ? t + 1 : t - 1;
     const bool has_prev = tp >= 0 && tp < Tn;
     // everything the cell derivative needs besides dh_rec
-    float dy[ITEMS], gt[ITEMS][4], cc[ITEMS], cp[ITEMS];
+    float dy[ITEMS], cc[ITEMS], cp[ITEMS];
+    bf16 gt[ITEMS][4];   // converted in the cell phase, so the gather does not wait for these loads
 #pragma unroll
     for (int i = 0; i < ITEMS; ++i) {
       int row = rowbase + (tid >> 5) + 8 * i;
@@ -330,7 +334,7 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
       cp[i] = has_prev ? a.C[((int64_t)tp * B + row) * 2 * H + (int64_t)d * H + unit] : 0.f;
       const bf16* gs = a.G + fr * 8 * H + (int64_t)d * 4 * H + unit;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) gt[i][q] = (float)gs[q * H];
+      for (int q = 0; q < 4; ++q) gt[i][q] = gs[q * H];
     }
 
     // gather dh_rec for the own units: items (row, unit pair), pair = tid % 16
@@ -342,13 +346,15 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
         const int p = tid & 15;
         float lo = 0.f, hi = 0.f;
         if (rowbase + r < rend) {
-          const uint64_t* src = xs + ((int64_t)d * a.rows + (rowbase + r - a.b0)) * wpr +
-                                (int64_t)(u0 / 2 + p) * NM;
+          // member m's partials of this row: H/2 contiguous words; the 16
+          // threads of a row read 16 adjacent words (128 bytes) per member
+          const uint64_t* src = xs + ((int64_t)d * a.rows + (rowbase + r - a.b0)) * wpr + u0 / 2 + p;
           uint64_t wv[PU / 2];
           for (int m0 = 0; m0 < NM; m0 += PU / 2) {
             const int nm = min(PU / 2, NM - m0);
 #pragma unroll
-            for (int k = 0; k < PU / 2; ++k) wv[k] = k < nm ? ll_load(src + m0 + k) : ((uint64_t)tau << 32);
+            for (int k = 0; k < PU / 2; ++k)
+              wv[k] = k < nm ? ll_load(src + (int64_t)(m0 + k) * (H / 2)) : ((uint64_t)tau << 32);
             for (unsigned it = 0;; ++it) {
               bool bad = false;
 #pragma unroll
@@ -362,7 +368,7 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
               __builtin_amdgcn_s_sleep(1);
 #pragma unroll
               for (int k = 0; k < PU / 2; ++k)
-                if ((uint32_t)(wv[k] >> 32) != (uint32_t)tau) wv[k] = ll_load(src + m0 + k);
+                if ((uint32_t)(wv[k] >> 32) != (uint32_t)tau) wv[k] = ll_load(src + (int64_t)(m0 + k) * (H / 2));
             }
 #pragma unroll
             for (int k = 0; k < PU / 2; ++k) {
@@ -387,7 +393,7 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
     for (int i = 0; i < ITEMS; ++i) {
       const int r = (tid >> 5) + 8 * i;
       const int row = rowbase + r;
-      const float ig = gt[i][0], fg = gt[i][1], gg = gt[i][2], og = gt[i][3];
+      const float ig = (float)gt[i][0], fg = (float)gt[i][1], gg = (float)gt[i][2], og = (float)gt[i][3];
       const float dh = dhl[r * PU + cu] + dy[i];
       const float tc = tanhf_(cc[i]);
       const float dc = dh * og * (1.f - tc * tc) + dcreg[i];
@@ -409,6 +415,30 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
       }
     }
     __syncthreads();
+
+    // the own da block (R rows x 128 gate rows, in LDS) also goes out
+    // frame-contiguous (DAT) and as bias-gradient partial sums per 16-row
+    // block (DBP): thread t takes gate row t/2 and 8 of the 16 rows of a block
+    if (a.DAT || a.DBP) {
+      const int kk = tid >> 1, h8 = (tid & 1) * 8;
+      const int q = (kk >> 4) & 3, unit = u0 + (kk >> 6) * 16 + (kk & 15);
+      const int64_t grow = (int64_t)d * 4 * H + (int64_t)q * H + unit;   // gate row of the layer
+#pragma unroll
+      for (int m = 0; m < MB; ++m) {
+        bf16 v[8];
+        float sum = 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          v[j] = al[((kk >> 3) * (R + 1) + m * 16 + h8 + j) * 8 + (kk & 7)];
+          sum += (float)v[j];
+        }
+        const int row = rowbase + m * 16 + h8;
+        if (a.DAT && row < rend) *(uint4*)(a.DAT + grow * a.M + (int64_t)t * B + row) = *(const uint4*)v;
+        sum += __shfl_xor(sum, 1);
+        if (a.DBP && (tid & 1) == 0 && rowbase + m * 16 < rend)
+          a.DBP[((int64_t)tau * ((B + 15) / 16) + (rowbase + m * 16) / 16) * 8 * H + grow] = sum;
+      }
+    }
 
     // P = da_own [R x 128] * W_own [128 x H]; 16-unit block nb goes to wave nb % 4
     if (tau + 1 < Tn) {
@@ -449,7 +479,7 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
               const int nb = base + w + 4 * j;
               const int unit = nb * 16 + (lane & 15);
               if ((lane & 1) == 0 && row < rend && nb < NB)
-                ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + (int64_t)(unit / 2) * NM + mem,
+                ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + (int64_t)mem * (H / 2) + unit / 2,
                          pack_bf16x2(v, vn), (uint32_t)(tau + 1));
             }
       }

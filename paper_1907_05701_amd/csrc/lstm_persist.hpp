@@ -13,6 +13,9 @@ struct PersistArgs {
   bf16* DA;           // backward: gate pre-activation gradients [M][8H]
   const float* DY;    // backward: gradient reaching the layer output [M][2H]
   uint64_t* X;        // step-exchange words (see lstm_persist.hip), PERSIST_XCH_BYTES
+  bf16* DAT;          // backward, optional: da also frame-contiguous [8H][M] (needs B % 8 == 0)
+  float* DBP;         // backward, optional: sums of da over 16-row blocks [Tn][cdiv(B,16)][8H]
+  int64_t M;          // frames, T*B (DAT row length)
   int* status;        // cleared before each launch; 1 if a poll ever gave up
   int Tn, B, H;
   int b0, rows, NS;   // batch chunk handled by one launch (filled in by persist_layer)
