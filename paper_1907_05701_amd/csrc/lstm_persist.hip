@@ -132,6 +132,7 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
     *(uint4*)&lds[(kc * LDN + n) * 8] = *(const uint4*)(Wd + row * H + kc * 8);
   }
   f32x4* red = (f32x4*)(lds + (size_t)kcn * LDN * 8);
+  bf16* hl = (bf16*)(red + 8 * 64);   // MB == 1: gathered h [H/8][16 + 1][8]
   __syncthreads();
 
   const int rend = a.b0 + a.rows;
@@ -183,7 +184,50 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
     for (int m = 0; m < MBW; ++m)
 #pragma unroll
       for (int q = 0; q < 4; ++q) acc[m][q] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (tau > 0) {
+    if (KSPLIT && tau > 0) {
+      // h of the previous step (16 rows x H/2 words, published with step
+      // number tau) is polled by all 256 threads in whole cache lines (thread
+      // t: row t/16, words t%16 + 16j) and staged in LDS in the MFMA A layout
+      const int tr = tid >> 4, tw = tid & 15;
+      const int row = rowbase + tr;
+      const bool rok = row < rend;
+      const int nj = H / 32;
+      const uint64_t* src = a.X + ((tau - 1) & 1) * slot_stride + ((int64_t)d * a.rows + (rok ? row - a.b0 : 0)) * wpr + tw;
+      uint64_t wv[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) wv[j] = (rok && j < nj) ? ll_load(src + 16 * j) : ((uint64_t)tau << 32);
+      for (unsigned it = 0;; ++it) {
+        bool bad = false;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) bad |= (uint32_t)(wv[j] >> 32) != (uint32_t)tau;
+        if (!bad) break;
+        if (it > SPIN_LIMIT ||
+            ((it & 63) == 63 && __hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
+          __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          if ((uint32_t)(wv[j] >> 32) != (uint32_t)tau) wv[j] = ll_load(src + 16 * j);
+      }
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        if (j >= nj) break;
+        const int k = 2 * (tw + 16 * j);   // units k, k+1
+        *(uint32_t*)&hl[((k >> 3) * 17 + tr) * 8 + (k & 7)] = rok ? (uint32_t)wv[j] : 0u;
+      }
+      __syncthreads();
+      for (int ks = ks_beg; ks < ks_end; ++ks) {
+        const int kg = ks * 4 + (lane >> 4);
+        const bf16x8 af = *(const bf16x8*)&hl[(kg * 17 + (lane & 15)) * 8];
+        bf16x8 bfr[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) bfr[q] = *(const bf16x8*)&lds[(kg * LDN + ub * 64 + q * 16 + (lane & 15)) * 8];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[0][q] = Mfma<bf16>::mma(af, bfr[q], acc[0][q]);
+      }
+    } else if (tau > 0) {
       // h of the previous step, published with step number tau
       const uint64_t* rp[MBW];
 #pragma unroll
@@ -500,7 +544,7 @@ __global__ __launch_bounds__(256) void clear_exchange_kernel(uint4* p, int64_t n
 size_t persist_lds_bytes(int H, bool backward, int MB) {
   if (backward)
     return (size_t)16 * (H + 1) * 16 + (size_t)16 * (16 * MB + 1) * 16 + (size_t)16 * MB * PU * 4;
-  return (size_t)(H / 8) * (128 + 1) * 16 + 8 * 64 * 16;
+  return (size_t)(H / 8) * (128 + 1) * 16 + 8 * 64 * 16 + (MB == 1 ? (size_t)(H / 8) * 17 * 16 : 0);
 }
 
 // Workgroups that can be co-resident: one per compute unit (the LDS slice
