@@ -619,7 +619,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     }
     // db_ih = db_hh = sum over frames of da
     if (step_fused)
-      colsum_parts("colsum_db", ss, DBPl, Tn * (int)cdiv(B, 16), 8 * H, 4 * H,
+      colsum_parts("colsum_db", ss, DBPl, (done ? 1 : Tn) * (int)cdiv(B, 16), 8 * H, 4 * H,
                    lo.bih[l][1] - lo.bih[l][0], grad + lo.bih[l][0], grad + lo.bhh[l][0]);
     else
       colsum<T>("colsum_db", s, DA, M, 8 * H, 8 * H, csp, 4 * H, lo.bih[l][1] - lo.bih[l][0],

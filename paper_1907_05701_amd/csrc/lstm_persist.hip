@@ -359,6 +359,14 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
   float dcreg[ITEMS];
 #pragma unroll
   for (int i = 0; i < ITEMS; ++i) dcreg[i] = 0.f;
+  // da^T and bias partials: thread t takes own gate row t/2 and 8 of the 16
+  // rows of each 16-row block; the bias partial of a block is summed over the
+  // steps in order and written once
+  const int dkk = tid >> 1, dh8 = (tid & 1) * 8;
+  const int64_t dgrow = (int64_t)d * 4 * H + (int64_t)((dkk >> 4) & 3) * H + u0 + (dkk >> 6) * 16 + (dkk & 15);
+  float dbacc[MB];
+#pragma unroll
+  for (int m = 0; m < MB; ++m) dbacc[m] = 0.f;
 
   for (int tau = 0; tau < Tn; ++tau) {
     const int t = d ? tau : Tn - 1 - tau;
@@ -464,23 +472,19 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
     // frame-contiguous (DAT) and as bias-gradient partial sums per 16-row
     // block (DBP): thread t takes gate row t/2 and 8 of the 16 rows of a block
     if (a.DAT || a.DBP) {
-      const int kk = tid >> 1, h8 = (tid & 1) * 8;
-      const int q = (kk >> 4) & 3, unit = u0 + (kk >> 6) * 16 + (kk & 15);
-      const int64_t grow = (int64_t)d * 4 * H + (int64_t)q * H + unit;   // gate row of the layer
 #pragma unroll
       for (int m = 0; m < MB; ++m) {
         bf16 v[8];
         float sum = 0.f;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          v[j] = al[((kk >> 3) * (R + 1) + m * 16 + h8 + j) * 8 + (kk & 7)];
+          v[j] = al[((dkk >> 3) * (R + 1) + m * 16 + dh8 + j) * 8 + (dkk & 7)];
           sum += (float)v[j];
         }
-        const int row = rowbase + m * 16 + h8;
-        if (a.DAT && row < rend) *(uint4*)(a.DAT + grow * a.M + (int64_t)t * B + row) = *(const uint4*)v;
+        const int row = rowbase + m * 16 + dh8;
+        if (a.DAT && row < rend) *(uint4*)(a.DAT + dgrow * a.M + (int64_t)t * B + row) = *(const uint4*)v;
         sum += __shfl_xor(sum, 1);
-        if (a.DBP && (tid & 1) == 0 && rowbase + m * 16 < rend)
-          a.DBP[((int64_t)tau * ((B + 15) / 16) + (rowbase + m * 16) / 16) * 8 * H + grow] = sum;
+        dbacc[m] += sum;   // steps in order
       }
     }
 
@@ -528,6 +532,11 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
             }
       }
     }
+  }
+  if (a.DBP && (tid & 1) == 0) {
+#pragma unroll
+    for (int m = 0; m < MB; ++m)
+      if (rowbase + m * 16 < rend) a.DBP[(int64_t)((rowbase + m * 16) / 16) * 8 * H + dgrow] = dbacc[m];
   }
 }
 

@@ -14,7 +14,7 @@ struct PersistArgs {
   const float* DY;    // backward: gradient reaching the layer output [M][2H]
   uint64_t* X;        // step-exchange words (see lstm_persist.hip), PERSIST_XCH_BYTES
   bf16* DAT;          // backward, optional: da also frame-contiguous [8H][M] (needs B % 8 == 0)
-  float* DBP;         // backward, optional: sums of da over 16-row blocks [Tn][cdiv(B,16)][8H]
+  float* DBP;         // backward, optional: sums of da over 16-row blocks and all steps [cdiv(B,16)][8H]
   int64_t M;          // frames, T*B (DAT row length)
   int* status;        // cleared before each launch; 1 if a poll ever gave up
   int Tn, B, H;
