@@ -37,6 +37,7 @@
 
 #define PU 32
 #define SPIN_LIMIT (1u << 18)
+#define H_MAX_MEMBERS 16   // H / 32 for the largest H whose W_hh slice fits in LDS
 
 __device__ __forceinline__ uint64_t ll_load(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -311,10 +312,10 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
 // already holds (its own da, kept in LDS, and its W_hh rows, LDS-resident),
 // publishes P_m as exchange words, and gathers for its own 32 units the
 // partials of all members, summed in member order.  Per step a member thus
-// reads rows x 32 x H/32 values instead of rows x 4H.  Exchange words are
-// member-major within a row (member m's H/2 words contiguous), so a member
-// publishes whole cache lines and a reader takes 128 contiguous bytes of each
-// member.
+// reads rows x 32 x H/32 values instead of rows x 4H.  An exchange word
+// holds one unit's partials for two adjacent rows; words are ordered (row
+// pair, member, unit), so a member publishes whole cache lines and a reader
+// takes 256 contiguous bytes of each member.
 // ---------------------------------------------------------------------------
 template <int MB>
 __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
@@ -352,8 +353,8 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
 
   const int rend = a.b0 + a.rows;
   const int rowbase = a.b0 + s * R;
-  const int wpr = (H / 2) * NM;                  // exchange words per row
-  const int64_t slot_stride = (int64_t)2 * a.rows * wpr;
+  const int rpairs = (a.rows + 1) / 2;             // row pairs of this launch
+  const int64_t slot_stride = (int64_t)2 * rpairs * NM * H;
   // cell items: unit cu = tid % 32, rows tid/32 + 8*i
   const int cu = tid & 31;
   float dcreg[ITEMS];
@@ -389,50 +390,45 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
       for (int q = 0; q < 4; ++q) gt[i][q] = gs[q * H];
     }
 
-    // gather dh_rec for the own units: items (row, unit pair), pair = tid % 16
+    // gather dh_rec for the own units: items (row pair, unit), unit = tid % 32;
+    // the 32 threads of a row pair read 32 adjacent words (256 bytes) per member
     if (tau > 0) {
       const uint64_t* xs = a.X + ((tau - 1) & 1) * slot_stride;
 #pragma unroll
       for (int i = 0; i < MB; ++i) {
-        const int r = (tid >> 4) + 16 * i;
-        const int p = tid & 15;
+        const int rp = (tid >> 5) + 8 * i;   // row pair within this member's rows
         float lo = 0.f, hi = 0.f;
-        if (rowbase + r < rend) {
-          // member m's partials of this row: H/2 contiguous words; the 16
-          // threads of a row read 16 adjacent words (128 bytes) per member
-          const uint64_t* src = xs + ((int64_t)d * a.rows + (rowbase + r - a.b0)) * wpr + u0 / 2 + p;
-          uint64_t wv[PU / 2];
-          for (int m0 = 0; m0 < NM; m0 += PU / 2) {
-            const int nm = min(PU / 2, NM - m0);
+        if (rowbase + 2 * rp < rend) {
+          const uint64_t* src = xs + ((int64_t)d * rpairs + (rowbase - a.b0) / 2 + rp) * NM * H + u0 + cu;
+          uint64_t wv[H_MAX_MEMBERS];
 #pragma unroll
-            for (int k = 0; k < PU / 2; ++k)
-              wv[k] = k < nm ? ll_load(src + (int64_t)(m0 + k) * (H / 2)) : ((uint64_t)tau << 32);
-            for (unsigned it = 0;; ++it) {
-              bool bad = false;
+          for (int k = 0; k < H_MAX_MEMBERS; ++k)
+            wv[k] = k < NM ? ll_load(src + (int64_t)k * H) : ((uint64_t)tau << 32);
+          for (unsigned it = 0;; ++it) {
+            bool bad = false;
 #pragma unroll
-              for (int k = 0; k < PU / 2; ++k) bad |= (uint32_t)(wv[k] >> 32) != (uint32_t)tau;
-              if (!bad) break;
-              if (it > SPIN_LIMIT ||
-                  ((it & 63) == 63 && __hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
-                __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                break;
-              }
-              __builtin_amdgcn_s_sleep(1);
-#pragma unroll
-              for (int k = 0; k < PU / 2; ++k)
-                if ((uint32_t)(wv[k] >> 32) != (uint32_t)tau) wv[k] = ll_load(src + (int64_t)(m0 + k) * (H / 2));
+            for (int k = 0; k < H_MAX_MEMBERS; ++k) bad |= (uint32_t)(wv[k] >> 32) != (uint32_t)tau;
+            if (!bad) break;
+            if (it > SPIN_LIMIT ||
+                ((it & 63) == 63 && __hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
+              __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              break;
             }
+            __builtin_amdgcn_s_sleep(1);
 #pragma unroll
-            for (int k = 0; k < PU / 2; ++k) {
-              if (k >= nm) break;
-              const uint32_t v = (uint32_t)wv[k];
-              lo += __builtin_bit_cast(float, v << 16);
-              hi += __builtin_bit_cast(float, v & 0xffff0000u);
-            }
+            for (int k = 0; k < H_MAX_MEMBERS; ++k)
+              if ((uint32_t)(wv[k] >> 32) != (uint32_t)tau) wv[k] = ll_load(src + (int64_t)k * H);
+          }
+#pragma unroll
+          for (int k = 0; k < H_MAX_MEMBERS; ++k) {
+            if (k >= NM) break;
+            const uint32_t v = (uint32_t)wv[k];
+            lo += __builtin_bit_cast(float, v << 16);
+            hi += __builtin_bit_cast(float, v & 0xffff0000u);
           }
         }
-        dhl[r * PU + 2 * p] = lo;
-        dhl[r * PU + 2 * p + 1] = hi;
+        dhl[(2 * rp) * PU + cu] = lo;
+        dhl[(2 * rp + 1) * PU + cu] = hi;
       }
     } else {
       for (int i = tid; i < R * PU; i += 256) dhl[i] = 0.f;
@@ -514,21 +510,19 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) acc[m][j] = Mfma<bf16>::mma(af[m], bfr[j], acc[m][j]);
         }
-        // publish: word (row, unit pair, member)
+        // publish: word (row pair, member, unit), the lane's rows 2r2, 2r2+1
 #pragma unroll
         for (int m = 0; m < MB; ++m)
 #pragma unroll
           for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const float v = acc[m][j][r];
-              const float vn = __shfl_xor(v, 1);
-              const int row = rowbase + m * 16 + (lane >> 4) * 4 + r;
+            for (int r2 = 0; r2 < 2; ++r2) {
+              const int rl = m * 16 + (lane >> 4) * 4 + 2 * r2;   // even row within this member
               const int nb = base + w + 4 * j;
               const int unit = nb * 16 + (lane & 15);
-              if ((lane & 1) == 0 && row < rend && nb < NB)
-                ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + (int64_t)mem * (H / 2) + unit / 2,
-                         pack_bf16x2(v, vn), (uint32_t)(tau + 1));
+              if (rowbase + rl < rend && nb < NB)
+                ll_store(xo + (((int64_t)d * rpairs + (rowbase - a.b0 + rl) / 2) * NM + mem) * H + unit,
+                         pack_bf16x2(acc[m][j][2 * r2], acc[m][j][2 * r2 + 1]), (uint32_t)(tau + 1));
             }
       }
     }
@@ -566,7 +560,7 @@ static int persist_max_wg() {
 }
 
 bool persist_supported(int H, int T) {
-  return H % PU == 0 && T < (1 << 30) && persist_lds_bytes(H, false, 1) <= 160 * 1024 &&
+  return H % PU == 0 && H / PU <= H_MAX_MEMBERS && T < (1 << 30) && persist_lds_bytes(H, false, 1) <= 160 * 1024 &&
          persist_lds_bytes(H, true, 1) <= 160 * 1024;
 }
 
@@ -624,7 +618,8 @@ hipError_t persist_layer(bool backward, PersistArgs a, hipStream_t s) {
     c.rows = std::min(chunk, a.B - b0);
     c.NS = (c.rows + 16 * MB - 1) / (16 * MB);
     // both exchange slots of this chunk start without any valid step number
-    const int64_t words = (int64_t)2 * 2 * c.rows * (c.H / 2) * (backward ? c.H / PU : 1);
+    const int64_t words = backward ? (int64_t)2 * 2 * ((c.rows + 1) / 2) * (c.H / PU) * c.H
+                                   : (int64_t)2 * 2 * c.rows * (c.H / 2);
     const int64_t n16 = words / 2;
     hipLaunchKernelGGL(clear_exchange_kernel, dim3((unsigned)std::min<int64_t>(cdiv(n16, 256), 2048)),
                        dim3(256), 0, s, (uint4*)c.X, n16, c.status);

@@ -25,11 +25,12 @@ struct PersistArgs {
 // launch covers at most PERSIST_MAX_SLICES*128 rows.
 #define PERSIST_MAX_SLICES 32
 #define PERSIST_MAX_ROWS (PERSIST_MAX_SLICES * 16 * 8)
-// Exchange buffer: 2 slots x 2 directions x rows x (H/2 unit pairs) x
-// (H/32 members) words of 8 bytes (the backward's partial sums; the forward
-// uses the first H/2 words per row).
+// Exchange buffer: 2 slots x 2 directions x row pairs x (H/32 members) x H
+// units words of 8 bytes (the backward's partial sums; the forward uses H/2
+// words per row).
 static inline size_t persist_xch_bytes(int B, int H) {
-  const size_t rows = B < PERSIST_MAX_ROWS ? B : PERSIST_MAX_ROWS;
+  size_t rows = B < PERSIST_MAX_ROWS ? B : PERSIST_MAX_ROWS;
+  rows += rows & 1;
   const size_t members = H / 32 > 0 ? H / 32 : 1;
   return (size_t)2 * 2 * rows * (H / 2) * members * 8;
 }
