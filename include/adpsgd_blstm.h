@@ -110,7 +110,11 @@ int softmax_ce_fwd_bwd(const blstm_dims* dims, const float* theta, const void* t
 /* Back-propagation through time of the LSTM stack given dy_top; act_ws and
  * y_top must come from blstm_fwd with the same theta and dims.  Overwrites
  * the LSTM slots of grad (both b_ih and b_hh receive the same bias
- * gradient); head slots are not touched.  act_ws is also used as scratch. */
+ * gradient); head slots are not touched.  act_ws is also used as scratch.
+ * When not under stream capture the call may also run work on an internal
+ * stream of the current device (created once, default priority); that work
+ * is joined into `stream` before the call returns, so stream order holds as
+ * for any other call.  ADPSGD_BLSTM_OVERLAP=0 disables it. */
 int blstm_bwd(const blstm_dims* dims, const float* theta, const void* theta_lp,
               void* act_ws, const void* y_top, const float* dy_top, float* grad,
               hipStream_t stream);
