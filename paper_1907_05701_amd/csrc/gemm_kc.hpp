@@ -18,8 +18,7 @@
 #pragma once
 
 #include "gemm.hpp"
-
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
+#include "dma.hpp"
 
 struct KcArgs {
   const bf16* A;

@@ -520,7 +520,8 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     }
     if (whh) have_wt = true;
   };
-  make_copies(lp && lo.L > 1, !use_persistent<T>(H, lo.T, true, s));
+  // W_hh^T serves the per-step kernels and the persistent kernel's LDS staging
+  make_copies(lp && lo.L > 1, true);
   // weight gradients on the side stream (bf16 per-step BPTT writing da^T):
   // layer l's buffers (da^T, bias partials, split-K partials) alternate by
   // layer parity, so BPTT of layer l waits only for the side work of l+2
@@ -549,6 +550,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     if (use_persistent<T>(H, lo.T, true, s)) {
       PersistArgs pa = persist_args(lo, (const bf16*)W, ws, l);
       pa.DA = (bf16*)DA; pa.DY = dY; pa.C = (float*)Cl; pa.G = (bf16*)Gl;
+      pa.WT = (const bf16*)(WT + (int64_t)(2 * l) * 4 * H * H);
       pa.DAT = lo.xpose_act ? (bf16*)DATl : nullptr;
       pa.DBP = DBPl;
       pa.M = M;

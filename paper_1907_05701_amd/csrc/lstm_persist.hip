@@ -34,6 +34,7 @@
 #include "common.hpp"
 #include "lstm_persist.hpp"
 #include "xpose.hpp"
+#include "dma.hpp"
 
 #define PU 32
 #define SPIN_LIMIT (1u << 18)
@@ -124,13 +125,18 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int ub = w & 1, wx = w >> 1;
 
-  // W_hh rows of this member: LDS row n = ub*64 + gate*16 + u
+  // W_hh rows of this member: LDS row n = ub*64 + gate*16 + u, stored as
+  // [k/8][n][8]; staged with direct-to-LDS loads (one load fills 64
+  // consecutive rows of one 8-wide k chunk), all in flight at once
   const bf16* Wd = a.W + (d ? a.whh1 : a.whh0);
   const int kcn = H / 8;
-  for (int c = tid; c < 128 * kcn; c += 256) {
-    const int n = c / kcn, kc = c % kcn;
+  {
+    const __amdgpu_buffer_rsrc_t rw = dma_rsrc(Wd);
+    const int n = (w & 1) * 64 + lane;   // row of this lane
     const int64_t row = (int64_t)((n >> 4) & 3) * H + u0 + (n >> 6) * 16 + (n & 15);
-    *(uint4*)&lds[(kc * LDN + n) * 8] = *(const uint4*)(Wd + row * H + kc * 8);
+    for (int kc = w >> 1; kc < kcn; kc += 2)
+      dma16(rw, (uint32_t)((row * H + kc * 8) * 2), lds + (kc * LDN + (w & 1) * 64) * 8);
+    dma_wait_all();
   }
   f32x4* red = (f32x4*)(lds + (size_t)kcn * LDN * 8);
   bf16* hl = (bf16*)(red + 8 * 64);   // MB == 1: gathered h [H/8][16 + 1][8]
@@ -335,19 +341,34 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
   bf16* wl = lds;
   bf16* al = wl + (size_t)16 * (H + 1) * 8;
   float* dhl = (float*)(al + (size_t)16 * (R + 1) * 8);
-  const bf16* Wd = a.W + (d ? a.whh1 : a.whh0);
-  for (int b = tid; b < 16 * (H / 8); b += 256) {
-    const int kg = b % 16, jb = b / 16;
-    uint4 in[8], out[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int kk = kg * 8 + i;
+  if (a.WT && H % 64 == 0) {
+    // from W_hh^T [H][4H] (made by the caller): the 8 own rows of k group kg
+    // are 16 contiguous bytes of W_hh^T row j; one direct-to-LDS load fills
+    // 64 consecutive j of one k group (a load always writes all 64 slots, so
+    // H must be a multiple of 64)
+    const __amdgpu_buffer_rsrc_t rw = dma_rsrc(a.WT + (int64_t)d * H * 4 * H);
+    for (int c = w; c < 16 * (H / 64); c += 4) {
+      const int kg = c % 16, j = (c / 16) * 64 + lane;
+      const int kk = kg * 8;
       const int64_t grow = (int64_t)((kk >> 4) & 3) * H + u0 + (kk >> 6) * 16 + (kk & 15);
-      in[i] = *(const uint4*)(Wd + grow * H + jb * 8);
+      dma16(rw, (uint32_t)(((int64_t)j * 4 * H + grow) * 2), wl + (kg * (H + 1) + (c / 16) * 64) * 8);
     }
-    transpose8x8(in, out);
+    dma_wait_all();
+  } else {
+    const bf16* Wd = a.W + (d ? a.whh1 : a.whh0);
+    for (int b = tid; b < 16 * (H / 8); b += 256) {
+      const int kg = b % 16, jb = b / 16;
+      uint4 in[8], out[8];
 #pragma unroll
-    for (int jj = 0; jj < 8; ++jj) *(uint4*)&wl[(kg * (H + 1) + jb * 8 + jj) * 8] = out[jj];
+      for (int i = 0; i < 8; ++i) {
+        const int kk = kg * 8 + i;
+        const int64_t grow = (int64_t)((kk >> 4) & 3) * H + u0 + (kk >> 6) * 16 + (kk & 15);
+        in[i] = *(const uint4*)(Wd + grow * H + jb * 8);
+      }
+      transpose8x8(in, out);
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) *(uint4*)&wl[(kg * (H + 1) + jb * 8 + jj) * 8] = out[jj];
+    }
   }
   __syncthreads();
 

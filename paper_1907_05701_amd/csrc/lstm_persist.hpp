@@ -7,6 +7,7 @@ struct PersistArgs {
   bf16* Y;            // layer output [M][2H] (forward: read h_prev, write h)
   const bf16* W;      // bf16 parameter copy (flat layout)
   int64_t whh0, whh1; // element offsets of W_hh for the two directions
+  const bf16* WT;     // backward, optional: W_hh^T of this layer, [2][H][4H] (directions)
   const bf16* Gx;     // forward: input projection [M][8H]
   float* C;           // cell states [M][2H] (forward writes, backward reads)
   bf16* G;            // activated gates [M][8H] (forward writes, backward reads)
