@@ -388,12 +388,14 @@ static PersistArgs persist_args(const Layout& lo, const bf16* W, char* ws, int l
   pa.Tn = lo.T;
   pa.B = lo.B;
   pa.H = lo.H;
+  pa.tag = (uint32_t)l;
   return pa;
 }
 
 template <typename T>
 static int fwd_impl(const Layout& lo, const float* theta, const T* W, const float* x, char* ws,
                     T* ytop, hipStream_t s) {
+  bool xch_cleared = false;   // exchange words cleared once per call (persist_clear)
   constexpr int V = VecW<T>::v;
   const int64_t M = lo.M;
   const int H = lo.H, B = lo.B;
@@ -423,7 +425,8 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
     if (use_persistent<T>(H, lo.T, false, s)) {
       PersistArgs pa = persist_args(lo, (const bf16*)W, ws, l);
       pa.Y = (bf16*)Yl; pa.Gx = (const bf16*)GX; pa.C = Cl; pa.G = (bf16*)Gl;
-      if (persist_layer(false, pa, s) == hipSuccess) continue;
+      if (!xch_cleared) xch_cleared = persist_clear(false, pa, s) == hipSuccess;
+      if (xch_cleared && persist_layer(false, pa, s) == hipSuccess) continue;
       (void)hipGetLastError();   // cooperative launch refused: take the per-step path
     }
     RecFwdArgs<T> ra;
@@ -478,6 +481,7 @@ static SideStream* side_stream() {
 template <typename T>
 static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const float* dytop,
                     float* grad, hipStream_t s) {
+  bool xch_cleared = false;   // exchange words cleared once per call (persist_clear)
   constexpr int V = VecW<T>::v;
   const int64_t M = lo.M;
   const int H = lo.H, B = lo.B, Tn = lo.T;
@@ -554,7 +558,8 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       pa.DAT = lo.xpose_act ? (bf16*)DATl : nullptr;
       pa.DBP = DBPl;
       pa.M = M;
-      done = persist_layer(true, pa, s) == hipSuccess;
+      if (!xch_cleared) xch_cleared = persist_clear(true, pa, s) == hipSuccess;
+      done = xch_cleared && persist_layer(true, pa, s) == hipSuccess;
       if (!done) (void)hipGetLastError();
       step_fused = done;
     }

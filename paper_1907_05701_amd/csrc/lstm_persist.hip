@@ -123,6 +123,7 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
   const int d = g & 1, s = g >> 1;
   const int u0 = mem * PU;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const uint32_t fb = a.tag << 8;   // step-number base of this launch (see persist_layer)
   const int ub = w & 1, wx = w >> 1;
 
   // W_hh rows of this member: LDS row n = ub*64 + gate*16 + u, stored as
@@ -202,11 +203,11 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
       const uint64_t* src = a.X + ((tau - 1) & 1) * slot_stride + ((int64_t)d * a.rows + (rok ? row - a.b0 : 0)) * wpr + tw;
       uint64_t wv[16];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) wv[j] = (rok && j < nj) ? ll_load(src + 16 * j) : ((uint64_t)tau << 32);
+      for (int j = 0; j < 16; ++j) wv[j] = (rok && j < nj) ? ll_load(src + 16 * j) : ((uint64_t)(fb | (uint32_t)tau) << 32);
       for (unsigned it = 0;; ++it) {
         bool bad = false;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) bad |= (uint32_t)(wv[j] >> 32) != (uint32_t)tau;
+        for (int j = 0; j < 16; ++j) bad |= (uint32_t)(wv[j] >> 32)  != (fb | (uint32_t)tau);
         if (!bad) break;
         if (it > SPIN_LIMIT ||
             ((it & 63) == 63 && __hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
@@ -216,7 +217,7 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
         __builtin_amdgcn_s_sleep(1);
 #pragma unroll
         for (int j = 0; j < 16; ++j)
-          if ((uint32_t)(wv[j] >> 32) != (uint32_t)tau) wv[j] = ll_load(src + 16 * j);
+          if ((uint32_t)(wv[j] >> 32)  != (fb | (uint32_t)tau)) wv[j] = ll_load(src + 16 * j);
       }
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
@@ -246,7 +247,7 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
       for (int ks0 = ks_beg; ks0 < ks_end; ks0 += KC) {
         const int nk = min(KC, ks_end - ks0);
         bf16x8 af[MBW][KC];
-        ll_fragments<MBW, KC>(rp, ks0, nk, (uint32_t)tau, lane, af, a.status);
+        ll_fragments<MBW, KC>(rp, ks0, nk, fb | (uint32_t)tau, lane, af, a.status);
 #pragma unroll
         for (int kk = 0; kk < KC; ++kk) {
           if (kk >= nk) break;
@@ -293,7 +294,7 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
           // activations below are only read after the launch
           if ((lane & 1) == 0)
             ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 2, pack_bf16x2(h, h_next_unit),
-                     (uint32_t)(tau + 1));
+                     fb | (uint32_t)(tau + 1));
           const int64_t fr = (int64_t)t * B + row;
           a.C[fr * 2 * H + (int64_t)d * H + unit] = c;
           a.Y[fr * 2 * H + (int64_t)d * H + unit] = (bf16)h;
@@ -334,6 +335,7 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
   const int d = g & 1, s = g >> 1;
   const int u0 = mem * PU;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const uint32_t fb = a.tag << 8;   // step-number base of this launch (see persist_layer)
 
   // LDS: W_hh of the 128 own gate rows, as the B operand [k/8][unit][8]
   // (k = own row kk: gate (kk>>4)&3, unit u0 + (kk>>6)*16 + (kk&15));
@@ -424,11 +426,11 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
           uint64_t wv[H_MAX_MEMBERS];
 #pragma unroll
           for (int k = 0; k < H_MAX_MEMBERS; ++k)
-            wv[k] = k < NM ? ll_load(src + (int64_t)k * H) : ((uint64_t)tau << 32);
+            wv[k] = k < NM ? ll_load(src + (int64_t)k * H) : ((uint64_t)(fb | (uint32_t)tau) << 32);
           for (unsigned it = 0;; ++it) {
             bool bad = false;
 #pragma unroll
-            for (int k = 0; k < H_MAX_MEMBERS; ++k) bad |= (uint32_t)(wv[k] >> 32) != (uint32_t)tau;
+            for (int k = 0; k < H_MAX_MEMBERS; ++k) bad |= (uint32_t)(wv[k] >> 32)  != (fb | (uint32_t)tau);
             if (!bad) break;
             if (it > SPIN_LIMIT ||
                 ((it & 63) == 63 && __hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
@@ -438,7 +440,7 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
             __builtin_amdgcn_s_sleep(1);
 #pragma unroll
             for (int k = 0; k < H_MAX_MEMBERS; ++k)
-              if ((uint32_t)(wv[k] >> 32) != (uint32_t)tau) wv[k] = ll_load(src + (int64_t)k * H);
+              if ((uint32_t)(wv[k] >> 32)  != (fb | (uint32_t)tau)) wv[k] = ll_load(src + (int64_t)k * H);
           }
 #pragma unroll
           for (int k = 0; k < H_MAX_MEMBERS; ++k) {
@@ -543,7 +545,7 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
               const int unit = nb * 16 + (lane & 15);
               if (rowbase + rl < rend && nb < NB)
                 ll_store(xo + (((int64_t)d * rpairs + (rowbase - a.b0 + rl) / 2) * NM + mem) * H + unit,
-                         pack_bf16x2(acc[m][j][2 * r2], acc[m][j][2 * r2 + 1]), (uint32_t)(tau + 1));
+                         pack_bf16x2(acc[m][j][2 * r2], acc[m][j][2 * r2 + 1]), fb | (uint32_t)(tau + 1));
             }
       }
     }
@@ -581,7 +583,7 @@ static int persist_max_wg() {
 }
 
 bool persist_supported(int H, int T) {
-  return H % PU == 0 && H / PU <= H_MAX_MEMBERS && T < (1 << 30) && persist_lds_bytes(H, false, 1) <= 160 * 1024 &&
+  return H % PU == 0 && H / PU <= H_MAX_MEMBERS && T <= 255 && persist_lds_bytes(H, false, 1) <= 160 * 1024 &&
          persist_lds_bytes(H, true, 1) <= 160 * 1024;
 }
 
@@ -622,28 +624,45 @@ static hipError_t launch_one(PersistArgs a, hipStream_t s) {
 
 // Runs all steps of one layer (both directions); returns hipSuccess or the
 // launch error (nothing was enqueued for the failing chunk in that case).
-hipError_t persist_layer(bool backward, PersistArgs a, hipStream_t s) {
-  const int NM = a.H / PU;
+// Rows per workgroup (16*MB) and rows per launch: as few rows as fill the
+// chip, up to 8 row blocks (4 in the backward, whose LDS also holds its own
+// da), more rows by chunking.  False if no launch fits.
+static bool persist_plan(bool backward, int H, int B, int* MBo, int* chunko) {
+  const int NM = H / PU;
   const int max_ns = std::min(persist_max_wg() / (2 * NM), PERSIST_MAX_SLICES);
-  if (max_ns < 1) return hipErrorInvalidValue;
-  // rows per workgroup: as few as fill the chip, up to 8 row blocks (4 in
-  // the backward, whose LDS also holds its own da), more rows by chunking
+  if (max_ns < 1) return false;
   const int mb_cap = backward ? 4 : 8;
   int MB = 1;
-  while (MB < mb_cap && (a.B + 16 * MB - 1) / (16 * MB) > max_ns) MB *= 2;
-  while (MB > 1 && persist_lds_bytes(a.H, backward, MB) > 160 * 1024) MB /= 2;
-  const int chunk = std::min(a.B, max_ns * 16 * MB);
+  while (MB < mb_cap && (B + 16 * MB - 1) / (16 * MB) > max_ns) MB *= 2;
+  while (MB > 1 && persist_lds_bytes(H, backward, MB) > 160 * 1024) MB /= 2;
+  *MBo = MB;
+  *chunko = std::min(B, max_ns * 16 * MB);
+  return (B + *chunko - 1) / *chunko <= 255;
+}
+
+hipError_t persist_clear(bool backward, const PersistArgs& a, hipStream_t s) {
+  int MB, chunk;
+  if (!persist_plan(backward, a.H, a.B, &MB, &chunk)) return hipErrorInvalidValue;
+  // both exchange slots start without any valid step number
+  const int64_t words = backward ? (int64_t)2 * 2 * ((chunk + 1) / 2) * (a.H / PU) * a.H
+                                 : (int64_t)2 * 2 * chunk * (a.H / 2);
+  const int64_t n16 = words / 2;
+  hipLaunchKernelGGL(clear_exchange_kernel, dim3((unsigned)std::min<int64_t>(cdiv(n16, 256), 2048)), dim3(256), 0,
+                     s, (uint4*)a.X, n16, a.status);
+  return hipGetLastError();
+}
+
+hipError_t persist_layer(bool backward, PersistArgs a, hipStream_t s) {
+  int MB, chunk;
+  if (!persist_plan(backward, a.H, a.B, &MB, &chunk)) return hipErrorInvalidValue;
   for (int b0 = 0; b0 < a.B; b0 += chunk) {
     PersistArgs c = a;
     c.b0 = b0;
     c.rows = std::min(chunk, a.B - b0);
     c.NS = (c.rows + 16 * MB - 1) / (16 * MB);
-    // both exchange slots of this chunk start without any valid step number
-    const int64_t words = backward ? (int64_t)2 * 2 * ((c.rows + 1) / 2) * (c.H / PU) * c.H
-                                   : (int64_t)2 * 2 * c.rows * (c.H / 2);
-    const int64_t n16 = words / 2;
-    hipLaunchKernelGGL(clear_exchange_kernel, dim3((unsigned)std::min<int64_t>(cdiv(n16, 256), 2048)),
-                       dim3(256), 0, s, (uint4*)c.X, n16, c.status);
+    // step numbers of this launch: tag = layer * 256 + chunk above the 8-bit
+    // step, so no word left by an earlier launch of the same call matches
+    c.tag = a.tag * 256 + (uint32_t)(b0 / chunk);
     hipError_t e;
     if (backward)
       e = MB == 1 ? launch_one<1, true>(c, s) : MB == 2 ? launch_one<2, true>(c, s) : launch_one<4, true>(c, s);
