@@ -511,28 +511,35 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
     if (tau + 1 < Tn) {
       const int NB = H / 16;
       uint64_t* xo = a.X + (tau & 1) * slot_stride;
+      // the A fragments (own da, 4 k-steps) serve every unit block
+      bf16x8 af[MB][4];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+          af[m][ks] = *(const bf16x8*)&al[((ks * 4 + (lane >> 4)) * (R + 1) + m * 16 + (lane & 15)) * 8];
       for (int base = 0; base < NB; base += 16) {
         f32x4 acc[MB][4];
 #pragma unroll
         for (int m = 0; m < MB; ++m)
 #pragma unroll
           for (int j = 0; j < 4; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        // all B fragments of this pass first (one LDS round trip), then the products
+        bf16x8 bfr[4][4];
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          const int kg = ks * 4 + (lane >> 4);
-          bf16x8 af[MB], bfr[4];
-#pragma unroll
-          for (int m = 0; m < MB; ++m) af[m] = *(const bf16x8*)&al[(kg * (R + 1) + m * 16 + (lane & 15)) * 8];
+        for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int nb = base + w + 4 * j;
-            bfr[j] = nb < NB ? *(const bf16x8*)&wl[(kg * (H + 1) + nb * 16 + (lane & 15)) * 8] : bf16x8{};
+            bfr[ks][j] = nb < NB ? *(const bf16x8*)&wl[((ks * 4 + (lane >> 4)) * (H + 1) + nb * 16 + (lane & 15)) * 8]
+                                 : bf16x8{};
           }
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
           for (int m = 0; m < MB; ++m)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[m][j] = Mfma<bf16>::mma(af[m], bfr[j], acc[m][j]);
-        }
+            for (int j = 0; j < 4; ++j) acc[m][j] = Mfma<bf16>::mma(af[m][ks], bfr[ks][j], acc[m][j]);
         // publish: word (row pair, member, unit), the lane's rows 2r2, 2r2+1
 #pragma unroll
         for (int m = 0; m < MB; ++m)
@@ -589,7 +596,9 @@ bool persist_supported(int H, int T) {
 
 template <int MB, bool BWD>
 static hipError_t launch_one(PersistArgs a, hipStream_t s) {
-  const void* fn = BWD ? (const void*)lstm_bwd_persist<MB> : (const void*)lstm_fwd_persist<MB>;
+  const void* fn;
+  if constexpr (BWD) fn = (const void*)lstm_bwd_persist<MB>;
+  else fn = (const void*)lstm_fwd_persist<MB>;
   const size_t lds = persist_lds_bytes(a.H, BWD, MB);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
