@@ -79,12 +79,19 @@ template <typename T, int NV>
 __global__ __launch_bounds__(256) void softmax_ce_rows_reg_kernel(T* __restrict__ S, int K, int Kp,
                                                                   const int32_t* __restrict__ labels,
                                                                   float scale, float* __restrict__ rowloss) {
+  // One pass over the row: each thread keeps its logits' exponentials
+  // e = exp(s - m_t) against its own maximum m_t and their sum; the
+  // (maximum, sum) pairs are combined across the workgroup (one barrier), and
+  // ds = scale * (e * exp(m_t - m) / sum - [k == label]).  The thread holding
+  // the label's logit writes the frame loss logsumexp - s[label].
   const int64_t m = blockIdx.x;
   T* s = S + m * Kp;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int nvec = Kp / 8;
+  const int lab = labels[m];
   float v[NV][8];
-  float mx = -INFINITY;
+  float mt = -INFINITY, slab = 0.f;
+  bool have_lab = false;
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const int c = tid + 256 * i;
@@ -94,38 +101,44 @@ __global__ __launch_bounds__(256) void softmax_ce_rows_reg_kernel(T* __restrict_
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         v[i][j] = (c * 8 + j < K) ? to_f32(e[j]) : -INFINITY;
-        mx = fmaxf(mx, v[i][j]);
+        mt = fmaxf(mt, v[i][j]);
+        if (c * 8 + j == lab) { slab = v[i][j]; have_lab = true; }
       }
     } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j) v[i][j] = -INFINITY;
     }
   }
-  __shared__ float red[4], sh_lse;
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-  if (lane == 0) red[wid] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  float sm = 0.f;
+  float st = 0.f;
+  const float mref = mt == -INFINITY ? 0.f : mt;   // a thread with padding only
 #pragma unroll
   for (int i = 0; i < NV; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) sm += __expf(v[i][j] - mx);   // exp(-inf) = 0 for padding
+    for (int j = 0; j < 8; ++j) {
+      v[i][j] = __expf(v[i][j] - mref);   // exp(-inf) = 0 for padding
+      st += v[i][j];
+    }
+  // combine (max, sum) pairs: within the wave by shuffles, then the 4 waves
+  float mw = mt, sw = st;
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) sm += __shfl_xor(sm, off);
-  __syncthreads();
-  if (lane == 0) red[wid] = sm;
-  __syncthreads();
-  const int lab = labels[m];
-  if (tid == 0) {
-    const float lse = mx + __logf(red[0] + red[1] + red[2] + red[3]);
-    sh_lse = lse;
-    // an out-of-range label is not read (the loss becomes NaN instead)
-    rowloss[m] = lse - ((lab >= 0 && lab < K) ? to_f32(s[lab]) : __int_as_float(0x7fc00000));
+  for (int off = 32; off > 0; off >>= 1) {
+    const float mo = __shfl_xor(mw, off), so = __shfl_xor(sw, off);
+    const float mn = fmaxf(mw, mo);
+    sw = (mw == -INFINITY ? 0.f : sw * __expf(mw - mn)) + (mo == -INFINITY ? 0.f : so * __expf(mo - mn));
+    mw = mn;
   }
+  __shared__ float rm[4], rs[4];
+  if (lane == 0) { rm[wid] = mw; rs[wid] = sw; }
   __syncthreads();
-  const float lse = sh_lse;
+  const float mx = fmaxf(fmaxf(rm[0], rm[1]), fmaxf(rm[2], rm[3]));
+  float sum = 0.f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) sum += rm[q] == -INFINITY ? 0.f : rs[q] * __expf(rm[q] - mx);
+  const float lse = mx + __logf(sum);
+  if (have_lab) rowloss[m] = lse - slab;
+  // an out-of-range label is not read (the loss becomes NaN instead)
+  if (tid == 0 && !(lab >= 0 && lab < K)) rowloss[m] = __int_as_float(0x7fc00000);
+  const float f = scale * __expf(mref - mx) / sum;
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const int c = tid + 256 * i;
@@ -135,7 +148,7 @@ __global__ __launch_bounds__(256) void softmax_ce_rows_reg_kernel(T* __restrict_
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int k = c * 8 + j;
-      e[j] = from_f32<T>(k < K ? scale * (__expf(v[i][j] - lse) - (k == lab ? 1.f : 0.f)) : 0.f);
+      e[j] = from_f32<T>(k < K ? v[i][j] * f - (k == lab ? scale : 0.f) : 0.f);
     }
     *(uint4*)(s + (int64_t)c * 8) = out;
   }
