@@ -12,6 +12,15 @@
 // operand and k beyond the range end are fetched with an out-of-range buffer
 // offset, which the hardware returns as zeros.
 //
+// An MN-contiguous operand (element (mn, k) at k*ld + mn) is staged as it
+// lies: LDS rows of one k, 256 bytes (128 mn) each, one load instruction
+// filling 4 rows, chunk c of row k in slot c ^ mn_swz(k).  Its MFMA fragments
+// come from gfx950's transposing LDS read (ds_read_b64_tr_b16): within each
+// 16-lane group, lane r points at 4 consecutive mn of k row r/4 and the
+// instruction hands lane i the 4 values of mn column i over those 4 k rows
+// (lane i, element j = lane 4j + i/4's element i%4).  Two such reads give a
+// lane its 8 consecutive k.
+//
 // Per k-tile each workgroup waits for its own oldest tile (vmcnt), meets at
 // one barrier (which also retires the previous tile's LDS reads), refills the
 // slot freed by the previous tile and multiplies the current one.
@@ -65,6 +74,13 @@ __device__ __forceinline__ int kc_slot(int c, int r) {
   else return c ^ ((((r >> 1) ^ (r >> 3)) & 1) | (((r >> 2) & 1) << 1));
 }
 
+// Slot of 16-byte chunk c (8 mn) in k row r of an MN-contiguous tile (16
+// chunks per 256-byte row): the 16 k rows one transposing read touches
+// (r & 3 and bit 3 of r vary) take distinct chunk pairs.
+__device__ __forceinline__ int mn_slot(int c, int r) { return c ^ (2 * ((r & 3) | (((r >> 3) & 1) << 2))); }
+
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
 template <int N>
 __device__ __forceinline__ void kc_wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
@@ -76,16 +92,74 @@ __device__ __forceinline__ void kc_barrier() {
   asm volatile("" ::: "memory");
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, int BK, class Epi>
+// Staging and fragment reads of one operand (rows BMN of the tile's M or N
+// side, BK deep), K-contiguous (KC) or MN-contiguous.
+template <bool KC, int BMN, int BK, int NW>
+struct KcOperand {
+  static constexpr int ROWB = KC ? BK * 2 : BMN * 2;        // LDS row bytes
+  static constexpr int CPR = ROWB / 16;                     // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;                      // rows per load instruction
+  static constexpr int LOADS = (KC ? BMN : BK) / RPI / NW;  // load instructions per wave per k-tile
+  static_assert(LOADS >= 1 && (KC ? BMN : BK) % (RPI * NW) == 0, "tile rows must split over the waves");
+  static_assert(KC || BMN == 128, "MN-contiguous tiles are 128 wide");
+
+  // base: the operand's batch base; mn0: tile's first MN row; ld: row pitch;
+  // mnrows: valid MN rows of this tile (KC) / MN extent left (MNC)
+  __device__ __forceinline__ static void issue(const bf16* base, int64_t ld, int64_t mn0, int64_t mnrows, int64_t k0,
+                                               int64_t kend, char* tile, int wid, int lane) {
+    if constexpr (KC) {
+      const __amdgpu_buffer_rsrc_t r = dma_rsrc(base + mn0 * ld);
+      const int lr = lane / CPR, ls = lane % CPR;
+#pragma unroll
+      for (int q = 0; q < LOADS; ++q) {
+        const int row = (q * NW + wid) * RPI + lr;
+        const int c = kc_slot<BK>(ls, row);   // slot ls holds chunk c (kc_slot is an involution in c)
+        const int64_t k = k0 + c * 8;
+        const uint32_t off = (row < mnrows && k < kend) ? (uint32_t)((row * ld + k) * 2) : DMA_OFF_NONE;
+        dma16(r, off, tile + (q * NW + wid) * 1024);
+      }
+    } else {
+      // per-k-tile base keeps the offsets small for long operands
+      const __amdgpu_buffer_rsrc_t r = dma_rsrc(base + k0 * ld + mn0);
+      const int lr = lane / CPR, ls = lane % CPR;
+#pragma unroll
+      for (int q = 0; q < LOADS; ++q) {
+        const int row = (q * NW + wid) * RPI + lr;   // k row within the tile
+        const int c = mn_slot(ls, row);
+        const bool ok = k0 + row < kend && c * 8 + 8 <= mnrows;
+        dma16(r, ok ? (uint32_t)((row * ld + c * 8) * 2) : DMA_OFF_NONE, tile + (q * NW + wid) * 1024);
+      }
+    }
+  }
+
+  // MFMA fragment (16 MN rows from mnb, 8 consecutive k of 32-k step ks)
+  __device__ __forceinline__ static bf16x8 frag(const char* tile, int mnb, int ks, int lane) {
+    if constexpr (KC) {
+      const int fr = lane & 15, fc = lane >> 4;
+      return *(const bf16x8*)(tile + (mnb + fr) * ROWB + kc_slot<BK>(ks * 4 + fc, fr) * 16);
+    } else {
+      const int g = lane >> 4, r = lane & 15;
+      const int mn = mnb + 4 * (r & 3);
+      bf16x4 h[2];
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int k = ks * 32 + 8 * g + 4 * hh + (r >> 2);
+        const char* pa = tile + k * ROWB + mn_slot(mn >> 3, k) * 16 + (mn & 7) * 2;
+        h[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4*)(pa));
+      }
+      return bf16x8{h[0][0], h[0][1], h[0][2], h[0][3], h[1][0], h[1][1], h[1][2], h[1][3]};
+    }
+  }
+};
+
+template <int BM, int BN, int WM, int WN, int STAGES, int BK, bool AKC, bool BKC, class Epi>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_kc_kernel(const KcArgs p, const Epi epi) {
   constexpr int NW = WM * WN;
-  constexpr int ROWB = BK * 2, CPR = BK / 8, RPI = 64 / CPR;   // row bytes, chunks per row, rows per load
   constexpr int FM = BM / WM / 16, FN = BN / WN / 16;
-  constexpr int LA = BM / RPI / NW, LB = BN / RPI / NW;   // load instructions per wave per k-tile
+  typedef KcOperand<AKC, BM, BK, NW> OA;
+  typedef KcOperand<BKC, BN, BK, NW> OB;
   static_assert(BK == 32 || BK == 64, "k-tile depth");
-  static_assert(LA >= 1 && LB >= 1 && BM % (RPI * NW) == 0 && BN % (RPI * NW) == 0,
-                "tile rows must split over the waves");
-  constexpr int STAGE = (BM + BN) * ROWB;
+  constexpr int TA = BM * BK * 2, STAGE = (BM + BN) * BK * 2;
   extern __shared__ __attribute__((aligned(1024))) char kc_lds[];
 
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -98,35 +172,14 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kc_kernel(const KcArgs p, c
   const int64_t kend = min(p.K, kbeg + p.ksplit);
   const int ntiles = kend > kbeg ? (int)((kend - kbeg + BK - 1) / BK) : 0;
 
-  // buffer resources based at this tile's first row (offsets stay < 2 GiB)
-  const bf16* abase = p.A + (int64_t)z * p.azs + m0 * p.lda;
-  const bf16* bbase = p.B + (int64_t)z * p.bzs + n0 * p.ldb;
-  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)abase, (short)0, 0x7ffffff0, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc((void*)bbase, (short)0, 0x7ffffff0, 0x00020000);
-  const int64_t arows = min((int64_t)BM, p.arows - m0), brows = min((int64_t)BN, p.brows - n0);
-
-  // per lane: row within the rows of one load and the slot it fills
-  const int lr = lane / CPR, ls = lane % CPR;
+  const bf16* abase = p.A + (int64_t)z * p.azs;
+  const bf16* bbase = p.B + (int64_t)z * p.bzs;
+  const int64_t arows = p.arows - m0, brows = p.brows - n0;   // valid MN rows from the tile start
   auto issue = [&](int j) {
     const int64_t k0 = kbeg + (int64_t)j * BK;
     char* st = kc_lds + (j % STAGES) * STAGE;
-#pragma unroll
-    for (int q = 0; q < LA; ++q) {
-      const int r = (q * NW + wid) * RPI + lr;
-      const int c = kc_slot<BK>(ls, r);   // slot ls holds chunk c (kc_slot is an involution in c)
-      const int64_t k = k0 + c * 8;
-      const uint32_t off = (r < arows && k < kend) ? (uint32_t)((r * p.lda + k) * 2) : 0x80000000u;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(st + (q * NW + wid) * 1024), 16, off, 0, 0, 0);
-    }
-#pragma unroll
-    for (int q = 0; q < LB; ++q) {
-      const int r = (q * NW + wid) * RPI + lr;
-      const int c = kc_slot<BK>(ls, r);
-      const int64_t k = k0 + c * 8;
-      const uint32_t off = (r < brows && k < kend) ? (uint32_t)((r * p.ldb + k) * 2) : 0x80000000u;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr_t)(st + BM * ROWB + (q * NW + wid) * 1024), 16, off, 0,
-                                               0, 0);
-    }
+    OA::issue(abase, p.lda, m0, arows, k0, kend, st, wid, lane);
+    OB::issue(bbase, p.ldb, n0, brows, k0, kend, st + TA, wid, lane);
   };
 
   f32x4 acc[FM][FN];
@@ -135,19 +188,15 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kc_kernel(const KcArgs p, c
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int fr = lane & 15, fc = lane >> 4;   // fragment row, chunk within a 32-k step
   auto compute = [&](int j) {
     const char* st = kc_lds + (j % STAGES) * STAGE;
-    const char* la = st + (wm * (BM / WM) + fr) * ROWB;
-    const char* lb = st + BM * ROWB + (wn * (BN / WN) + fr) * ROWB;
 #pragma unroll
     for (int ks = 0; ks < BK / 32; ++ks) {
-      const int slot = kc_slot<BK>(ks * 4 + fc, fr) * 16;   // row offsets below are multiples of 16
       bf16x8 a[FM], b[FN];
 #pragma unroll
-      for (int i = 0; i < FM; ++i) a[i] = *(const bf16x8*)(la + i * 16 * ROWB + slot);
+      for (int i = 0; i < FM; ++i) a[i] = OA::frag(st, wm * (BM / WM) + i * 16, ks, lane);
 #pragma unroll
-      for (int jn = 0; jn < FN; ++jn) b[jn] = *(const bf16x8*)(lb + jn * 16 * ROWB + slot);
+      for (int jn = 0; jn < FN; ++jn) b[jn] = OB::frag(st + TA, wn * (BN / WN) + jn * 16, ks, lane);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -160,7 +209,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kc_kernel(const KcArgs p, c
     if (j < ntiles) issue(j);
   for (int it = 0; it < ntiles; ++it) {
     if (it + STAGES - 2 < ntiles)
-      kc_wait_vm<(STAGES - 2) * (LA + LB)>();
+      kc_wait_vm<(STAGES - 2) * (OA::LOADS + OB::LOADS)>();
     else
       kc_wait_vm<0>();
     kc_barrier();
@@ -171,20 +220,26 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kc_kernel(const KcArgs p, c
 }
 
 // Whether an operand can go through the direct-to-LDS path: plain rows
-// (no segments or gate interleave), 16-byte aligned rows and batch strides.
-static inline bool kc_operand_ok(const Opnd& o, int64_t K) {
-  return o.seg == 0 && o.ilH == 0 && o.ld % 8 == 0 && o.zstride % 8 == 0 &&
-         ((uintptr_t)o.base & 15) == 0 && o.ext >= K;
+// (no segments or gate interleave), 16-byte aligned rows and batch strides,
+// the whole k range inside the operand; MN-contiguous operands also need an
+// MN extent that is a multiple of 8 (whole 16-byte chunks).
+static inline bool kc_operand_ok(const Opnd& o, int64_t K, bool kc) {
+  const bool plain = o.seg == 0 && o.ilH == 0 && o.ld % 8 == 0 && o.zstride % 8 == 0 && ((uintptr_t)o.base & 15) == 0;
+  return plain && (kc ? o.ext >= K : (o.rows >= K && o.ext % 8 == 0));
 }
 
 static int kc_group_rows = 4;   // measured best at the learner-step shapes
 
-template <class C, class Epi>
+template <class C, bool AKC, bool BKC, class Epi>
 static inline void gemm_kc_launch(const char* name, hipStream_t s, const Opnd& A, const Opnd& B, int64_t M,
                                   int64_t N, int64_t K, int batches, int splits, const Epi& epi) {
   KcArgs p;
-  p.A = (const bf16*)A.base; p.lda = A.ld; p.azs = A.zstride; p.arows = std::min(A.rows, M);
-  p.B = (const bf16*)B.base; p.ldb = B.ld; p.bzs = B.zstride; p.brows = std::min(B.rows, N);
+  // MN extent: the row count of a K-contiguous operand (at most the output
+  // extent), the contiguous extent of an MN-contiguous one (whole 16-byte
+  // chunks up to it are loaded even past the output extent, whose rows the
+  // epilogue drops)
+  p.A = (const bf16*)A.base; p.lda = A.ld; p.azs = A.zstride; p.arows = AKC ? std::min<int64_t>(A.rows, M) : A.ext;
+  p.B = (const bf16*)B.base; p.ldb = B.ld; p.bzs = B.zstride; p.brows = BKC ? std::min<int64_t>(B.rows, N) : B.ext;
   p.M = M; p.N = N; p.K = K;
   p.ksplit = splits > 1 ? rup(cdiv(K, splits), C::BK) : (K > 0 ? K : 1);
   p.splits = splits;
@@ -192,7 +247,7 @@ static inline void gemm_kc_launch(const char* name, hipStream_t s, const Opnd& A
   p.ntm = (int)cdiv(M, C::BM);
   p.gm = kc_group_rows;
   p.total = batches * splits * p.ntm * p.ntn;
-  auto fn = gemm_kc_kernel<C::BM, C::BN, C::WM, C::WN, C::STAGES, C::BK, Epi>;
+  auto fn = gemm_kc_kernel<C::BM, C::BN, C::WM, C::WN, C::STAGES, C::BK, AKC, BKC, Epi>;
   static bool attr_set = false;   // raising the LDS limit is per function, once
   if (!attr_set) {
     (void)hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::lds_bytes);
@@ -208,19 +263,21 @@ static inline void gemm_kc_launch(const char* name, hipStream_t s, const Opnd& A
 // blocks per CU.
 typedef KcCfg<128, 128, 2, 4, 2> KcTile;
 
-// GEMM dispatch: bf16 K-contiguous operands with 16-byte aligned rows go to
-// the direct-to-LDS kernel, everything else to the generic kernel.
+// GEMM dispatch: bf16 operands with 16-byte aligned rows go to the
+// direct-to-LDS kernel, everything else to the generic kernel.
 template <typename T, bool AKC, bool BKC, int VA, int VB, class Epi>
 static inline void gemm_launch(const char* name, hipStream_t s, const Opnd& A, const Opnd& B,
                                int64_t M, int64_t N, int64_t K, int batches, int splits,
                                const Epi& epi) {
-  if constexpr (std::is_same<T, bf16>::value && AKC && BKC) {
-    if (K % 8 == 0 && kc_operand_ok(A, K) && kc_operand_ok(B, K)) {
-      gemm_kc_launch<KcTile>(name, s, A, B, M, N, K, batches, splits, epi);
+  if constexpr (std::is_same<T, bf16>::value) {
+    if (K % 8 == 0 && kc_operand_ok(A, K, AKC) && kc_operand_ok(B, K, BKC)) {
+      gemm_kc_launch<KcTile, AKC, BKC>(name, s, A, B, M, N, K, batches, splits, epi);
       return;
     }
-    gemm_launch_cfg<T, GemmCfgK32, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits, epi);
-    return;
+    if constexpr (AKC && BKC) {
+      gemm_launch_cfg<T, GemmCfgK32, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits, epi);
+      return;
+    }
   }
   gemm_launch_cfg<T, GemmCfg<T>, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits, epi);
 }
