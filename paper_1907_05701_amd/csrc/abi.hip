@@ -120,15 +120,20 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   const int BMt = es == 2 ? GemmCfg<bf16>::BM : GemmCfg<float>::BM;
   const int BNt = es == 2 ? GemmCfg<bf16>::BN : GemmCfg<float>::BN;
   const int BKt = es == 2 ? GemmCfg<bf16>::BK : GemmCfg<float>::BK;
+  // each layer's three products own disjoint partial regions (dW_ih, dW_hh,
+  // dX), so that they can run as one grouped launch
   size_t skp = 0;
   L.sp_dWhh = plan_splits(4 * H, H, (int64_t)(d->T - 1) * d->B, BMt, BNt, BKt, 2, es == 2);
-  if (L.sp_dWhh > 1) skp = std::max(skp, (size_t)L.sp_dWhh * 2 * 4 * H * H * 4);
+  const size_t hh_bytes = L.sp_dWhh > 1 ? align256((size_t)L.sp_dWhh * 2 * 4 * H * H * 4) : 0;
   for (int l = 0; l < d->L; ++l) {
     const int64_t Dl = l == 0 ? d->D : 2 * H;
     L.sp_dWih[l] = plan_splits(4 * H, Dl, M, BMt, BNt, BKt, 2, es == 2);
-    if (L.sp_dWih[l] > 1) skp = std::max(skp, (size_t)L.sp_dWih[l] * 2 * 4 * H * Dl * 4);
+    const size_t ih_bytes = L.sp_dWih[l] > 1 ? align256((size_t)L.sp_dWih[l] * 2 * 4 * H * Dl * 4) : 0;
     L.sp_dX[l] = l > 0 ? plan_splits(M, Dl, 8 * H, BMt, BNt, BKt, 1, es == 2) : 1;
-    if (L.sp_dX[l] > 1) skp = std::max(skp, (size_t)L.sp_dX[l] * M * Dl * 4);
+    const size_t dx_bytes = L.sp_dX[l] > 1 ? align256((size_t)L.sp_dX[l] * M * Dl * 4) : 0;
+    L.skp_hh[l] = ih_bytes;
+    L.skp_dx[l] = ih_bytes + hh_bytes;
+    skp = std::max(skp, ih_bytes + hh_bytes + dx_bytes);
   }
   L.SKP = a; a = align256(a + skp);
   L.SKP2 = a; a = align256(a + skp);   // split-K partials of the side-stream products

@@ -152,8 +152,10 @@ struct KcOperand {
   }
 };
 
+// One output tile of one product; w is the workgroup's index within the
+// product's workgroups (those at or past p.total have no tile).
 template <int BM, int BN, int WM, int WN, int STAGES, int BK, bool AKC, bool BKC, class Epi>
-__global__ __launch_bounds__(WM * WN * 64) void gemm_kc_kernel(const KcArgs p, const Epi epi) {
+__device__ __forceinline__ void kc_gemm_tile(const KcArgs& p, const Epi& epi, int w) {
   constexpr int NW = WM * WN;
   constexpr int FM = BM / WM / 16, FN = BN / WN / 16;
   typedef KcOperand<AKC, BM, BK, NW> OA;
@@ -164,8 +166,9 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kc_kernel(const KcArgs p, c
 
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int wm = wid % WM, wn = wid / WM;
+  if (w >= p.total) return;
   int zs, tm, tn;
-  kc_tile_of(p, blockIdx.x, zs, tm, tn);
+  kc_tile_of(p, w, zs, tm, tn);
   const int z = zs / p.splits, sp = zs % p.splits;
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const int64_t kbeg = (int64_t)sp * p.ksplit;
@@ -219,6 +222,30 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kc_kernel(const KcArgs p, c
   epi.template apply<FM, FN>(z, sp, m0 + wm * (BM / WM), n0 + wn * (BN / WN), acc, lane);
 }
 
+template <int BM, int BN, int WM, int WN, int STAGES, int BK, bool AKC, bool BKC, class Epi>
+__global__ __launch_bounds__(WM * WN * 64) void gemm_kc_kernel(const KcArgs p, const Epi epi) {
+  kc_gemm_tile<BM, BN, WM, WN, STAGES, BK, AKC, BKC, Epi>(p, epi, blockIdx.x);
+}
+
+// Several independent products in one launch (fills the chip when each alone
+// would not): product i owns workgroups [start[i], start[i+1]); every start is
+// a multiple of 8 so that the XCD-aware tile order of each product holds.
+#define KC_MAX_GROUP 4
+template <class Epi>
+struct KcGroup {
+  KcArgs p[KC_MAX_GROUP];
+  Epi e[KC_MAX_GROUP];
+  int start[KC_MAX_GROUP + 1];
+  int n;
+};
+
+template <int BM, int BN, int WM, int WN, int STAGES, int BK, bool AKC, bool BKC, class Epi>
+__global__ __launch_bounds__(WM * WN * 64) void gemm_kc_group_kernel(const KcGroup<Epi> g) {
+  int i = 0;
+  while (i + 1 < g.n && (int)blockIdx.x >= g.start[i + 1]) ++i;
+  kc_gemm_tile<BM, BN, WM, WN, STAGES, BK, AKC, BKC, Epi>(g.p[i], g.e[i], (int)blockIdx.x - g.start[i]);
+}
+
 // Whether an operand can go through the direct-to-LDS path: plain rows
 // (no segments or gate interleave), 16-byte aligned rows and batch strides,
 // the whole k range inside the operand; MN-contiguous operands also need an
@@ -230,9 +257,8 @@ static inline bool kc_operand_ok(const Opnd& o, int64_t K, bool kc) {
 
 static int kc_group_rows = 4;   // measured best at the learner-step shapes
 
-template <class C, bool AKC, bool BKC, class Epi>
-static inline void gemm_kc_launch(const char* name, hipStream_t s, const Opnd& A, const Opnd& B, int64_t M,
-                                  int64_t N, int64_t K, int batches, int splits, const Epi& epi) {
+template <class C, bool AKC, bool BKC>
+static inline KcArgs kc_args(const Opnd& A, const Opnd& B, int64_t M, int64_t N, int64_t K, int batches, int splits) {
   KcArgs p;
   // MN extent: the row count of a K-contiguous operand (at most the output
   // extent), the contiguous extent of an MN-contiguous one (whole 16-byte
@@ -247,6 +273,13 @@ static inline void gemm_kc_launch(const char* name, hipStream_t s, const Opnd& A
   p.ntm = (int)cdiv(M, C::BM);
   p.gm = kc_group_rows;
   p.total = batches * splits * p.ntm * p.ntn;
+  return p;
+}
+
+template <class C, bool AKC, bool BKC, class Epi>
+static inline void gemm_kc_launch(const char* name, hipStream_t s, const Opnd& A, const Opnd& B, int64_t M,
+                                  int64_t N, int64_t K, int batches, int splits, const Epi& epi) {
+  const KcArgs p = kc_args<C, AKC, BKC>(A, B, M, N, K, batches, splits);
   auto fn = gemm_kc_kernel<C::BM, C::BN, C::WM, C::WN, C::STAGES, C::BK, AKC, BKC, Epi>;
   static bool attr_set = false;   // raising the LDS limit is per function, once
   if (!attr_set) {
@@ -280,4 +313,39 @@ static inline void gemm_launch(const char* name, hipStream_t s, const Opnd& A, c
     }
   }
   gemm_launch_cfg<T, GemmCfg<T>, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits, epi);
+}
+
+// One product of a grouped launch.
+struct KcItem {
+  Opnd A, B;
+  int64_t M, N, K;
+  int batches, splits;
+};
+
+// Launches products with the same operand layouts as one grid; false (and
+// nothing launched) if any of them cannot take the direct-to-LDS path.
+template <bool AKC, bool BKC, class Epi>
+static inline bool gemm_kc_group_launch(const char* name, hipStream_t s, int n, const KcItem* it, const Epi* epi) {
+  typedef KcTile C;
+  if (n < 1 || n > KC_MAX_GROUP) return false;
+  KcGroup<Epi> g;
+  g.n = n;
+  int start = 0;
+  for (int i = 0; i < n; ++i) {
+    if (it[i].K % 8 != 0 || !kc_operand_ok(it[i].A, it[i].K, AKC) || !kc_operand_ok(it[i].B, it[i].K, BKC))
+      return false;
+    g.p[i] = kc_args<C, AKC, BKC>(it[i].A, it[i].B, it[i].M, it[i].N, it[i].K, it[i].batches, it[i].splits);
+    g.e[i] = epi[i];
+    g.start[i] = start;
+    start += (int)rup(g.p[i].total, 8);
+  }
+  g.start[n] = start;
+  auto fn = gemm_kc_group_kernel<C::BM, C::BN, C::WM, C::WN, C::STAGES, C::BK, AKC, BKC, Epi>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    (void)hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::lds_bytes);
+    attr_set = true;
+  }
+  BLSTM_LAUNCH(name, fn, dim3((unsigned)start), dim3(C::WM * C::WN * 64), C::lds_bytes, s, g);
+  return true;
 }

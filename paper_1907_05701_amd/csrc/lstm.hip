@@ -584,7 +584,11 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       (void)hipStreamWaitEvent(ss, side->bptt_done[l], 0);
     }
     const int64_t Kr = (int64_t)(Tn - 1) * B;
-    bool dw_done = false;
+    float* part_ih = part_side;
+    float* part_hh = (float*)((char*)part_side + lo.skp_hh[l]);
+    float* part_dx = (float*)((char*)part + lo.skp_dx[l]);
+    float* dst_dx = (dY == (const float*)(ws + lo.DYa)) ? (float*)(ws + lo.DYb) : (float*)(ws + lo.DYa);
+    bool dw_done = false, dx_done = l == 0;
     if constexpr (lp) {
       if (lo.xpose_act) {
         // K-contiguous (frame-contiguous) copies for the weight gradients: da^T
@@ -600,14 +604,25 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
         if (l == lo.L - 1) jobs.j[n++] = XposeJob{(const bf16*)Yl, (bf16*)YTl, 2 * H, M, (int)M, 2 * H};
         jobs.j[n++] = XposeJob{(const bf16*)Xl, (bf16*)XTl, Dpl, M, (int)M, Dpl};
         transpose_bf16("transpose_act", ss, jobs, n);
-        // dW_ih[d] = da_d^T X_l  (4H x D_l, reduction over all frames)
-        gemm_f32<T, true, true, V, V>("gemm_dwih", ss, opnd(DAT, M, (int)M, 4 * H, 4 * H * M),
-                                      opnd(XTl, M, (int)M, Dl), 4 * H, Dl, M, 2, lo.sp_dWih[l], grad + lo.Wih[l][0], Dl,
-                                      lo.Wih[l][1] - lo.Wih[l][0], part_side);
-        // dW_hh[d] = sum_t da_d[t]^T h_d[t_prev] (frames shifted as below)
-        gemm_f32<T, true, true, V, V>("gemm_dwhh", ss, opnd(DAT + B, M, (int)Kr, 4 * H, 4 * H * M - B),
-                                      opnd(YTl, M, (int)Kr, H, (int64_t)H * M + B), 4 * H, H, Kr, 2, lo.sp_dWhh,
-                                      grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part_side);
+        // dW_ih[d] = da_d^T X_l  (4H x D_l, reduction over all frames);
+        // dW_hh[d] = sum_t da_d[t]^T h_d[t_prev] (frames shifted as below);
+        // without the side stream also dX_l (below), all in one launch
+        F32Job g[3];
+        g[0] = F32Job{opnd(DAT, M, (int)M, 4 * H, 4 * H * M), opnd(XTl, M, (int)M, Dl), 4 * H, Dl, M, 2,
+                      lo.sp_dWih[l], grad + lo.Wih[l][0], Dl, lo.Wih[l][1] - lo.Wih[l][0], part_ih};
+        g[1] = F32Job{opnd(DAT + B, M, (int)Kr, 4 * H, 4 * H * M - B), opnd(YTl, M, (int)Kr, H, (int64_t)H * M + B),
+                      4 * H, H, Kr, 2, lo.sp_dWhh, grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part_hh};
+        int ng = 2;
+        if (!side && l > 0)
+          g[ng++] = F32Job{opnd(DA, 8 * H, 8 * H, M), opnd(WIT + (int64_t)(l - 1) * 2 * H * 8 * H, 8 * H, 8 * H, Dl),
+                           M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0, part_dx};
+        if (gemm_f32_group<true, true>("gemm_bwd_group", ss, ng, g)) {
+          dx_done = dx_done || ng == 3;
+        } else {
+          for (int i = 0; i < 2; ++i)
+            gemm_f32<T, true, true, V, V>(i ? "gemm_dwhh" : "gemm_dwih", ss, g[i].A, g[i].B, g[i].M, g[i].N, g[i].K,
+                                          g[i].batches, g[i].splits, g[i].dst, g[i].ld, g[i].dst_zstride, g[i].part);
+        }
         dw_done = true;
       }
     }
@@ -616,13 +631,13 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       const Opnd A = opnd(DA, 8 * H, 4 * H, M, 4 * H);
       const Opnd Bx = opnd(Xl, Dpl, Dpl, M);
       gemm_f32<T, false, false, V, V>("gemm_dwih", s, A, Bx, 4 * H, Dl, M, 2, lo.sp_dWih[l],
-                                      grad + lo.Wih[l][0], Dl, lo.Wih[l][1] - lo.Wih[l][0], part);
+                                      grad + lo.Wih[l][0], Dl, lo.Wih[l][1] - lo.Wih[l][0], part_ih);
       // dW_hh[d] = sum_t da_d[t]^T h_d[t_prev]: frames shifted by one step, the
       // forward direction pairing t with t-1 and the reverse direction t with t+1
       const Opnd Ad = opnd(DA + (int64_t)B * 8 * H, 8 * H, 4 * H, Kr, 4 * H - (int64_t)B * 8 * H);
       const Opnd Bh = opnd(Yl, 2 * H, H, Kr, (int64_t)B * 2 * H + H);
       gemm_f32<T, false, false, V, V>("gemm_dwhh", s, Ad, Bh, 4 * H, H, Kr, 2, lo.sp_dWhh,
-                                      grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part);
+                                      grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part_hh);
     }
     // db_ih = db_hh = sum over frames of da
     if (step_fused)
@@ -633,22 +648,21 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
                 grad + lo.bih[l][0], grad + lo.bhh[l][0]);
     if (side) (void)hipEventRecord(side->dw_done[l], ss);
     // dX_l = sum_d da_d W_ih[d]  (the gradient reaching the layer below)
-    if (l > 0) {
+    if (!dx_done) {
       const Opnd A = opnd(DA, 8 * H, 8 * H, M);
-      float* dst = (dY == (const float*)(ws + lo.DYa)) ? (float*)(ws + lo.DYb) : (float*)(ws + lo.DYa);
       if constexpr (lp) {
         const Opnd Bw = opnd(WIT + (int64_t)(l - 1) * 2 * H * 8 * H, 8 * H, 8 * H, Dl);
-        gemm_f32<T, true, true, V, V>("gemm_dx", s, A, Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst, Dl, 0,
-                                      part);
+        gemm_f32<T, true, true, V, V>("gemm_dx", s, A, Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0,
+                                      part_dx);
       } else {
         Opnd Bw = opnd(W + lo.Wih[l][0], Dl, Dl, 8 * H);
         Bw.seg = 4 * H;
         Bw.segstride = lo.Wih[l][1] - lo.Wih[l][0];
-        gemm_f32<T, true, false, V, V>("gemm_dx", s, A, Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst, Dl, 0,
-                                       part);
+        gemm_f32<T, true, false, V, V>("gemm_dx", s, A, Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0,
+                                       part_dx);
       }
-      dY = dst;
     }
+    if (l > 0) dY = dst_dx;
   }
   if (side) (void)hipStreamWaitEvent(s, side->dw_done[0], 0);   // join before returning
   return blstm_check_launch("blstm_bwd");

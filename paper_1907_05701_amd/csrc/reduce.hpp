@@ -133,3 +133,79 @@ static inline void gemm_f32(const char* name, hipStream_t s, const Opnd& A, cons
   BLSTM_LAUNCH("splitk_reduce", splitk_reduce_kernel<T>, dim3(grid), dim3(256), 0, s, part, splits,
                batches, M, N, dst, ld, dst_zstride, dstc, ldc);
 }
+
+// Several float32-destination products in one launch (see gemm_f32), then
+// one launch of all their split-K reductions.
+struct F32Job {
+  Opnd A, B;
+  int64_t M, N, K;
+  int batches, splits;
+  float* dst;
+  int64_t ld, dst_zstride;
+  float* part;   // splits x M x N floats per batch entry when splits > 1
+};
+
+// One reduction of a grouped launch: float4 e of the job covers batch entry
+// z = e / (M N/4), row m and columns 4c..4c+3 of what remains.
+struct ReduceJob {
+  const float* part;
+  float* dst;
+  uint32_t N4, per, count;   // N/4; M N/4; batches M N/4
+  int64_t ld, dst_zstride;
+  int splits, start;         // start: first block of this job
+};
+struct ReduceGroup {
+  ReduceJob j[KC_MAX_GROUP];
+  int n;
+};
+
+static __global__ __launch_bounds__(256) void splitk_reduce_group_kernel(const ReduceGroup g) {
+  int i = 0;
+  while (i + 1 < g.n && (int)blockIdx.x >= g.j[i + 1].start) ++i;
+  const ReduceJob& r = g.j[i];
+  const uint32_t e = ((uint32_t)blockIdx.x - (uint32_t)r.start) * 256u + threadIdx.x;
+  if (e >= r.count) return;
+  const uint32_t z = e / r.per, rem = e - z * r.per;
+  const uint32_t m = rem / r.N4, n = (rem - m * r.N4) * 4;
+  const int64_t mn = (int64_t)r.per * 4;
+  const float* p = r.part + (int64_t)z * r.splits * mn + (int64_t)m * r.N4 * 4 + n;
+  float4 acc = *(const float4*)p;
+  for (int k = 1; k < r.splits; ++k) {
+    const float4 v = *(const float4*)(p + (int64_t)k * mn);
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  *(float4*)(r.dst + (int64_t)z * r.dst_zstride + (int64_t)m * r.ld + n) = acc;
+}
+
+// bf16 products only (the direct-to-LDS kernel); false and nothing launched
+// if a product cannot take that path or its reduction needs unaligned rows.
+template <bool AKC, bool BKC>
+static inline bool gemm_f32_group(const char* name, hipStream_t s, int n, const F32Job* jb) {
+  if (n < 1 || n > KC_MAX_GROUP) return false;
+  KcItem it[KC_MAX_GROUP];
+  EpiStore<float> e[KC_MAX_GROUP];
+  ReduceGroup rg;
+  rg.n = 0;
+  int rblocks = 0;
+  for (int i = 0; i < n; ++i) {
+    const F32Job& j = jb[i];
+    it[i] = KcItem{j.A, j.B, j.M, j.N, j.K, j.batches, j.splits};
+    if (j.splits == 1) {
+      e[i] = epi_store<float>(j.dst, j.ld, j.M, j.N, j.dst_zstride);
+      continue;
+    }
+    const int64_t count = (int64_t)j.batches * j.M * j.N / 4;
+    if (j.N % 4 != 0 || j.ld % 4 != 0 || j.dst_zstride % 4 != 0 || ((uintptr_t)j.dst & 15) != 0 ||
+        ((uintptr_t)j.part & 15) != 0 || count >= ((int64_t)1 << 31))
+      return false;
+    e[i] = epi_store<float>(j.part, j.N, j.M, j.N, (int64_t)j.splits * j.M * j.N, j.M * j.N);
+    ReduceJob& r = rg.j[rg.n++];
+    r.part = j.part; r.dst = j.dst;
+    r.N4 = (uint32_t)(j.N / 4); r.per = (uint32_t)(j.M * j.N / 4); r.count = (uint32_t)count;
+    r.ld = j.ld; r.dst_zstride = j.dst_zstride; r.splits = j.splits; r.start = rblocks;
+    rblocks += (int)cdiv(count, 256);
+  }
+  if (!gemm_kc_group_launch<AKC, BKC>(name, s, n, it, e)) return false;
+  if (rg.n) BLSTM_LAUNCH("splitk_reduce_group", splitk_reduce_group_kernel, dim3((unsigned)rblocks), dim3(256), 0, s, rg);
+  return true;
+}
