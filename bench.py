@@ -141,6 +141,86 @@ def cpu_baseline(cfg, budget_s=12.0):
                       f"dimensions with B={Bs} of {cfg['B']} sequences, {el:.1f} s"}
 
 
+def update_bytes(n, R, write_peer, shadow):
+    """Algorithmic HBM bytes of one fused update: R replica gradients, theta
+    and theta_peer read once, theta written (and theta_peer, the bf16 copy)."""
+    return n * (4 * R + 4 + 4 + 4 + (4 if write_peer else 0) + (2 if shadow else 0))
+
+
+def cpu_update_baseline(n, R, lr, budget_s=12.0):
+    """The float32-order oracle update on the host on a bounded slice of the
+    parameter vector, in GB/s of the same algorithmic bytes."""
+    import numpy as np
+    from oracle import blstm_ref as ref
+    from paper_1907_05701_amd import inputs
+    ns = min(n, 1 << 22)
+    theta = inputs.params(ns)
+    peer = inputs.peer(theta)
+    grads = inputs.replica_grads(ns, R)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        ref.adpsgd_update_fp32(theta, peer, grads, 1.0 / R, lr)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 200:
+            break
+    return {"value": round(update_bytes(ns, R, False, False) * reps / el / 1e9, 3), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{reps} float32-order oracle update(s) of the first {ns} of {n} parameters "
+                      f"with R={R}, {el:.1f} s (numpy, one thread)"}
+
+
+def bench_update(args, cfg):
+    """The update-only workload: R resident replica gradients of the full
+    model's flat parameter vector, fused sum + SGD + pairwise averaging.
+    Timed with HIP events on the launching stream; value in HBM GB/s of the
+    algorithmic bytes, for the plain update and its variants (peer write,
+    bf16 operand copy)."""
+    import torch
+    from paper_1907_05701_amd import binding as bd
+    from paper_1907_05701_amd import inputs
+    R, lr = cfg["R"], cfg["lr"]
+    n = bd.blstm_param_count(bd.make_dims(*(cfg[k] for k in "LDHPKTB"), "fp32"))
+    dev = torch.device("cuda:0")
+    theta0 = inputs.params(n)
+    th = torch.from_numpy(theta0).to(dev)
+    pe = torch.from_numpy(inputs.peer(theta0)).to(dev)
+    gs = [torch.from_numpy(g).to(dev) for g in inputs.replica_grads(n, R)]
+    lp = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    s = torch.cuda.current_stream()
+    variants = {"plain": (0, None), "write_peer": (bd.ADPSGD_WRITE_PEER, None), "bf16_copy": (0, lp),
+                "write_peer_bf16_copy": (bd.ADPSGD_WRITE_PEER, lp)}
+    res = {}
+    for name, (flags, shadow) in variants.items():
+        for _ in range(args.warmup):
+            bd.adpsgd_step(th, pe, gs, 1.0 / R, lr, flags, shadow)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(s)
+        for _ in range(args.steps):
+            bd.adpsgd_step(th, pe, gs, 1.0 / R, lr, flags, shadow)
+        e1.record(s)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / args.steps
+        nbytes = update_bytes(n, R, flags & bd.ADPSGD_WRITE_PEER, shadow is not None)
+        res[name] = {"bytes_per_param": nbytes // n, "us": round(us, 2), "GB/s": round(nbytes / us / 1e3, 1)}
+    base = res["plain"]
+    out = {"metric": "fused replica-sum + SGD + averaging update, HBM GB/s", "value": base["GB/s"],
+           "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(base["us"] / 1e3, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "fp32", "data": "synthetic",
+           "config": {"workload": args.workload, "n": n, "R": R, "lr": lr},
+           "roofline": {"bound": "hbm", "achieved": base["GB/s"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(base["GB/s"] / PEAK_HBM_GBS, 5),
+                        "traffic": recorded_traffic("adpsgd_update", args.workload), "kernel": "adpsgd_update",
+                        "avg_launch_us": base["us"], "algorithmic_per_launch": update_bytes(n, R, False, False),
+                        "algorithmic_unit": "byte"},
+           "variants": res}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_update_baseline(n, R, lr)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -169,7 +249,8 @@ def main():
 
     cfg = dict(inputs.CONFIGS[args.workload])
     if "R" in cfg:
-        raise SystemExit("the update-only workload is measured by the update test, not here")
+        bench_update(args, cfg)
+        return
     shape = {k: cfg[k] for k in "LDHPKTB"}
     st = LearnerStep(**shape, precision=cfg["precision"])
     theta = inputs.params(st.n)

@@ -122,6 +122,52 @@ def test_full_model_dims_fp32_b8(gpu_lib):
                          dist="zipf", check_update=False)
 
 
+def run_replicated_and_compare(shape, reps, tol, seed=11):
+    """The step at a large batch built from `reps` copies of a small seeded
+    batch of shape["B"] sequences.  Sequences are independent in the model
+    and the loss is a mean over frames, so the loss and the gradient equal
+    those of the small batch and every copy's y_top equals the small batch's:
+    the oracle runs on the small batch only, while the GPU runs the full
+    batch in the launch configuration of the large workload."""
+    from paper_1907_05701_amd.step import LearnerStep
+    dims = ref.Dims(**shape)
+    B0, T = dims.B, dims.T
+    big = dict(shape, B=B0 * reps)
+    say(f"[parity] replicated batch {B0} x {reps}: shape={big}")
+    n = ref.param_count(dims)
+    theta = inputs.params(n, seed=seed)
+    x = inputs.features(T, B0, dims.D, seed=seed + 1)
+    lab = inputs.labels(T, B0, dims.K, seed=seed + 2, dist="zipf")
+    xb = np.ascontiguousarray(np.tile(x, (1, reps, 1)))
+    lb = np.ascontiguousarray(np.tile(lab, (1, reps)))
+    st = LearnerStep(**big, precision="bf16")
+    st.load(theta, xb, lb, inputs.peer(theta, seed=seed + 3))
+    st.gradient()
+    torch.cuda.synchronize()
+    want = ref.learner_gradient(theta, dims, x, lab)
+    loss = float(st.loss.cpu()[0])
+    y = st.y_top.float().cpu().numpy().reshape(T, reps, B0, -1)
+    errs = {"loss": abs(loss - want["loss"]) / abs(want["loss"])}
+    for c in sorted({0, reps // 2, reps - 1}):
+        errs[f"y_top copy {c}"] = rel(y[:, c], want["y_top"])
+    grad = st.grad.cpu().numpy()
+    errs.update({str(k): v for k, v in block_errors(grad, want["grad"], dims).items()})
+    worst = max(errs.items(), key=lambda kv: kv[1])
+    say(f"[parity] loss gpu={loss:.7f} ref={want['loss']:.7f}; worst {worst[0]}={worst[1]:.3e}")
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, bad
+
+
+def test_full_model_b512_replicated(gpu_lib):
+    """The large-batch workload (B = 512, T = 21) as 32 copies of 16 sequences."""
+    run_replicated_and_compare(dict(L=6, D=260, H=512, P=256, K=32000, T=21, B=16), 32, BF16_TOL)
+
+
+def test_stress_t64_b1024_replicated(gpu_lib):
+    """The stress workload (T = 64, B = 1024) as 64 copies of 16 sequences."""
+    run_replicated_and_compare(dict(L=6, D=260, H=512, P=256, K=32000, T=64, B=16), 64, BF16_TOL, seed=21)
+
+
 @pytest.mark.parametrize("B", [200, 300, 1100], ids=["mb2", "mb4", "mb8_two_chunks"])
 def test_recurrence_batch_regimes_bf16(gpu_lib, B):
     """Batches large enough that each recurrent workgroup covers 2, 4 or 8
