@@ -111,7 +111,7 @@ __device__ __forceinline__ void ll_fragments(const uint64_t* const (&rp)[MBW], i
 // Forward.
 // ---------------------------------------------------------------------------
 template <int MB>
-__global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void lstm_fwd_persist(const PersistArgs a) {
   extern __shared__ __attribute__((aligned(16))) bf16 lds[];
   constexpr bool KSPLIT = MB == 1;
   constexpr int MBW = KSPLIT ? 1 : MB / 2;
@@ -126,12 +126,14 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
   const uint32_t fb = a.tag << 8;   // step-number base of this launch (see persist_layer)
   const int ub = w & 1, wx = w >> 1;
 
-  // W_hh rows of this member: LDS row n = ub*64 + gate*16 + u, stored as
-  // [k/8][n][8]; staged with direct-to-LDS loads (one load fills 64
-  // consecutive rows of one 8-wide k chunk), all in flight at once
+  // W_hh rows of this member.  MB > 1: in LDS, row n = ub*64 + gate*16 + u,
+  // stored as [k/8][n][8]; staged with direct-to-LDS loads (one load fills
+  // 64 consecutive rows of one 8-wide k chunk), all in flight at once.
+  // MB == 1: in registers (below), each wave holding the fragments of its
+  // unit block and k half, so the products read no W from LDS.
   const bf16* Wd = a.W + (d ? a.whh1 : a.whh0);
   const int kcn = H / 8;
-  {
+  if constexpr (!KSPLIT) {
     const __amdgpu_buffer_rsrc_t rw = dma_rsrc(Wd);
     const int n = (w & 1) * 64 + lane;   // row of this lane
     const int64_t row = (int64_t)((n >> 4) & 3) * H + u0 + (n >> 6) * 16 + (n & 15);
@@ -139,7 +141,7 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
       dma16(rw, (uint32_t)((row * H + kc * 8) * 2), lds + (kc * LDN + (w & 1) * 64) * 8);
     dma_wait_all();
   }
-  f32x4* red = (f32x4*)(lds + (size_t)kcn * LDN * 8);
+  f32x4* red = (f32x4*)(lds + (KSPLIT ? (size_t)0 : (size_t)kcn * LDN * 8));
   bf16* hl = (bf16*)(red + 8 * 64);   // MB == 1: gathered h [H/8][16 + 1][8]
   __syncthreads();
 
@@ -151,6 +153,20 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
   const int nks = H / 32;
   const int ks_beg = KSPLIT ? (wx ? nks / 2 : 0) : 0;
   const int ks_end = KSPLIT ? (wx ? nks : nks / 2) : nks;
+  // MB == 1: B fragments of the k half (at most H_MAX_MEMBERS / 2 k-steps;
+  // lane l: gate row q*H + unit, k = ks*32 + (l/16)*8 .. +8); k-steps past
+  // the half's end hold a valid k-step and meet a zero A fragment
+  constexpr int KH = H_MAX_MEMBERS / 2;
+  bf16x8 bw[KSPLIT ? KH : 1][4];
+  if constexpr (KSPLIT) {
+#pragma unroll
+    for (int i = 0; i < KH; ++i) {
+      const int ks = max(0, min(ks_beg + i, ks_end - 1));
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        bw[i][q] = *(const bf16x8*)(Wd + (int64_t)(q * H + unit) * H + ks * 32 + (lane >> 4) * 8);
+    }
+  }
   const int wpr = H / 2;                        // exchange words per row
   const int64_t slot_stride = (int64_t)2 * a.rows * wpr;
 
@@ -226,15 +242,19 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
         *(uint32_t*)&hl[((k >> 3) * 17 + tr) * 8 + (k & 7)] = rok ? (uint32_t)wv[j] : 0u;
       }
       __syncthreads();
-      for (int ks = ks_beg; ks < ks_end; ++ks) {
+      // A fragments of the half (W is in registers), then the products
+      bf16x8 af[KH];
+#pragma unroll
+      for (int i = 0; i < KH; ++i) {
+        const int ks = max(0, min(ks_beg + i, ks_end - 1));
         const int kg = ks * 4 + (lane >> 4);
-        const bf16x8 af = *(const bf16x8*)&hl[(kg * 17 + (lane & 15)) * 8];
-        bf16x8 bfr[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) bfr[q] = *(const bf16x8*)&lds[(kg * LDN + ub * 64 + q * 16 + (lane & 15)) * 8];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) acc[0][q] = Mfma<bf16>::mma(af, bfr[q], acc[0][q]);
+        af[i] = *(const bf16x8*)&hl[(kg * 17 + (lane & 15)) * 8];
+        if (ks_beg + i >= ks_end) af[i] = bf16x8{};
       }
+#pragma unroll
+      for (int i = 0; i < KH; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[0][q] = Mfma<bf16>::mma(af[i], bw[i][q], acc[0][q]);
     } else if (tau > 0) {
       // h of the previous step, published with step number tau
       const uint64_t* rp[MBW];
@@ -275,34 +295,44 @@ __global__ __launch_bounds__(256) void lstm_fwd_persist(const PersistArgs a) {
       }
     }
     if (epi) {
+      // cell math of all rows, then h published (the other members wait for
+      // it), then the saved activations (only read after the launch)
       uint64_t* xo = a.X + (tau & 1) * slot_stride;
+      float hv[MBW][4], gv[MBW][4][4];
+#pragma unroll
+      for (int m = 0; m < MBW; ++m)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          gv[m][r][0] = sigmoidf_(acc[m][0][r] + (float)gx[m][r][0]);
+          gv[m][r][1] = sigmoidf_(acc[m][1][r] + (float)gx[m][r][1]);
+          gv[m][r][2] = tanhf_(acc[m][2][r] + (float)gx[m][r][2]);
+          gv[m][r][3] = sigmoidf_(acc[m][3][r] + (float)gx[m][r][3]);
+          const float c = gv[m][r][1] * creg[m][r] + gv[m][r][0] * gv[m][r][2];
+          creg[m][r] = c;
+          hv[m][r] = gv[m][r][3] * tanhf_(c);
+        }
 #pragma unroll
       for (int m = 0; m < MBW; ++m)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int row = rowbase + (mb0 + m) * 16 + (lane >> 4) * 4 + r;
-          const float ig = sigmoidf_(acc[m][0][r] + (float)gx[m][r][0]);
-          const float fg = sigmoidf_(acc[m][1][r] + (float)gx[m][r][1]);
-          const float gg = tanhf_(acc[m][2][r] + (float)gx[m][r][2]);
-          const float og = sigmoidf_(acc[m][3][r] + (float)gx[m][r][3]);
-          const float c = fg * creg[m][r] + ig * gg;
-          creg[m][r] = c;
-          const float h = og * tanhf_(c);
-          const float h_next_unit = __shfl_xor(h, 1);   // lanes of one row, units u and u^1
-          if (row >= rend) continue;
-          // publish h first: the other members wait for it, the saved
-          // activations below are only read after the launch
-          if ((lane & 1) == 0)
-            ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 2, pack_bf16x2(h, h_next_unit),
+          const float h_next_unit = __shfl_xor(hv[m][r], 1);   // lanes of one row, units u and u^1
+          if (row < rend && (lane & 1) == 0)
+            ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 2, pack_bf16x2(hv[m][r], h_next_unit),
                      fb | (uint32_t)(tau + 1));
+        }
+#pragma unroll
+      for (int m = 0; m < MBW; ++m)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = rowbase + (mb0 + m) * 16 + (lane >> 4) * 4 + r;
+          if (row >= rend) continue;
           const int64_t fr = (int64_t)t * B + row;
-          a.C[fr * 2 * H + (int64_t)d * H + unit] = c;
-          a.Y[fr * 2 * H + (int64_t)d * H + unit] = (bf16)h;
+          a.C[fr * 2 * H + (int64_t)d * H + unit] = creg[m][r];
+          a.Y[fr * 2 * H + (int64_t)d * H + unit] = (bf16)hv[m][r];
           bf16* gs = a.G + fr * 8 * H + (int64_t)d * 4 * H + unit;
-          gs[0] = (bf16)ig;
-          gs[H] = (bf16)fg;
-          gs[2 * H] = (bf16)gg;
-          gs[3 * H] = (bf16)og;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) gs[q * H] = (bf16)gv[m][r][q];
         }
     }
     if (epi && tau + 1 < Tn) load_gx(d ? Tn - 2 - tau : tau + 1);
@@ -577,7 +607,9 @@ __global__ __launch_bounds__(256) void clear_exchange_kernel(uint4* p, int64_t n
 size_t persist_lds_bytes(int H, bool backward, int MB) {
   if (backward)
     return (size_t)16 * (H + 1) * 16 + (size_t)16 * (16 * MB + 1) * 16 + (size_t)16 * MB * PU * 4;
-  return (size_t)(H / 8) * (128 + 1) * 16 + 8 * 64 * 16 + (MB == 1 ? (size_t)(H / 8) * 17 * 16 : 0);
+  // MB == 1 keeps W_hh in registers: reduction buffer and gathered h only
+  if (MB == 1) return (size_t)8 * 64 * 16 + (size_t)(H / 8) * 17 * 16;
+  return (size_t)(H / 8) * (128 + 1) * 16 + 8 * 64 * 16;
 }
 
 // Workgroups that can be co-resident: one per compute unit (the LDS slice
@@ -590,7 +622,7 @@ static int persist_max_wg() {
 }
 
 bool persist_supported(int H, int T) {
-  return H % PU == 0 && H / PU <= H_MAX_MEMBERS && T <= 255 && persist_lds_bytes(H, false, 1) <= 160 * 1024 &&
+  return H % PU == 0 && H / PU <= H_MAX_MEMBERS && T <= 255 && persist_lds_bytes(H, false, 2) <= 160 * 1024 &&
          persist_lds_bytes(H, true, 1) <= 160 * 1024;
 }
 
