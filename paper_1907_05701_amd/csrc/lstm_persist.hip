@@ -355,7 +355,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 // takes 256 contiguous bytes of each member.
 // ---------------------------------------------------------------------------
 template <int MB>
-__global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void lstm_bwd_persist(const PersistArgs a) {
   extern __shared__ __attribute__((aligned(16))) bf16 lds[];
   constexpr int R = 16 * MB;            // rows of this member's slice
   constexpr int ITEMS = 2 * MB;         // (row, unit) cell items per thread
@@ -368,12 +368,43 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
   const uint32_t fb = a.tag << 8;   // step-number base of this launch (see persist_layer)
 
   // LDS: W_hh of the 128 own gate rows, as the B operand [k/8][unit][8]
-  // (k = own row kk: gate (kk>>4)&3, unit u0 + (kk>>6)*16 + (kk&15));
-  // own da as the A operand [k/8][row][8]; gathered dh_rec [row][32] fp32.
+  // (k = own row kk: gate (kk>>4)&3, unit u0 + (kk>>6)*16 + (kk&15)), for
+  // MB > 1 (MB == 1 holds it in registers, below); own da as the A operand
+  // [k/8][row][8]; gathered dh_rec [row][32] fp32.
+  constexpr bool WREG = MB == 1;
   bf16* wl = lds;
-  bf16* al = wl + (size_t)16 * (H + 1) * 8;
+  bf16* al = wl + (WREG ? (size_t)0 : (size_t)16 * (H + 1) * 8);
   float* dhl = (float*)(al + (size_t)16 * (R + 1) * 8);
-  if (a.WT && H % 64 == 0) {
+  const int NB = H / 16;
+  // MB == 1: B fragments of the unit blocks nb = 16*bi + w + 4*j of this
+  // wave, k-step ks (lane l: own rows ks*32 + (l/16)*8 .. +8, unit
+  // nb*16 + l%16), from W_hh^T (16 contiguous bytes) or else W_hh
+  bf16x8 bw[WREG ? 2 : 1][4][4];
+  if constexpr (WREG) {
+    const bf16* WTd = a.WT ? a.WT + (int64_t)d * H * 4 * H : nullptr;
+    const bf16* Wd = a.W + (d ? a.whh1 : a.whh0);
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int nb = bi * 16 + w + 4 * j;
+          const int kk = ks * 32 + (lane >> 4) * 8;
+          const int64_t grow = (int64_t)((kk >> 4) & 3) * H + u0 + (kk >> 6) * 16 + (kk & 15);
+          const int64_t n = (int64_t)nb * 16 + (lane & 15);
+          bf16x8 v{};
+          if (nb < NB) {
+            if (WTd) {
+              v = *(const bf16x8*)(WTd + n * 4 * H + grow);
+            } else {
+#pragma unroll
+              for (int i = 0; i < 8; ++i) v[i] = Wd[(grow + i) * H + n];
+            }
+          }
+          bw[bi][ks][j] = v;
+        }
+  } else if (a.WT && H % 64 == 0) {
     // from W_hh^T [H][4H] (made by the caller): the 8 own rows of k group kg
     // are 16 contiguous bytes of W_hh^T row j; one direct-to-LDS load fills
     // 64 consecutive j of one k group (a load always writes all 64 slots, so
@@ -386,7 +417,7 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
       dma16(rw, (uint32_t)(((int64_t)j * 4 * H + grow) * 2), wl + (kg * (H + 1) + (c / 16) * 64) * 8);
     }
     dma_wait_all();
-  } else {
+  } else if constexpr (!WREG) {
     const bf16* Wd = a.W + (d ? a.whh1 : a.whh0);
     for (int b = tid; b < 16 * (H / 8); b += 256) {
       const int kg = b % 16, jb = b / 16;
@@ -539,7 +570,6 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
 
     // P = da_own [R x 128] * W_own [128 x H]; 16-unit block nb goes to wave nb % 4
     if (tau + 1 < Tn) {
-      const int NB = H / 16;
       uint64_t* xo = a.X + (tau & 1) * slot_stride;
       // the A fragments (own da, 4 k-steps) serve every unit block
       bf16x8 af[MB][4];
@@ -548,21 +578,28 @@ __global__ __launch_bounds__(256) void lstm_bwd_persist(const PersistArgs a) {
 #pragma unroll
         for (int m = 0; m < MB; ++m)
           af[m][ks] = *(const bf16x8*)&al[((ks * 4 + (lane >> 4)) * (R + 1) + m * 16 + (lane & 15)) * 8];
-      for (int base = 0; base < NB; base += 16) {
+#pragma unroll
+      for (int bi = 0; bi < H_MAX_MEMBERS / 8; ++bi) {
+        const int base = bi * 16;
+        if (base >= NB) break;
         f32x4 acc[MB][4];
 #pragma unroll
         for (int m = 0; m < MB; ++m)
 #pragma unroll
           for (int j = 0; j < 4; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        // all B fragments of this pass first (one LDS round trip), then the products
+        // all B fragments of this pass first (registers, or one LDS round
+        // trip), then the products
         bf16x8 bfr[4][4];
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int nb = base + w + 4 * j;
-            bfr[ks][j] = nb < NB ? *(const bf16x8*)&wl[((ks * 4 + (lane >> 4)) * (H + 1) + nb * 16 + (lane & 15)) * 8]
-                                 : bf16x8{};
+            if constexpr (WREG)
+              bfr[ks][j] = bw[bi][ks][j];
+            else
+              bfr[ks][j] = nb < NB ? *(const bf16x8*)&wl[((ks * 4 + (lane >> 4)) * (H + 1) + nb * 16 + (lane & 15)) * 8]
+                                   : bf16x8{};
           }
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks)
@@ -605,8 +642,9 @@ __global__ __launch_bounds__(256) void clear_exchange_kernel(uint4* p, int64_t n
 // Host side.
 // ---------------------------------------------------------------------------
 size_t persist_lds_bytes(int H, bool backward, int MB) {
-  if (backward)
-    return (size_t)16 * (H + 1) * 16 + (size_t)16 * (16 * MB + 1) * 16 + (size_t)16 * MB * PU * 4;
+  if (backward)   // MB == 1 keeps W_hh in registers
+    return (MB == 1 ? (size_t)0 : (size_t)16 * (H + 1) * 16) + (size_t)16 * (16 * MB + 1) * 16 +
+           (size_t)16 * MB * PU * 4;
   // MB == 1 keeps W_hh in registers: reduction buffer and gathered h only
   if (MB == 1) return (size_t)8 * 64 * 16 + (size_t)(H / 8) * 17 * 16;
   return (size_t)(H / 8) * (128 + 1) * 16 + 8 * 64 * 16;
@@ -623,7 +661,7 @@ static int persist_max_wg() {
 
 bool persist_supported(int H, int T) {
   return H % PU == 0 && H / PU <= H_MAX_MEMBERS && T <= 255 && persist_lds_bytes(H, false, 2) <= 160 * 1024 &&
-         persist_lds_bytes(H, true, 1) <= 160 * 1024;
+         persist_lds_bytes(H, true, 2) <= 160 * 1024;
 }
 
 template <int MB, bool BWD>
