@@ -453,26 +453,45 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
   for (int m = 0; m < MB; ++m) dbacc[m] = 0.f;
 
-  for (int tau = 0; tau < Tn; ++tau) {
-    const int t = d ? tau : Tn - 1 - tau;
-    const int tp = d ? t + 1 : t - 1;
-    const bool has_prev = tp >= 0 && tp < Tn;
-    // everything the cell derivative needs besides dh_rec
-    float dy[ITEMS], cc[ITEMS], cp[ITEMS];
-    bf16 gt[ITEMS][4];   // converted in the cell phase, so the gather does not wait for these loads
+  // everything the cell derivative needs besides dh_rec: dy, the gates and
+  // c at t, c at the step's predecessor in forward time (which is the next
+  // step's t).  Fetched one step ahead, right after the previous step's
+  // gather, so that no gather waits for them; c at t is the previous step's
+  // predecessor value.
+  float dyn[ITEMS], cpn[ITEMS], cc[ITEMS];
+  bf16 gtn[ITEMS][4];
+  auto fetch = [&](int tau_) {
+    const int t_ = d ? tau_ : Tn - 1 - tau_;
+    const int tp_ = d ? t_ + 1 : t_ - 1;
+    const bool hp = tp_ >= 0 && tp_ < Tn;
 #pragma unroll
     for (int i = 0; i < ITEMS; ++i) {
       int row = rowbase + (tid >> 5) + 8 * i;
       row = row < rend ? row : a.b0;
-      const int64_t fr = (int64_t)t * B + row;
+      const int64_t fr = (int64_t)t_ * B + row;
       const int unit = u0 + cu;
-      dy[i] = a.DY[fr * 2 * H + (int64_t)d * H + unit];
-      cc[i] = a.C[fr * 2 * H + (int64_t)d * H + unit];
-      cp[i] = has_prev ? a.C[((int64_t)tp * B + row) * 2 * H + (int64_t)d * H + unit] : 0.f;
+      dyn[i] = a.DY[fr * 2 * H + (int64_t)d * H + unit];
+      cpn[i] = hp ? a.C[((int64_t)tp_ * B + row) * 2 * H + (int64_t)d * H + unit] : 0.f;
       const bf16* gs = a.G + fr * 8 * H + (int64_t)d * 4 * H + unit;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) gt[i][q] = gs[q * H];
+      for (int q = 0; q < 4; ++q) gtn[i][q] = gs[q * H];
     }
+  };
+  {
+    const int t0 = d ? 0 : Tn - 1;
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      int row = rowbase + (tid >> 5) + 8 * i;
+      row = row < rend ? row : a.b0;
+      cc[i] = a.C[((int64_t)t0 * B + row) * 2 * H + (int64_t)d * H + u0 + cu];
+    }
+  }
+  fetch(0);
+
+  for (int tau = 0; tau < Tn; ++tau) {
+    const int t = d ? tau : Tn - 1 - tau;
+    float dy[ITEMS], cp[ITEMS];
+    bf16 gt[ITEMS][4];
 
     // gather dh_rec for the own units: items (row pair, unit), unit = tid % 32;
     // the 32 threads of a row pair read 32 adjacent words (256 bytes) per member
@@ -518,6 +537,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       for (int i = tid; i < R * PU; i += 256) dhl[i] = 0.f;
     }
     __syncthreads();
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      dy[i] = dyn[i];
+      cp[i] = cpn[i];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) gt[i][q] = gtn[i][q];
+    }
+    if (tau + 1 < Tn) fetch(tau + 1);
 
     // cell derivatives; da goes to global memory (weight gradients) and to
     // LDS (next partial product)
@@ -545,6 +572,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         const int kk = (cu >> 4) * 64 + q * 16 + (cu & 15);
         al[((kk >> 3) * (R + 1) + r) * 8 + (kk & 7)] = v;
       }
+      cc[i] = cp[i];   // c at the next step's t
     }
     __syncthreads();
 
