@@ -563,11 +563,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       da[2] = dc * ig * (1.f - gg * gg);
       da[3] = dh * tc * og * (1.f - og);
       const bool ok = row < rend;
-      bf16* dst = a.DA + ((int64_t)t * B + (ok ? row : a.b0)) * 8 * H + (int64_t)d * 4 * H + u0 + cu;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const bf16 v = ok ? (bf16)da[q] : (bf16)0.f;
-        if (ok) dst[q * H] = v;
         // own row kk = (cu >> 4)*64 + q*16 + (cu & 15)
         const int kk = (cu >> 4) * 64 + q * 16 + (cu & 15);
         al[((kk >> 3) * (R + 1) + r) * 8 + (kk & 7)] = v;
@@ -576,6 +574,78 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
     __syncthreads();
 
+    // P = da_own [R x 128] * W_own [128 x H]; 16-unit block nb goes to wave
+    // nb % 4.  On the critical path, so before the global copies of da.
+    if (tau + 1 < Tn) {
+      uint64_t* xo = a.X + (tau & 1) * slot_stride;
+      // the A fragments (own da, 4 k-steps) serve every unit block
+      bf16x8 af[MB][4];
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+          af[m][ks] = *(const bf16x8*)&al[((ks * 4 + (lane >> 4)) * (R + 1) + m * 16 + (lane & 15)) * 8];
+      // unit blocks per pass and wave: all (up to 8) with W in registers,
+      // else 4 per pass (two passes cover H_MAX_MEMBERS * 32 units)
+      constexpr int JP = WREG ? 8 : 4;
+#pragma unroll
+      for (int bi = 0; bi < (WREG ? 1 : H_MAX_MEMBERS / 8); ++bi) {
+        const int base = bi * 16;
+        if (base >= NB) break;
+        f32x4 acc[MB][JP];
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+#pragma unroll
+          for (int j = 0; j < JP; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        // all B fragments of this pass first (registers, or one LDS round
+        // trip), then the products
+        bf16x8 bfr[4][JP];
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+          for (int j = 0; j < JP; ++j) {
+            const int nb = base + w + 4 * j;
+            if constexpr (WREG)
+              bfr[ks][j] = bw[j / 4][ks][j % 4];
+            else
+              bfr[ks][j] = nb < NB ? *(const bf16x8*)&wl[((ks * 4 + (lane >> 4)) * (H + 1) + nb * 16 + (lane & 15)) * 8]
+                                   : bf16x8{};
+          }
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+          for (int m = 0; m < MB; ++m)
+#pragma unroll
+            for (int j = 0; j < JP; ++j) acc[m][j] = Mfma<bf16>::mma(af[m][ks], bfr[ks][j], acc[m][j]);
+        // publish: word (row pair, member, unit), the lane's rows 2r2, 2r2+1
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+#pragma unroll
+          for (int j = 0; j < JP; ++j)
+#pragma unroll
+            for (int r2 = 0; r2 < 2; ++r2) {
+              const int rl = m * 16 + (lane >> 4) * 4 + 2 * r2;   // even row within this member
+              const int nb = base + w + 4 * j;
+              const int unit = nb * 16 + (lane & 15);
+              if (rowbase + rl < rend && nb < NB)
+                ll_store(xo + (((int64_t)d * rpairs + (rowbase - a.b0 + rl) / 2) * NM + mem) * H + unit,
+                         pack_bf16x2(acc[m][j][2 * r2], acc[m][j][2 * r2 + 1]), fb | (uint32_t)(tau + 1));
+            }
+      }
+    }
+
+    // da in frame-major rows (DA, for dX): thread t copies 8 own gate rows
+    // (16 contiguous bytes of LDS and of DA) of one row
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      const int kg = tid & 15, r = m * 16 + (tid >> 4);
+      const int row = rowbase + r;
+      if (row < rend) {
+        const int kk = kg * 8;
+        const int64_t col = (int64_t)d * 4 * H + (int64_t)((kk >> 4) & 3) * H + u0 + (kk >> 6) * 16 + (kk & 15);
+        *(uint4*)(a.DA + ((int64_t)t * B + row) * 8 * H + col) = *(const uint4*)&al[(kg * (R + 1) + r) * 8];
+      }
+    }
     // the own da block (R rows x 128 gate rows, in LDS) also goes out
     // frame-contiguous (DAT) and as bias-gradient partial sums per 16-row
     // block (DBP): thread t takes gate row t/2 and 8 of the 16 rows of a block
@@ -596,61 +666,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
     }
 
-    // P = da_own [R x 128] * W_own [128 x H]; 16-unit block nb goes to wave nb % 4
-    if (tau + 1 < Tn) {
-      uint64_t* xo = a.X + (tau & 1) * slot_stride;
-      // the A fragments (own da, 4 k-steps) serve every unit block
-      bf16x8 af[MB][4];
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-        for (int m = 0; m < MB; ++m)
-          af[m][ks] = *(const bf16x8*)&al[((ks * 4 + (lane >> 4)) * (R + 1) + m * 16 + (lane & 15)) * 8];
-#pragma unroll
-      for (int bi = 0; bi < H_MAX_MEMBERS / 8; ++bi) {
-        const int base = bi * 16;
-        if (base >= NB) break;
-        f32x4 acc[MB][4];
-#pragma unroll
-        for (int m = 0; m < MB; ++m)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        // all B fragments of this pass first (registers, or one LDS round
-        // trip), then the products
-        bf16x8 bfr[4][4];
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int nb = base + w + 4 * j;
-            if constexpr (WREG)
-              bfr[ks][j] = bw[bi][ks][j];
-            else
-              bfr[ks][j] = nb < NB ? *(const bf16x8*)&wl[((ks * 4 + (lane >> 4)) * (H + 1) + nb * 16 + (lane & 15)) * 8]
-                                   : bf16x8{};
-          }
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-          for (int m = 0; m < MB; ++m)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc[m][j] = Mfma<bf16>::mma(af[m][ks], bfr[ks][j], acc[m][j]);
-        // publish: word (row pair, member, unit), the lane's rows 2r2, 2r2+1
-#pragma unroll
-        for (int m = 0; m < MB; ++m)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int r2 = 0; r2 < 2; ++r2) {
-              const int rl = m * 16 + (lane >> 4) * 4 + 2 * r2;   // even row within this member
-              const int nb = base + w + 4 * j;
-              const int unit = nb * 16 + (lane & 15);
-              if (rowbase + rl < rend && nb < NB)
-                ll_store(xo + (((int64_t)d * rpairs + (rowbase - a.b0 + rl) / 2) * NM + mem) * H + unit,
-                         pack_bf16x2(acc[m][j][2 * r2], acc[m][j][2 * r2 + 1]), fb | (uint32_t)(tau + 1));
-            }
-      }
-    }
   }
   if (a.DBP && (tid & 1) == 0) {
 #pragma unroll
