@@ -295,6 +295,11 @@ static inline void gemm_kc_launch(const char* name, hipStream_t s, const Opnd& A
 // rings): 128x128 blocks of 8 waves (64x32 each), two 64-deep stages, two
 // blocks per CU.
 typedef KcCfg<128, 128, 2, 4, 2> KcTile;
+// 192-row blocks (two per CU fill 160 KB of LDS): fewer, larger tiles for
+// products with more 128x128 tiles than one round of two blocks per CU
+// (the gate projection, 448 instead of 672 blocks, and the logits)
+typedef KcCfg<192, 128, 2, 4, 2> KcTileTall;
+static constexpr int64_t kc_round_blocks = 2 * 256;   // two blocks on each of 256 CUs
 
 // GEMM dispatch: bf16 operands with 16-byte aligned rows go to the
 // direct-to-LDS kernel, everything else to the generic kernel.
@@ -304,6 +309,12 @@ static inline void gemm_launch(const char* name, hipStream_t s, const Opnd& A, c
                                const Epi& epi) {
   if constexpr (std::is_same<T, bf16>::value) {
     if (K % 8 == 0 && kc_operand_ok(A, K, AKC) && kc_operand_ok(B, K, BKC)) {
+      if constexpr (AKC) {
+        if (M >= KcTileTall::BM && cdiv(M, 128) * cdiv(N, 128) * batches * splits > kc_round_blocks) {
+          gemm_kc_launch<KcTileTall, AKC, BKC>(name, s, A, B, M, N, K, batches, splits, epi);
+          return;
+        }
+      }
       gemm_kc_launch<KcTile, AKC, BKC>(name, s, A, B, M, N, K, batches, splits, epi);
       return;
     }

@@ -48,6 +48,11 @@ __device__ __forceinline__ void ll_store(uint64_t* p, uint32_t payload, uint32_t
   __hip_atomic_store(p, ((uint64_t)flag << 32) | payload, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// the value of lane l ^ 1 (a DPP quad permutation, no LDS round trip)
+__device__ __forceinline__ float lane_xor1(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+}
+
 // two bf16 values in one dword, `lo` in the low half
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)__builtin_bit_cast(uint16_t, (bf16)lo) |
@@ -311,12 +316,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
           creg[m][r] = c;
           hv[m][r] = gv[m][r][3] * tanhf_(c);
         }
+      // every row's h before the first publish (the empty asm pins the
+      // values here, so the compiler cannot sink their math past a publish)
+#pragma unroll
+      for (int m = 0; m < MBW; ++m)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) __asm__ volatile("" : "+v"(hv[m][r]));
 #pragma unroll
       for (int m = 0; m < MBW; ++m)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int row = rowbase + (mb0 + m) * 16 + (lane >> 4) * 4 + r;
-          const float h_next_unit = __shfl_xor(hv[m][r], 1);   // lanes of one row, units u and u^1
+          const float h_next_unit = lane_xor1(hv[m][r]);   // lanes of one row, units u and u^1
           if (row < rend && (lane & 1) == 0)
             ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 2, pack_bf16x2(hv[m][r], h_next_unit),
                      fb | (uint32_t)(tau + 1));
