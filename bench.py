@@ -307,6 +307,7 @@ def main():
             st.step(lr)
         torch.cuda.synchronize()
     dom = bd.blstm_timing_end()[dominant]
+    st.check_recurrence()   # raises if a persistent launch's exchange wait gave up
     loss = float(st.loss.cpu()[0])
 
     ms_per_step = elapsed * 1e3 / args.steps

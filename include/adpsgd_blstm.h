@@ -119,6 +119,17 @@ int blstm_bwd(const blstm_dims* dims, const float* theta, const void* theta_lp,
               void* act_ws, const void* y_top, const float* dy_top, float* grad,
               hipStream_t stream);
 
+/* Whether every recurrent exchange wait of the persistent kernels completed
+ * since the last blstm_fwd on act_ws (covering that call and the blstm_bwd
+ * after it).  The persistent kernels are plain launches when the occupancy
+ * query shows the whole grid resident at once; if other streams or
+ * processes occupy CUs, a wait gives up after its bound instead of hanging
+ * and the result of that call is not valid.  Returns BLSTM_OK, or
+ * BLSTM_EHIP with a message.  Synchronises `stream`; not during stream
+ * capture.  ADPSGD_BLSTM_COOPERATIVE=1 makes every persistent launch
+ * cooperative (guaranteed residency, about 15 us more per launch). */
+int blstm_recurrence_ok(const blstm_dims* dims, const void* act_ws, hipStream_t stream);
+
 /* Super-learner reduction (eq. 6): out = scale * sum_{r=0}^{R-1} grads[r],
  * summed left to right in float32.  grads is a HOST array of R device
  * pointers (1 <= R <= 16), each to n floats; out may equal grads[0]. */

@@ -22,7 +22,7 @@ BLSTM_EHIP = -3
 
 EXPORTED = ("blstm_param_count", "blstm_workspace_bytes", "blstm_pack_params", "blstm_fwd",
             "softmax_ce_fwd_bwd", "blstm_bwd", "replica_grad_reduce", "adpsgd_step",
-            "blstm_last_error", "blstm_timing_begin", "blstm_timing_end")
+            "blstm_recurrence_ok", "blstm_last_error", "blstm_timing_begin", "blstm_timing_end")
 
 
 class Dims(ctypes.Structure):
@@ -60,6 +60,7 @@ def lib():
         L.blstm_fwd.argtypes = [DP, P, P, P, P, P, P]
         L.softmax_ce_fwd_bwd.argtypes = [DP, P, P, P, P, ctypes.c_float, P, P, P, P, P]
         L.blstm_bwd.argtypes = [DP, P, P, P, P, P, P, P]
+        L.blstm_recurrence_ok.argtypes = [DP, P, P]
         L.replica_grad_reduce.argtypes = [ctypes.POINTER(P), ctypes.c_int32, ctypes.c_int64,
                                           ctypes.c_float, P, P]
         L.adpsgd_step.argtypes = [P, P, ctypes.POINTER(P), ctypes.c_int32, ctypes.c_float,
@@ -136,6 +137,11 @@ def blstm_bwd(dims, theta, theta_lp, act_ws, y_top, dy_top, grad, stream=None):
     return _check("blstm_bwd", lib().blstm_bwd(
         ctypes.byref(dims), _ptr(theta), _ptr(theta_lp), _ptr(act_ws), _ptr(y_top), _ptr(dy_top),
         _ptr(grad), _stream(stream)))
+
+
+def blstm_recurrence_ok(dims, act_ws, stream=None):
+    return _check("blstm_recurrence_ok", lib().blstm_recurrence_ok(ctypes.byref(dims), _ptr(act_ws),
+                                                                   _stream(stream)))
 
 
 def _ptr_array(tensors):

@@ -396,6 +396,8 @@ template <typename T>
 static int fwd_impl(const Layout& lo, const float* theta, const T* W, const float* x, char* ws,
                     T* ytop, hipStream_t s) {
   bool xch_cleared = false;   // exchange words cleared once per call (persist_clear)
+  // the recurrence status covers this forward call and the backward call after it
+  if (persist_status_clear((int*)(ws + lo.SYNC), s) != hipSuccess) return blstm_check_launch("blstm_fwd");
   constexpr int V = VecW<T>::v;
   const int64_t M = lo.M;
   const int H = lo.H, B = lo.B;
@@ -666,6 +668,23 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
   }
   if (side) (void)hipStreamWaitEvent(s, side->dw_done[0], 0);   // join before returning
   return blstm_check_launch("blstm_bwd");
+}
+
+extern "C" int blstm_recurrence_ok(const blstm_dims* dims, const void* act_ws, hipStream_t stream) {
+  Layout lo;
+  int rc = make_layout(dims, &lo);
+  if (rc) return rc;
+  if (!act_ws) return blstm_fail(BLSTM_EINVAL, "blstm_recurrence_ok: NULL act_ws");
+  int gave_up = 0;
+  if (hipMemcpyAsync(&gave_up, (const char*)act_ws + lo.SYNC, sizeof(int), hipMemcpyDeviceToHost, stream) !=
+          hipSuccess ||
+      hipStreamSynchronize(stream) != hipSuccess)
+    return blstm_fail(BLSTM_EHIP, "blstm_recurrence_ok: %s", hipGetErrorString(hipGetLastError()));
+  if (gave_up)
+    return blstm_fail(BLSTM_EHIP,
+                      "blstm_recurrence_ok: a recurrent exchange wait gave up (the workgroups of a persistent "
+                      "launch were not all resident; set ADPSGD_BLSTM_COOPERATIVE=1 on a shared device)");
+  return BLSTM_OK;
 }
 
 extern "C" int blstm_fwd(const blstm_dims* dims, const float* theta, const void* theta_lp,

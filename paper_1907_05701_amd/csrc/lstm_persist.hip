@@ -29,6 +29,7 @@
 // consumed the slot's current contents.  The buffer is cleared before each
 // launch, so no word from an earlier launch can carry a valid step number.
 // The launch is cooperative, so every member of a group is resident.
+#include <stdlib.h>
 #include <string.h>
 
 #include "common.hpp"
@@ -685,11 +686,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   }
 }
 
+// status: cleared too when non-null
 __global__ __launch_bounds__(256) void clear_exchange_kernel(uint4* p, int64_t n16, int* status) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
     p[i] = make_uint4(0u, 0u, 0u, 0u);
-  if (blockIdx.x == 0 && threadIdx.x == 0) *status = 0;
+  if (status && blockIdx.x == 0 && threadIdx.x == 0) *status = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -718,6 +720,21 @@ bool persist_supported(int H, int T) {
          persist_lds_bytes(H, true, 2) <= 160 * 1024;
 }
 
+// Launch mode.  Every workgroup of a launch waits for the others, so all
+// must be resident at once.  A cooperative launch guarantees that, at a
+// measured cost of about 15 us per launch on MI355X (12 launches per learner
+// step).  A plain launch is used instead when the occupancy query shows that
+// the whole grid fits on the device at once (one workgroup per CU here):
+// the stream's previous kernel has completed, so every CU is free unless
+// other streams or processes occupy some.  In that case the waits give up
+// after their bound, the kernel still ends, and the status word (see
+// blstm_recurrence_ok) reports it.  ADPSGD_BLSTM_COOPERATIVE=1 forces
+// cooperative launches (for devices shared with other work).
+static bool force_cooperative() {
+  const char* e = getenv("ADPSGD_BLSTM_COOPERATIVE");
+  return e && e[0] == '1';
+}
+
 template <int MB, bool BWD>
 static hipError_t launch_one(PersistArgs a, hipStream_t s) {
   const void* fn;
@@ -728,12 +745,24 @@ static hipError_t launch_one(PersistArgs a, hipStream_t s) {
   if (e != hipSuccess) return e;
   const dim3 grid(2 * a.NS * (a.H / PU)), block(256);
   void* args[] = {&a};
+  // the whole grid resident at once? (per device; the answer depends only
+  // on the kernel and its resources)
+  bool fits = false;
+  if (!force_cooperative()) {
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, lds) == hipSuccess)
+      fits = (int64_t)per_cu * persist_max_wg() >= (int64_t)grid.x;
+    else
+      (void)hipGetLastError();
+  }
   const char* name = BWD ? "lstm_rec_bwd_persist" : "lstm_rec_fwd_persist";
   const int slot = g_timing_on ? timing_pre(name, s) : -1;
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
   e = hipStreamIsCapturing(s, &cap);
   if (e != hipSuccess) return e;
-  if (cap == hipStreamCaptureStatusNone) {
+  if (fits) {
+    e = hipLaunchKernel(fn, grid, block, args, lds, s);
+  } else if (cap == hipStreamCaptureStatusNone) {
     e = hipLaunchCooperativeKernel(fn, grid, block, args, (unsigned)lds, s);
   } else {
     // recorded into a graph as a kernel node with the cooperative attribute
@@ -781,7 +810,12 @@ hipError_t persist_clear(bool backward, const PersistArgs& a, hipStream_t s) {
                                  : (int64_t)2 * 2 * chunk * (a.H / 2);
   const int64_t n16 = words / 2;
   hipLaunchKernelGGL(clear_exchange_kernel, dim3((unsigned)std::min<int64_t>(cdiv(n16, 256), 2048)), dim3(256), 0,
-                     s, (uint4*)a.X, n16, a.status);
+                     s, (uint4*)a.X, n16, nullptr);
+  return hipGetLastError();
+}
+
+hipError_t persist_status_clear(int* status, hipStream_t s) {
+  hipLaunchKernelGGL(clear_exchange_kernel, dim3(1), dim3(64), 0, s, (uint4*)nullptr, (int64_t)0, status);
   return hipGetLastError();
 }
 

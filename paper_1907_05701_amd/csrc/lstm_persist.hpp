@@ -17,7 +17,7 @@ struct PersistArgs {
   bf16* DAT;          // backward, optional: da also frame-contiguous [8H][M] (needs B % 8 == 0)
   float* DBP;         // backward, optional: sums of da over 16-row blocks and all steps [cdiv(B,16)][8H]
   int64_t M;          // frames, T*B (DAT row length)
-  int* status;        // cleared by persist_clear; 1 if a poll ever gave up
+  int* status;        // cleared by the forward pass's persist_clear; 1 if a wait ever gave up
   uint32_t tag;       // caller: layer index; step numbers carry it (exchange words of
                       // earlier layers of the same call never match)
   int Tn, B, H;
@@ -41,9 +41,11 @@ static inline size_t persist_xch_bytes(int B, int H) {
 // True if the persistent kernels can hold a W_hh slice for this H in LDS
 // (and T fits the 8-bit step numbers).
 bool persist_supported(int H, int T);
-// Clears the exchange words and the status word; once per forward or
-// backward call, before its first persist_layer.
+// Clears the exchange words; once per forward or backward call, before its
+// first persist_layer.
 hipError_t persist_clear(bool backward, const PersistArgs& a, hipStream_t s);
+// Clears the status word (once per forward call, whatever path it takes).
+hipError_t persist_status_clear(int* status, hipStream_t s);
 // Runs every step of one layer, both directions; hipSuccess or the error of
-// the cooperative launch that failed.  Layers of one call need distinct tags.
+// the launch that failed.  Layers of one call need distinct tags.
 hipError_t persist_layer(bool backward, PersistArgs a, hipStream_t s);

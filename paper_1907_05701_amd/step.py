@@ -71,6 +71,11 @@ class LearnerStep:
         self.head()
         self.backward()
 
+    def check_recurrence(self):
+        """Raises if a recurrent exchange wait gave up since the last forward
+        call (synchronises the current stream)."""
+        bd.blstm_recurrence_ok(self.dims, self.act_ws)
+
     def update(self, lr, flags=0, grads=None, scale=1.0):
         bd.adpsgd_step(self.theta, self.peer, [self.grad] if grads is None else grads, scale, lr,
                        flags, self.theta_lp)

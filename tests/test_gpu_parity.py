@@ -58,6 +58,7 @@ def run_step_and_compare(shape, precision, tol, dist="uniform", seed=0, check_up
     st.load(theta, x, lab, peer)
     st.gradient()
     torch.cuda.synchronize()
+    st.check_recurrence()
     want = ref.learner_gradient(theta, dims, x, lab)
     loss = float(st.loss.cpu()[0])
     errs = {"loss": abs(loss - want["loss"]) / abs(want["loss"]),
@@ -144,6 +145,7 @@ def run_replicated_and_compare(shape, reps, tol, seed=11):
     st.load(theta, xb, lb, inputs.peer(theta, seed=seed + 3))
     st.gradient()
     torch.cuda.synchronize()
+    st.check_recurrence()
     want = ref.learner_gradient(theta, dims, x, lab)
     loss = float(st.loss.cpu()[0])
     y = st.y_top.float().cpu().numpy().reshape(T, reps, B0, -1)
@@ -174,6 +176,29 @@ def test_recurrence_batch_regimes_bf16(gpu_lib, B):
     row blocks, and (B=1100) that the batch is processed in two chunks."""
     run_step_and_compare(dict(L=1, D=40, H=512, P=32, K=50, T=3, B=B), "bf16", BF16_TOL, seed=11,
                          check_update=False)
+
+
+def test_cooperative_and_plain_persistent_launches_agree(gpu_lib, monkeypatch):
+    """The persistent kernels as plain launches (default when the grid fits)
+    and as cooperative launches give bit-identical results; both report
+    that every exchange wait completed."""
+    from paper_1907_05701_amd.step import LearnerStep
+    shape = dict(L=2, D=260, H=512, P=256, K=1000, T=21, B=128)
+    dims = ref.Dims(**shape)
+    theta = inputs.params(ref.param_count(dims), seed=31)
+    x = inputs.features(dims.T, dims.B, dims.D, seed=32)
+    lab = inputs.labels(dims.T, dims.B, dims.K, seed=33, dist="zipf")
+    grads = []
+    for coop in ("0", "1"):
+        monkeypatch.setenv("ADPSGD_BLSTM_COOPERATIVE", coop)
+        say(f"[launch] cooperative={coop}")
+        st = LearnerStep(**shape, precision="bf16")
+        st.load(theta, x, lab, inputs.peer(theta))
+        st.gradient()
+        torch.cuda.synchronize()
+        st.check_recurrence()
+        grads.append(st.grad.cpu().numpy())
+    np.testing.assert_array_equal(grads[0].view(np.uint32), grads[1].view(np.uint32))
 
 
 def test_per_step_recurrence_path_bf16(gpu_lib, monkeypatch):
