@@ -35,10 +35,13 @@ extern "C" const char* blstm_last_error(void) { return g_err; }
 // split, below 256 tiles.  bf16 (direct-to-LDS kernel) aims at 256
 // workgroups (measured: more splits cost more in the partial reduction than
 // they gain), float32 at 512.
-int plan_splits(int64_t Mo, int64_t No, int64_t Kr, int BMt, int BNt, int BK, int batches, bool lp) {
+int plan_splits(int64_t Mo, int64_t No, int64_t Kr, int BMt, int BNt, int BK, int batches, bool lp, bool alone) {
   const int64_t tiles = cdiv(Mo, BMt) * cdiv(No, BNt) * batches;
   if (tiles >= 256) return 1;
-  int64_t s = cdiv(lp ? 256 : 512, tiles);
+  // a product launched alone (bf16) fills one round of two blocks per CU
+  // without starting a second; the backward layer products share a grouped
+  // launch and split to half a round each
+  int64_t s = lp && alone ? std::max<int64_t>(512 / tiles, 1) : cdiv(lp ? 256 : 512, tiles);
   const int64_t kt = cdiv(Kr, BK);
   s = std::min<int64_t>(s, std::max<int64_t>(kt / 4, 1));
   s = std::min<int64_t>(s, 16);
@@ -123,13 +126,13 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   // each layer's three products own disjoint partial regions (dW_ih, dW_hh,
   // dX), so that they can run as one grouped launch
   size_t skp = 0;
-  L.sp_dWhh = plan_splits(4 * H, H, (int64_t)(d->T - 1) * d->B, BMt, BNt, BKt, 2, es == 2);
+  L.sp_dWhh = plan_splits(4 * H, H, (int64_t)(d->T - 1) * d->B, BMt, BNt, BKt, 2, es == 2, false);
   const size_t hh_bytes = L.sp_dWhh > 1 ? align256((size_t)L.sp_dWhh * 2 * 4 * H * H * 4) : 0;
   for (int l = 0; l < d->L; ++l) {
     const int64_t Dl = l == 0 ? d->D : 2 * H;
-    L.sp_dWih[l] = plan_splits(4 * H, Dl, M, BMt, BNt, BKt, 2, es == 2);
+    L.sp_dWih[l] = plan_splits(4 * H, Dl, M, BMt, BNt, BKt, 2, es == 2, false);
     const size_t ih_bytes = L.sp_dWih[l] > 1 ? align256((size_t)L.sp_dWih[l] * 2 * 4 * H * Dl * 4) : 0;
-    L.sp_dX[l] = l > 0 ? plan_splits(M, Dl, 8 * H, BMt, BNt, BKt, 1, es == 2) : 1;
+    L.sp_dX[l] = l > 0 ? plan_splits(M, Dl, 8 * H, BMt, BNt, BKt, 1, es == 2, false) : 1;
     const size_t dx_bytes = L.sp_dX[l] > 1 ? align256((size_t)L.sp_dX[l] * M * Dl * 4) : 0;
     L.skp_hh[l] = ih_bytes;
     L.skp_dx[l] = ih_bytes + hh_bytes;
@@ -151,13 +154,13 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   L.DZT = h; h = align256(h + (size_t)M * P * es);
   L.HCSP = h; h = align256(h + (size_t)COLSUM_MAX_CHUNKS * std::max<int64_t>(L.Kp, P) * 4);
   size_t hsk = 0;
-  L.sp_dz = plan_splits(M, P, d->K, BMt, BNt, BKt, 1, es == 2);
+  L.sp_dz = plan_splits(M, P, d->K, BMt, BNt, BKt, 1, es == 2, true);
   hsk = std::max(hsk, (size_t)L.sp_dz * M * P * 4);  // dz always goes through partials
-  L.sp_dWs = plan_splits(d->K, P, M, BMt, BNt, BKt, 1, es == 2);
+  L.sp_dWs = plan_splits(d->K, P, M, BMt, BNt, BKt, 1, es == 2, true);
   if (L.sp_dWs > 1) hsk = std::max(hsk, (size_t)L.sp_dWs * d->K * P * 4);
-  L.sp_dWl = plan_splits(P, 2 * H, M, BMt, BNt, BKt, 1, es == 2);
+  L.sp_dWl = plan_splits(P, 2 * H, M, BMt, BNt, BKt, 1, es == 2, true);
   if (L.sp_dWl > 1) hsk = std::max(hsk, (size_t)L.sp_dWl * P * 2 * H * 4);
-  L.sp_dy = plan_splits(M, 2 * H, P, BMt, BNt, BKt, 1, es == 2);
+  L.sp_dy = plan_splits(M, 2 * H, P, BMt, BNt, BKt, 1, es == 2, true);
   if (L.sp_dy > 1) hsk = std::max(hsk, (size_t)L.sp_dy * M * 2 * H * 4);
   L.HSKP = h; h = align256(h + hsk);
   L.head_xposed = es == 2 && d->K % 8 == 0;

@@ -100,7 +100,7 @@ int make_layout(const blstm_dims* d, Layout* lo);
 
 // Split-K factor for an output of Mo x No tiles of BMt x BNt with a reduction
 // of Kr over BK-deep tiles: 1 when the grid already fills the chip.
-int plan_splits(int64_t Mo, int64_t No, int64_t Kr, int BMt, int BNt, int BK, int batches, bool lp);
+int plan_splits(int64_t Mo, int64_t No, int64_t Kr, int BMt, int BNt, int BK, int batches, bool lp, bool alone);
 
 // Error reporting (thread-local message).
 int blstm_fail(int code, const char* fmt, ...);

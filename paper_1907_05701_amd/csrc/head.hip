@@ -72,13 +72,16 @@ __global__ __launch_bounds__(256) void softmax_ce_rows_kernel(T* __restrict__ S,
   }
 }
 
-// Single-pass variant for rows of up to 256*8*NV classes: each thread keeps
-// its NV 8-element vectors of the row in registers, so the logits are read
-// once and ds written once.
+// Single-pass variant for rows of up to SM_TPB*8*NV classes: each thread
+// keeps its NV 8-element vectors of the row in registers, so the logits are
+// read once and ds written once.  512 threads per row (eight waves, 64
+// values each at 32000 classes) measured 25% faster on MI355X than 256
+// threads with twice the registers, and than 1024.
+#define SM_TPB 512
 template <typename T, int NV>
-__global__ __launch_bounds__(256) void softmax_ce_rows_reg_kernel(T* __restrict__ S, int K, int Kp,
-                                                                  const int32_t* __restrict__ labels,
-                                                                  float scale, float* __restrict__ rowloss) {
+__global__ __launch_bounds__(SM_TPB) void softmax_ce_rows_reg_kernel(T* __restrict__ S, int K, int Kp,
+                                                                     const int32_t* __restrict__ labels,
+                                                                     float scale, float* __restrict__ rowloss) {
   // One pass over the row: each thread keeps its logits' exponentials
   // e = exp(s - m_t) against its own maximum m_t and their sum; the
   // (maximum, sum) pairs are combined across the workgroup (one barrier), and
@@ -94,7 +97,7 @@ __global__ __launch_bounds__(256) void softmax_ce_rows_reg_kernel(T* __restrict_
   bool have_lab = false;
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
-    const int c = tid + 256 * i;
+    const int c = tid + SM_TPB * i;
     if (c < nvec) {
       const uint4 raw = *(const uint4*)(s + (int64_t)c * 8);
       const T* e = (const T*)&raw;
@@ -118,7 +121,7 @@ __global__ __launch_bounds__(256) void softmax_ce_rows_reg_kernel(T* __restrict_
       v[i][j] = __expf(v[i][j] - mref);   // exp(-inf) = 0 for padding
       st += v[i][j];
     }
-  // combine (max, sum) pairs: within the wave by shuffles, then the 4 waves
+  // combine (max, sum) pairs: within the wave by shuffles, then the waves
   float mw = mt, sw = st;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
@@ -127,13 +130,16 @@ __global__ __launch_bounds__(256) void softmax_ce_rows_reg_kernel(T* __restrict_
     sw = (mw == -INFINITY ? 0.f : sw * __expf(mw - mn)) + (mo == -INFINITY ? 0.f : so * __expf(mo - mn));
     mw = mn;
   }
-  __shared__ float rm[4], rs[4];
+  constexpr int NW = SM_TPB / 64;
+  __shared__ float rm[NW], rs[NW];
   if (lane == 0) { rm[wid] = mw; rs[wid] = sw; }
   __syncthreads();
-  const float mx = fmaxf(fmaxf(rm[0], rm[1]), fmaxf(rm[2], rm[3]));
+  float mx = -INFINITY;
+#pragma unroll
+  for (int q = 0; q < NW; ++q) mx = fmaxf(mx, rm[q]);
   float sum = 0.f;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) sum += rm[q] == -INFINITY ? 0.f : rs[q] * __expf(rm[q] - mx);
+  for (int q = 0; q < NW; ++q) sum += rm[q] == -INFINITY ? 0.f : rs[q] * __expf(rm[q] - mx);
   const float lse = mx + __logf(sum);
   if (have_lab) rowloss[m] = lse - slab;
   // an out-of-range label is not read (the loss becomes NaN instead)
@@ -141,7 +147,7 @@ __global__ __launch_bounds__(256) void softmax_ce_rows_reg_kernel(T* __restrict_
   const float f = scale * __expf(mref - mx) / sum;
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
-    const int c = tid + 256 * i;
+    const int c = tid + SM_TPB * i;
     if (c >= nvec) continue;
     uint4 out;
     T* e = (T*)&out;
@@ -196,17 +202,19 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
   // per-frame loss and ds (in place)
   {
     // ds in place; rows of up to 32768 classes stay in registers (bf16, 16 B vectors)
-    const int nv = (int)cdiv(Kp / 8, 256);
-    const dim3 g((unsigned)M), b(256);
-    if (std::is_same<T, bf16>::value && nv <= 16) {
+    const int nv = (int)cdiv(Kp / 8, SM_TPB);
+    const dim3 g((unsigned)M), b(SM_TPB), b256(256);
+    if (std::is_same<T, bf16>::value && nv <= 8) {
       if (nv <= 1)
         BLSTM_LAUNCH("softmax_ce_rows", (softmax_ce_rows_reg_kernel<bf16, 1>), g, b, 0, s, (bf16*)S, K, Kp, labels, scale, RL);
+      else if (nv <= 2)
+        BLSTM_LAUNCH("softmax_ce_rows", (softmax_ce_rows_reg_kernel<bf16, 2>), g, b, 0, s, (bf16*)S, K, Kp, labels, scale, RL);
       else if (nv <= 4)
         BLSTM_LAUNCH("softmax_ce_rows", (softmax_ce_rows_reg_kernel<bf16, 4>), g, b, 0, s, (bf16*)S, K, Kp, labels, scale, RL);
       else
-        BLSTM_LAUNCH("softmax_ce_rows", (softmax_ce_rows_reg_kernel<bf16, 16>), g, b, 0, s, (bf16*)S, K, Kp, labels, scale, RL);
+        BLSTM_LAUNCH("softmax_ce_rows", (softmax_ce_rows_reg_kernel<bf16, 8>), g, b, 0, s, (bf16*)S, K, Kp, labels, scale, RL);
     } else {
-      BLSTM_LAUNCH("softmax_ce_rows", softmax_ce_rows_kernel<T>, g, b, 0, s, S, K, Kp, labels, scale, RL);
+      BLSTM_LAUNCH("softmax_ce_rows", softmax_ce_rows_kernel<T>, g, b256, 0, s, S, K, Kp, labels, scale, RL);
     }
   }
   BLSTM_LAUNCH("loss_sum", loss_sum_kernel, dim3(1), dim3(256), 0, s, RL, M, scale, loss);
