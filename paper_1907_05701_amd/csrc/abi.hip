@@ -163,9 +163,6 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   L.sp_dy = plan_splits(M, 2 * H, P, BMt, BNt, BKt, 1, es == 2, true);
   if (L.sp_dy > 1) hsk = std::max(hsk, (size_t)L.sp_dy * M * 2 * H * 4);
   L.HSKP = h; h = align256(h + hsk);
-  L.head_xposed = es == 2 && d->K % 8 == 0;
-  L.WST = h; h = align256(h + (L.head_xposed ? (size_t)P * d->K * es : 0));
-  L.WLT = h; h = align256(h + (L.head_xposed ? (size_t)2 * H * P * es : 0));
   L.head_bytes = h;
   L.ytop_bytes = (size_t)M * 2 * H * es;
   return BLSTM_OK;

@@ -84,8 +84,7 @@ struct Layout {
   bool xpose_act;     // bf16 with B % 8 == 0: weight gradients from transposed activations
   size_t act_bytes;
   // head_ws byte offsets
-  size_t Z, S, RL, DZ, DZT, HCSP, HSKP, WST, WLT;
-  bool head_xposed;   // bf16 with K % 8 == 0: dz and dy use transposed weight copies
+  size_t Z, S, RL, DZ, DZT, HCSP, HSKP;
   size_t head_bytes;
   size_t ytop_bytes;
   // split-K factors of the weight/input-gradient GEMMs (1 = direct store)

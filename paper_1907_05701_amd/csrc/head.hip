@@ -13,7 +13,6 @@
 #include <type_traits>
 
 #include "common.hpp"
-#include "xpose.hpp"
 #include "gemm_kc.hpp"
 #include "reduce.hpp"
 
@@ -224,35 +223,20 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
   gemm_f32<T, false, false, V, V>("gemm_dws", s, opnd(S, Kp, Kp, M), opnd(Z, P, P, M), K, P, M, 1,
                                   lo.sp_dWs, grad + lo.Ws, P, 0, part);
   // bf16: W_s^T and W_l^T copies make dz and dy K-contiguous products
-  T* WST = (T*)(hws + lo.WST);
-  T* WLT = (T*)(hws + lo.WLT);
-  if constexpr (std::is_same<T, bf16>::value) {
-    if (lo.head_xposed) {
-      XposeJobs jobs;
-      jobs.j[0] = XposeJob{W + lo.Ws, WST, P, K, K, P};
-      jobs.j[1] = XposeJob{W + lo.Wl, WLT, H2, P, P, H2};
-      transpose_bf16("transpose_head", s, jobs, 2);
-    }
-  }
-  // dz = ds W_s (float32 and a low-precision copy for the next products)
-  if (lo.head_xposed)
-    gemm_f32<T, true, true, V, V>("gemm_dz", s, opnd(S, Kp, Kp, M), opnd(WST, K, K, P), M, P, K, 1,
-                                  lo.sp_dz, DZ, P, 0, part, DZT, P);
-  else
-    gemm_f32<T, true, false, V, V>("gemm_dz", s, opnd(S, Kp, Kp, M), opnd(W + lo.Ws, P, P, K), M, P,
-                                   K, 1, lo.sp_dz, DZ, P, 0, part, DZT, P);
+  // dz = ds W_s (float32 and a low-precision copy for the next products);
+  // W_s [K][P] is the MN-contiguous operand as it lies (the direct-to-LDS
+  // kernel reads it with transposing LDS reads; measured faster than
+  // transposing W_s each step first)
+  gemm_f32<T, true, false, V, V>("gemm_dz", s, opnd(S, Kp, Kp, M), opnd(W + lo.Ws, P, P, K), M, P,
+                                 K, 1, lo.sp_dz, DZ, P, 0, part, DZT, P);
   // db_l = sum over frames of dz
   colsum<float>("colsum_dbl", s, DZ, M, P, P, csp, P, 0, grad + lo.bl, nullptr);
   // dW_l = dz^T y
   gemm_f32<T, false, false, V, V>("gemm_dwl", s, opnd(DZT, P, P, M), opnd(ytop, H2, H2, M), P, H2, M,
                                   1, lo.sp_dWl, grad + lo.Wl, H2, 0, part);
-  // dy = dz W_l
-  if (lo.head_xposed)
-    gemm_f32<T, true, true, V, V>("gemm_dy", s, opnd(DZT, P, P, M), opnd(WLT, P, P, H2), M, H2, P, 1,
-                                  lo.sp_dy, dytop, H2, 0, part);
-  else
-    gemm_f32<T, true, false, V, V>("gemm_dy", s, opnd(DZT, P, P, M), opnd(W + lo.Wl, H2, H2, P), M,
-                                   H2, P, 1, lo.sp_dy, dytop, H2, 0, part);
+  // dy = dz W_l (W_l [P][2H] MN-contiguous as it lies)
+  gemm_f32<T, true, false, V, V>("gemm_dy", s, opnd(DZT, P, P, M), opnd(W + lo.Wl, H2, H2, P), M,
+                                 H2, P, 1, lo.sp_dy, dytop, H2, 0, part);
   return blstm_check_launch("softmax_ce_fwd_bwd");
 }
 
