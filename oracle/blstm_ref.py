@@ -382,3 +382,49 @@ def lr_schedule(epoch, base_lr, base_batch, batch, warmup_epochs=10):
     if epoch <= warmup_epochs:
         return target * epoch / warmup_epochs
     return target * math.sqrt(0.5) ** (epoch - warmup_epochs)
+
+
+# --------------------------------------------------------------------------
+# The ring of learners (Section 2, eq. 7; Section 4): several learners'
+# columns of Theta, each super-learner's gradient the mean of its replicas.
+# --------------------------------------------------------------------------
+
+def ring_partner(s, k, n):
+    """The neighbour learner s averages with in round k of an n-learner ring:
+    T_k pairs every learner with one ring neighbour, the right one when
+    s + k is even and the left one otherwise, so that consecutive rounds
+    alternate between the two neighbours and every round is a perfect
+    matching (n must be even)."""
+    if n < 2 or n % 2:
+        raise ValueError("the ring pairing needs an even number of learners")
+    return (s + 1) % n if (s + k) % 2 == 0 else (s - 1) % n
+
+
+def ring_matrix(k, n):
+    """T_k of eq. 7 for round k: 0.5 on the diagonal and at each learner's
+    partner (symmetric, rows and columns summing to 1)."""
+    T = np.zeros((n, n))
+    for s in range(n):
+        T[s, s] += 0.5
+        T[ring_partner(s, k, n), s] += 0.5
+    return T
+
+
+def ring_round(thetas, grads, lr, k, peers=None):
+    """One round of eq. 7 for n learners: Theta_{k+1} = W T_k - lr * G, where
+    column s of G is learner s's gradient and W holds the weights the
+    averaging reads: the round-start weights themselves (peers=None), or an
+    earlier round's weights (a learner reading stale peer copies, as in the
+    asynchronous variant).  The learner's own column of W is its current
+    weight vector in either case.  Returns the list of new weight vectors.
+
+    With super-learners (Section 4), grads[s] is already the mean of the
+    replica gradients (replica_grad_reduce with scale 1/N, eq. 6)."""
+    n = len(thetas)
+    cur = [np.asarray(t, dtype=np.float64) for t in thetas]
+    src = cur if peers is None else [np.asarray(t, dtype=np.float64) for t in peers]
+    out = []
+    for s in range(n):
+        p = ring_partner(s, k, n)
+        out.append(0.5 * cur[s] + 0.5 * src[p] - lr * np.asarray(grads[s], dtype=np.float64))
+    return out
