@@ -221,6 +221,42 @@ def bench_update(args, cfg):
     print(json.dumps(out), flush=True)
 
 
+def bench_ring(args, cfg):
+    """S super-learners of N replicas in the ring of eq. 7 on one GPU: a
+    round is S*N learner gradients and S updates (each learner's update
+    overlapped with the next learner's gradients).  value = all learners'
+    frames per second."""
+    import torch
+    from paper_1907_05701_amd import inputs
+    from paper_1907_05701_amd.ring import LearnerRing
+    shape = {k: cfg[k] for k in "LDHPKTB"}
+    S, N, lr = cfg["S"], cfg["N"], cfg["lr"]
+    ring = LearnerRing(shape, S, N, precision=cfg["precision"])
+    n = ring.steps[0][0].n
+    thetas = [inputs.params(n, seed=s) for s in range(S)]
+    batches = [[(inputs.features(cfg["T"], cfg["B"], cfg["D"], seed=100 + 10 * s + r),
+                 inputs.labels(cfg["T"], cfg["B"], cfg["K"], seed=200 + 10 * s + r, dist=cfg["label_dist"]))
+                for r in range(N)] for s in range(S)]
+    ring.load(thetas, batches)
+    for _ in range(args.warmup):
+        ring.round(lr)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        ring.round(lr)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    ring.check_recurrence()
+    value = ring.frames_per_round * args.steps / el
+    out = {"metric": "ring of learners (eq. 7): training frames/s of all learners on one GPU",
+           "value": round(value, 1), "unit": "frames/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(el * 1e3 / args.steps, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": cfg["precision"], "data": "synthetic",
+           "config": {"workload": args.workload, **shape, "super_learners": S, "replicas": N,
+                      "frames_per_round": ring.frames_per_round, "mode": "eager"}}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -250,6 +286,9 @@ def main():
     cfg = dict(inputs.CONFIGS[args.workload])
     if "R" in cfg:
         bench_update(args, cfg)
+        return
+    if "S" in cfg:
+        bench_ring(args, cfg)
         return
     shape = {k: cfg[k] for k in "LDHPKTB"}
     st = LearnerStep(**shape, precision=cfg["precision"])

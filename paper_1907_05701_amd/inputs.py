@@ -100,4 +100,7 @@ CONFIGS = {
                       label_dist="zipf", lr=0.05, R=8),
     "stress_t64_b1024": dict(L=6, D=260, H=512, P=256, K=32000, T=64, B=1024, precision="bf16",
                              label_dist="zipf", lr=0.05),
+    # two super-learners of two replicas each in the ring of eq. 7
+    "ring_s2_n2": dict(L=6, D=260, H=512, P=256, K=32000, T=21, B=128, precision="bf16",
+                       label_dist="zipf", lr=0.05, S=2, N=2),
 }
