@@ -112,3 +112,14 @@ def test_fp32_reduce_order_is_left_to_right():
     out = ref.replica_grad_reduce_fp32([a, b, c], 1.0)
     assert out[0] == np.float32(1.0)                    # each tiny add rounds away
     assert (a + (b + c))[0] == np.float32(1.0 + 2.0**-23)
+
+
+def test_training_loop_rate_matches_the_oracle_recipe():
+    """The training loop's learning-rate function against the oracle's
+    recipe (itself pinned to Section 3's worked example above), over the
+    warm-up, the annealing and other batch ratios."""
+    from paper_1907_05701_amd import train
+    for base_lr, base_batch, batch, warm in ((0.1, 256, 2560, 10), (0.05, 128, 512, 10), (1.0, 8, 8, 3)):
+        for e in range(1, 20):
+            want = ref.lr_schedule(e, base_lr, base_batch, batch, warm)
+            assert abs(train.lr_schedule(e, base_lr, base_batch, batch, warm) - want) <= 1e-15 * max(1.0, want)
