@@ -105,16 +105,11 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   L.DYb = a; a = align256(a + (size_t)M * 2 * H * 4);
   L.DC = a; a = align256(a + (size_t)2 * d->B * H * 4);
   L.WT = a; a = align256(a + (size_t)2 * d->L * 4 * H * H * es);
-  // bf16: W_ih^T of layers 1.. (both directions side by side) for dX
-  L.WIT = a; a = align256(a + (es == 2 ? (size_t)(d->L - 1) * 2 * H * 8 * H * es : 0));
-  // bf16: K-contiguous (transposed) layer inputs/outputs for the weight gradients
-  L.xpose_act = es == 2 && d->B % 8 == 0;
-  for (int i = 0; i < 2; ++i) {
-    L.YT[i] = a;
-    a = align256(a + (L.xpose_act ? (size_t)std::max<int64_t>(2 * H, L.Dp0) * M * es : 0));
-  }
+  // bf16 with B % 8 == 0: the BPTT kernels also write da frame-contiguous
+  // (da^T), the A operand of the weight gradients
+  L.write_dat = es == 2 && d->B % 8 == 0;
   // da^T [8H][M] and per-step bias partials, two of each (alternating layers)
-  L.dat_bytes = align256(L.xpose_act ? (size_t)M * 8 * H * es : 0);
+  L.dat_bytes = align256(L.write_dat ? (size_t)M * 8 * H * es : 0);
   L.DAT = a; a += 2 * L.dat_bytes;
   L.dbp_bytes = align256((size_t)d->T * cdiv(d->B, 16) * 8 * H * 4);
   L.DBP = a; a += 2 * L.dbp_bytes;

@@ -79,9 +79,9 @@ struct Layout {
   int64_t Wih[MAX_LAYERS][2], Whh[MAX_LAYERS][2], bih[MAX_LAYERS][2], bhh[MAX_LAYERS][2];
   int64_t Wl, bl, Ws, bs;
   // act_ws byte offsets
-  size_t X0, Y[MAX_LAYERS], G[MAX_LAYERS], C[MAX_LAYERS], GX, DYa, DYb, DC, WT, WIT, YT[2], DAT, DBP, CSP, SKP, SKP2, SYNC, XCH;
+  size_t X0, Y[MAX_LAYERS], G[MAX_LAYERS], C[MAX_LAYERS], GX, DYa, DYb, DC, WT, DAT, DBP, CSP, SKP, SKP2, SYNC, XCH;
   size_t dat_bytes, dbp_bytes;   // one of the two alternating da^T / bias-partial buffers
-  bool xpose_act;     // bf16 with B % 8 == 0: weight gradients from transposed activations
+  bool write_dat;     // bf16 with B % 8 == 0: BPTT also writes da^T [8H][M] for the weight gradients
   size_t act_bytes;
   // head_ws byte offsets
   size_t Z, S, RL, DZ, DZT, HCSP, HSKP;

@@ -1,5 +1,6 @@
-// bf16 GEMM with both operands K-contiguous (C[m][n] = sum_k A[m][k] B[n][k]),
-// the layout every product of the learner step is brought into.
+// bf16 GEMM C[m][n] = sum_k A(m, k) B(n, k) with each operand K-contiguous
+// (element (mn, k) at mn*ld + k) or MN-contiguous (at k*ld + mn), so that the
+// learner step's products read their operands as they lie.
 //
 // Global -> LDS moves use gfx950's direct-to-LDS buffer loads
 // (buffer_load_dwordx4 ... lds): each lane's 16 bytes land in LDS at the
@@ -19,7 +20,9 @@
 // 16-lane group, lane r points at 4 consecutive mn of k row r/4 and the
 // instruction hands lane i the 4 values of mn column i over those 4 k rows
 // (lane i, element j = lane 4j + i/4's element i%4).  Two such reads give a
-// lane its 8 consecutive k.
+// lane its 8 consecutive k.  Such an operand may also come in k segments (a
+// power of two of rows, whole k-tiles, at a fixed stride): the two direction
+// blocks of W_ih.
 //
 // Per k-tile each workgroup waits for its own oldest tile (vmcnt), meets at
 // one barrier (which also retires the previous tile's LDS reads), refills the
@@ -32,8 +35,12 @@
 struct KcArgs {
   const bf16* A;
   int64_t lda, azs, arows;   // A rows m (< arows valid), batch stride azs
+  int asegsh;                // MN-contiguous A: k rows in segments of 2^asegsh (0: one segment) ...
+  int64_t asegs;             // ... whose starts are asegs elements apart
   const bf16* B;
   int64_t ldb, bzs, brows;
+  int bsegsh;
+  int64_t bsegs;
   int64_t M, N, K, ksplit;   // k range of split s: [s*ksplit, min(K, (s+1)*ksplit))
   int splits, ntm, ntn;      // tiles along m and n
   int gm;                    // tile rows per group of the XCD-aware order
@@ -92,6 +99,26 @@ __device__ __forceinline__ void kc_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Transposing LDS read (ds_read_b64_tr_b16) as inline asm.  The compiler's
+// own form of this read is made to wait for every direct-to-LDS load in
+// flight (vmcnt(0)), since it cannot tell which LDS bytes they write; here
+// that wait would take the next k-tile's loads out of the overlap.  The loop
+// already orders the reads after the current tile's loads (its own vmcnt wait
+// and the barrier); kc_lds_wait() gives the results back to the compiler.
+__device__ __forceinline__ bf16x4 kc_read_tr(const char* p) {
+  const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+  bf16x4 v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(a));
+  return v;
+}
+
+template <int N>
+__device__ __forceinline__ void kc_lds_wait(bf16x8 (&f)[N]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(f[i]));
+}
+
 // Staging and fragment reads of one operand (rows BMN of the tile's M or N
 // side, BK deep), K-contiguous (KC) or MN-contiguous.
 template <bool KC, int BMN, int BK, int NW>
@@ -104,9 +131,12 @@ struct KcOperand {
   static_assert(KC || BMN == 128, "MN-contiguous tiles are 128 wide");
 
   // base: the operand's batch base; mn0: tile's first MN row; ld: row pitch;
-  // mnrows: valid MN rows of this tile (KC) / MN extent left (MNC)
-  __device__ __forceinline__ static void issue(const bf16* base, int64_t ld, int64_t mn0, int64_t mnrows, int64_t k0,
-                                               int64_t kend, char* tile, int wid, int lane) {
+  // mnrows: valid MN rows of this tile (KC) / MN extent left (MNC); segsh,
+  // segs: k rows of an MNC operand in segments of 2^segsh rows (at least BK,
+  // so no k-tile straddles two) whose starts are segs apart, or segsh = 0
+  __device__ __forceinline__ static void issue(const bf16* base, int64_t ld, int segsh, int64_t segs, int64_t mn0,
+                                               int64_t mnrows, int64_t k0, int64_t kend, char* tile, int wid,
+                                               int lane) {
     if constexpr (KC) {
       const __amdgpu_buffer_rsrc_t r = dma_rsrc(base + mn0 * ld);
       const int lr = lane / CPR, ls = lane % CPR;
@@ -120,7 +150,8 @@ struct KcOperand {
       }
     } else {
       // per-k-tile base keeps the offsets small for long operands
-      const __amdgpu_buffer_rsrc_t r = dma_rsrc(base + k0 * ld + mn0);
+      const int64_t kb = segsh ? (k0 >> segsh) * segs + (k0 & ((1LL << segsh) - 1)) * ld : k0 * ld;
+      const __amdgpu_buffer_rsrc_t r = dma_rsrc(base + kb + mn0);
       const int lr = lane / CPR, ls = lane % CPR;
 #pragma unroll
       for (int q = 0; q < LOADS; ++q) {
@@ -145,7 +176,7 @@ struct KcOperand {
       for (int hh = 0; hh < 2; ++hh) {
         const int k = ks * 32 + 8 * g + 4 * hh + (r >> 2);
         const char* pa = tile + k * ROWB + mn_slot(mn >> 3, k) * 16 + (mn & 7) * 2;
-        h[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4*)(pa));
+        h[hh] = kc_read_tr(pa);
       }
       return bf16x8{h[0][0], h[0][1], h[0][2], h[0][3], h[1][0], h[1][1], h[1][2], h[1][3]};
     }
@@ -181,8 +212,8 @@ __device__ __forceinline__ void kc_gemm_tile(const KcArgs& p, const Epi& epi, in
   auto issue = [&](int j) {
     const int64_t k0 = kbeg + (int64_t)j * BK;
     char* st = kc_lds + (j % STAGES) * STAGE;
-    OA::issue(abase, p.lda, m0, arows, k0, kend, st, wid, lane);
-    OB::issue(bbase, p.ldb, n0, brows, k0, kend, st + TA, wid, lane);
+    OA::issue(abase, p.lda, p.asegsh, p.asegs, m0, arows, k0, kend, st, wid, lane);
+    OB::issue(bbase, p.ldb, p.bsegsh, p.bsegs, n0, brows, k0, kend, st + TA, wid, lane);
   };
 
   f32x4 acc[FM][FN];
@@ -200,6 +231,8 @@ __device__ __forceinline__ void kc_gemm_tile(const KcArgs& p, const Epi& epi, in
       for (int i = 0; i < FM; ++i) a[i] = OA::frag(st, wm * (BM / WM) + i * 16, ks, lane);
 #pragma unroll
       for (int jn = 0; jn < FN; ++jn) b[jn] = OB::frag(st + TA, wn * (BN / WN) + jn * 16, ks, lane);
+      if constexpr (!AKC) kc_lds_wait(a);
+      if constexpr (!BKC) kc_lds_wait(b);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -246,14 +279,20 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kc_group_kernel(const KcGro
   kc_gemm_tile<BM, BN, WM, WN, STAGES, BK, AKC, BKC, Epi>(g.p[i], g.e[i], (int)blockIdx.x - g.start[i]);
 }
 
-// Whether an operand can go through the direct-to-LDS path: plain rows
-// (no segments or gate interleave), 16-byte aligned rows and batch strides,
-// the whole k range inside the operand; MN-contiguous operands also need an
-// MN extent that is a multiple of 8 (whole 16-byte chunks).
+// Whether an operand can go through the direct-to-LDS path: no gate
+// interleave, 16-byte aligned rows and batch strides, the whole k range inside
+// the operand; MN-contiguous operands also need an MN extent that is a
+// multiple of 8 (whole 16-byte chunks), and may come in k segments of a power
+// of two of at least 64 rows (whole k-tiles); K-contiguous ones may not be
+// segmented.
 static inline bool kc_operand_ok(const Opnd& o, int64_t K, bool kc) {
-  const bool plain = o.seg == 0 && o.ilH == 0 && o.ld % 8 == 0 && o.zstride % 8 == 0 && ((uintptr_t)o.base & 15) == 0;
-  return plain && (kc ? o.ext >= K : (o.rows >= K && o.ext % 8 == 0));
+  const bool plain = o.ilH == 0 && o.ld % 8 == 0 && o.zstride % 8 == 0 && ((uintptr_t)o.base & 15) == 0;
+  if (kc) return plain && o.seg == 0 && o.ext >= K;
+  const bool segok = o.seg == 0 || (o.seg >= 64 && (o.seg & (o.seg - 1)) == 0 && o.segstride % 8 == 0);
+  return plain && o.rows >= K && o.ext % 8 == 0 && segok;
 }
+
+static inline int kc_seg_shift(const Opnd& o) { return o.seg > 0 ? __builtin_ctzll((unsigned long long)o.seg) : 0; }
 
 static int kc_group_rows = 4;   // measured best at the learner-step shapes
 
@@ -266,6 +305,8 @@ static inline KcArgs kc_args(const Opnd& A, const Opnd& B, int64_t M, int64_t N,
   // epilogue drops)
   p.A = (const bf16*)A.base; p.lda = A.ld; p.azs = A.zstride; p.arows = AKC ? std::min<int64_t>(A.rows, M) : A.ext;
   p.B = (const bf16*)B.base; p.ldb = B.ld; p.bzs = B.zstride; p.brows = BKC ? std::min<int64_t>(B.rows, N) : B.ext;
+  p.asegsh = AKC ? 0 : kc_seg_shift(A); p.asegs = A.segstride;
+  p.bsegsh = BKC ? 0 : kc_seg_shift(B); p.bsegs = B.segstride;
   p.M = M; p.N = N; p.K = K;
   p.ksplit = splits > 1 ? rup(cdiv(K, splits), C::BK) : (K > 0 ? K : 1);
   p.splits = splits;

@@ -493,29 +493,19 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
   float* part = (float*)(ws + lo.SKP);
   float* csp = (float*)(ws + lo.CSP);
   constexpr bool lp = std::is_same<T, bf16>::value;
-  T* WIT = (T*)(ws + lo.WIT);
-  // Transposed operand copies (bf16): W_ih^T of layers 1.. with both
-  // directions side by side, so dX is one K-contiguous product over 8H, and
-  // W_hh^T for the per-step BPTT kernels.  One launch makes all of them.
+  // W_hh^T (bf16 and float32 paths): the per-step BPTT kernels' operand and
+  // the persistent kernel's staging source.  One launch makes all layers'.
   bool have_wt = false;
-  auto make_copies = [&](bool wih, bool whh) {
+  auto make_copies = [&]() {
     if constexpr (lp) {
       XposeJobs jobs;
       int n = 0;
-      if (whh)
-        for (int l = 0; l < lo.L; ++l)
-          for (int d = 0; d < 2; ++d)
-            jobs.j[n++] = XposeJob{(const bf16*)(W + lo.Whh[l][d]), (bf16*)(WT + (int64_t)(2 * l + d) * 4 * H * H),
-                                   H, 4 * H, 4 * H, H};
-      if (wih)
-        for (int l = 1; l < lo.L; ++l)
-          for (int d = 0; d < 2; ++d)
-            jobs.j[n++] = XposeJob{(const bf16*)(W + lo.Wih[l][d]),
-                                   (bf16*)(WIT + (int64_t)(l - 1) * 2 * H * 8 * H + (int64_t)d * 4 * H),
-                                   2 * H, 8 * H, 4 * H, 2 * H};
+      for (int l = 0; l < lo.L; ++l)
+        for (int d = 0; d < 2; ++d)
+          jobs.j[n++] = XposeJob{(const bf16*)(W + lo.Whh[l][d]), (bf16*)(WT + (int64_t)(2 * l + d) * 4 * H * H),
+                                 H, 4 * H, 4 * H, H};
       transpose_bf16("transpose_w", s, jobs, n);
     } else {
-      if (!whh) return;
       TransposeSrc src;
       for (int i = 0; i < 2 * MAX_LAYERS; ++i) src.p[i] = nullptr;
       for (int l = 0; l < lo.L; ++l)
@@ -524,10 +514,9 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
                    dim3((unsigned)cdiv(H, 32), (unsigned)cdiv(4 * H, 32), 2 * lo.L), dim3(256), 0, s,
                    src, 4 * H, H, WT);
     }
-    if (whh) have_wt = true;
+    have_wt = true;
   };
-  // W_hh^T serves the per-step kernels and the persistent kernel's LDS staging
-  make_copies(lp && lo.L > 1, true);
+  make_copies();
   // weight gradients on the side stream (bf16 per-step BPTT writing da^T):
   // layer l's buffers (da^T, bias partials, split-K partials) alternate by
   // layer parity, so BPTT of layer l waits only for the side work of l+2
@@ -536,7 +525,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
   if (hipStreamIsCapturing(s, &cap) != hipSuccess) { (void)hipGetLastError(); cap = hipStreamCaptureStatusActive; }
   // not under stream capture: replaying graphs with these parallel branches
   // measured far slower on MI355X than the serial graph
-  if (lp && lo.xpose_act && cap == hipStreamCaptureStatusNone && !use_persistent<T>(H, lo.T, true, s))
+  if (lp && lo.write_dat && cap == hipStreamCaptureStatusNone && !use_persistent<T>(H, lo.T, true, s))
     side = side_stream();
   hipStream_t ss = side ? side->st : s;
   float* part_side = side ? (float*)(ws + lo.SKP2) : part;
@@ -557,7 +546,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       PersistArgs pa = persist_args(lo, (const bf16*)W, ws, l);
       pa.DA = (bf16*)DA; pa.DY = dY; pa.C = (float*)Cl; pa.G = (bf16*)Gl;
       pa.WT = (const bf16*)(WT + (int64_t)(2 * l) * 4 * H * H);
-      pa.DAT = lo.xpose_act ? (bf16*)DATl : nullptr;
+      pa.DAT = lo.write_dat ? (bf16*)DATl : nullptr;
       pa.DBP = DBPl;
       pa.M = M;
       if (!xch_cleared) xch_cleared = persist_clear(true, pa, s) == hipSuccess;
@@ -566,11 +555,11 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       step_fused = done;
     }
     if (!done) {
-      if (!have_wt) make_copies(false, true);
+      if (!have_wt) make_copies();
       RecBwdArgs<T> rb;
       rb.DA = DA; rb.WT0 = WT + (int64_t)(2 * l) * 4 * H * H; rb.WT1 = WT + (int64_t)(2 * l + 1) * 4 * H * H;
       rb.DY = dY; rb.G = Gl; rb.C = Cl; rb.DC = DC; rb.Tn = Tn; rb.B = B; rb.H = H;
-      rb.DAT = lo.xpose_act ? DATl : nullptr;
+      rb.DAT = lo.write_dat ? DATl : nullptr;
       rb.DBP = DBPl;
       rb.M = M;
       const dim3 grid(H / 16, (unsigned)cdiv(B, 16), 2);
@@ -591,40 +580,35 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     float* part_dx = (float*)((char*)part + lo.skp_dx[l]);
     float* dst_dx = (dY == (const float*)(ws + lo.DYa)) ? (float*)(ws + lo.DYb) : (float*)(ws + lo.DYa);
     bool dw_done = false, dx_done = l == 0;
+    // W_ih of both directions as the dX product's B operand, read as it lies
+    // (k = gate row of direction d in segment d, n = input unit)
+    Opnd Bw = opnd(W + lo.Wih[l][0], Dl, Dl, 8 * H);
+    Bw.seg = 4 * H;
+    Bw.segstride = lo.Wih[l][1] - lo.Wih[l][0];
     if constexpr (lp) {
-      if (lo.xpose_act) {
-        // K-contiguous (frame-contiguous) copies for the weight gradients: da^T
-        // (written by the per-step BPTT kernel, else transposed here), X_l^T
-        // into the buffer that held Y_{l+1}^T; Y_l^T was made one layer up (or
-        // from y_top).
-        T* DAT = DATl;
-        T* YTl = (T*)(ws + lo.YT[l & 1]);
-        T* XTl = (T*)(ws + lo.YT[(l + 1) & 1]);
-        XposeJobs jobs;
-        int n = 0;
-        if (!step_fused) jobs.j[n++] = XposeJob{(const bf16*)DA, (bf16*)DAT, 8 * H, M, (int)M, 8 * H};
-        if (l == lo.L - 1) jobs.j[n++] = XposeJob{(const bf16*)Yl, (bf16*)YTl, 2 * H, M, (int)M, 2 * H};
-        jobs.j[n++] = XposeJob{(const bf16*)Xl, (bf16*)XTl, Dpl, M, (int)M, Dpl};
-        transpose_bf16("transpose_act", ss, jobs, n);
+      if (lo.write_dat) {
+        // A: da^T (frame-contiguous, written by the BPTT kernel); B: the layer
+        // input X_l and output h_l as they lie (frame rows).
         // dW_ih[d] = da_d^T X_l  (4H x D_l, reduction over all frames);
-        // dW_hh[d] = sum_t da_d[t]^T h_d[t_prev] (frames shifted as below);
+        // dW_hh[d] = sum_t da_d[t]^T h_d[t_prev] (the forward direction pairs
+        // frame t with t-1, the reverse one t with t+1);
         // without the side stream also dX_l (below), all in one launch
+        T* DAT = DATl;
         F32Job g[3];
-        g[0] = F32Job{opnd(DAT, M, (int)M, 4 * H, 4 * H * M), opnd(XTl, M, (int)M, Dl), 4 * H, Dl, M, 2,
+        g[0] = F32Job{opnd(DAT, M, (int)M, 4 * H, 4 * H * M), opnd(Xl, Dpl, Dpl, M), 4 * H, Dl, M, 2,
                       lo.sp_dWih[l], grad + lo.Wih[l][0], Dl, lo.Wih[l][1] - lo.Wih[l][0], part_ih};
-        g[1] = F32Job{opnd(DAT + B, M, (int)Kr, 4 * H, 4 * H * M - B), opnd(YTl, M, (int)Kr, H, (int64_t)H * M + B),
+        g[1] = F32Job{opnd(DAT + B, M, (int)Kr, 4 * H, 4 * H * M - B), opnd(Yl, 2 * H, H, Kr, (int64_t)B * 2 * H + H),
                       4 * H, H, Kr, 2, lo.sp_dWhh, grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part_hh};
         int ng = 2;
         if (!side && l > 0)
-          g[ng++] = F32Job{opnd(DA, 8 * H, 8 * H, M), opnd(WIT + (int64_t)(l - 1) * 2 * H * 8 * H, 8 * H, 8 * H, Dl),
-                           M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0, part_dx};
-        if (gemm_f32_group<true, true>("gemm_bwd_group", ss, ng, g)) {
-          dx_done = dx_done || ng == 3;
-        } else {
-          for (int i = 0; i < 2; ++i)
-            gemm_f32<T, true, true, V, V>(i ? "gemm_dwhh" : "gemm_dwih", ss, g[i].A, g[i].B, g[i].M, g[i].N, g[i].K,
-                                          g[i].batches, g[i].splits, g[i].dst, g[i].ld, g[i].dst_zstride, g[i].part);
+          g[ng++] = F32Job{opnd(DA, 8 * H, 8 * H, M), Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0, part_dx};
+        if (!gemm_f32_group<true, false>("gemm_bwd_group", ss, ng, g)) {
+          static const char* const nm[3] = {"gemm_dwih", "gemm_dwhh", "gemm_dx"};
+          for (int i = 0; i < ng; ++i)
+            gemm_f32<T, true, false, V, V>(nm[i], ss, g[i].A, g[i].B, g[i].M, g[i].N, g[i].K, g[i].batches,
+                                           g[i].splits, g[i].dst, g[i].ld, g[i].dst_zstride, g[i].part);
         }
+        dx_done = dx_done || ng == 3;
         dw_done = true;
       }
     }
@@ -652,17 +636,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     // dX_l = sum_d da_d W_ih[d]  (the gradient reaching the layer below)
     if (!dx_done) {
       const Opnd A = opnd(DA, 8 * H, 8 * H, M);
-      if constexpr (lp) {
-        const Opnd Bw = opnd(WIT + (int64_t)(l - 1) * 2 * H * 8 * H, 8 * H, 8 * H, Dl);
-        gemm_f32<T, true, true, V, V>("gemm_dx", s, A, Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0,
-                                      part_dx);
-      } else {
-        Opnd Bw = opnd(W + lo.Wih[l][0], Dl, Dl, 8 * H);
-        Bw.seg = 4 * H;
-        Bw.segstride = lo.Wih[l][1] - lo.Wih[l][0];
-        gemm_f32<T, true, false, V, V>("gemm_dx", s, A, Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0,
-                                       part_dx);
-      }
+      gemm_f32<T, true, false, V, V>("gemm_dx", s, A, Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0, part_dx);
     }
     if (l > 0) dY = dst_dx;
   }
