@@ -579,7 +579,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     float* part_hh = (float*)((char*)part_side + lo.skp_hh[l]);
     float* part_dx = (float*)((char*)part + lo.skp_dx[l]);
     float* dst_dx = (dY == (const float*)(ws + lo.DYa)) ? (float*)(ws + lo.DYb) : (float*)(ws + lo.DYa);
-    bool dw_done = false, dx_done = l == 0;
+    bool dw_done = false, dx_done = l == 0, db_done = false;
     // W_ih of both directions as the dX product's B operand, read as it lies
     // (k = gate row of direction d in segment d, n = input unit)
     Opnd Bw = opnd(W + lo.Wih[l][0], Dl, Dl, 8 * H);
@@ -602,7 +602,14 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
         int ng = 2;
         if (!side && l > 0)
           g[ng++] = F32Job{opnd(DA, 8 * H, 8 * H, M), Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0, part_dx};
-        if (!gemm_f32_group<true, false>("gemm_bwd_group", ss, ng, g)) {
+        // db_ih = db_hh = sum over frames of da, from the BPTT kernel's
+        // per-row-block partials, in the same reduction launch
+        const ColSumJob cs{DBPl, (done ? 1 : Tn) * (int)cdiv(B, 16), 2, 4 * H, 8 * H, 4 * H,
+                           grad + lo.bih[l][0], grad + lo.bhh[l][0], lo.bih[l][1] - lo.bih[l][0]};
+        const bool with_db = step_fused && colsum_job_ok(cs);
+        if (gemm_f32_group<true, false>("gemm_bwd_group", ss, ng, g, with_db ? &cs : nullptr)) {
+          db_done = with_db;
+        } else {
           static const char* const nm[3] = {"gemm_dwih", "gemm_dwhh", "gemm_dx"};
           for (int i = 0; i < ng; ++i)
             gemm_f32<T, true, false, V, V>(nm[i], ss, g[i].A, g[i].B, g[i].M, g[i].N, g[i].K, g[i].batches,
@@ -625,13 +632,15 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       gemm_f32<T, false, false, V, V>("gemm_dwhh", s, Ad, Bh, 4 * H, H, Kr, 2, lo.sp_dWhh,
                                       grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part_hh);
     }
-    // db_ih = db_hh = sum over frames of da
-    if (step_fused)
-      colsum_parts("colsum_db", ss, DBPl, (done ? 1 : Tn) * (int)cdiv(B, 16), 8 * H, 4 * H,
-                   lo.bih[l][1] - lo.bih[l][0], grad + lo.bih[l][0], grad + lo.bhh[l][0]);
-    else
-      colsum<T>("colsum_db", s, DA, M, 8 * H, 8 * H, csp, 4 * H, lo.bih[l][1] - lo.bih[l][0],
-                grad + lo.bih[l][0], grad + lo.bhh[l][0]);
+    // db_ih = db_hh = sum over frames of da (unless the reduction above did it)
+    if (!db_done) {
+      if (step_fused)
+        colsum_parts("colsum_db", ss, DBPl, (done ? 1 : Tn) * (int)cdiv(B, 16), 8 * H, 4 * H,
+                     lo.bih[l][1] - lo.bih[l][0], grad + lo.bih[l][0], grad + lo.bhh[l][0]);
+      else
+        colsum<T>("colsum_db", s, DA, M, 8 * H, 8 * H, csp, 4 * H, lo.bih[l][1] - lo.bih[l][0],
+                  grad + lo.bih[l][0], grad + lo.bhh[l][0]);
+    }
     if (side) (void)hipEventRecord(side->dw_done[l], ss);
     // dX_l = sum_d da_d W_ih[d]  (the gradient reaching the layer below)
     if (!dx_done) {

@@ -145,14 +145,28 @@ struct F32Job {
   float* part;   // splits x M x N floats per batch entry when splits > 1
 };
 
+// Column sums riding on a grouped launch's reduction: dst[z][n] (and dst2)
+// = sum over r < rows of part[z * zin + r * kstride + n], n < N, in row order.
+struct ColSumJob {
+  const float* part;
+  int rows, batches;
+  int64_t N, kstride, zin;
+  float* dst;
+  float* dst2;   // optional second copy
+  int64_t dst_zstride;
+};
+
 // One reduction of a grouped launch: float4 e of the job covers batch entry
-// z = e / (M N/4), row m and columns 4c..4c+3 of what remains.
+// z = e / (M N/4), row m and columns 4c..4c+3 of what remains; the summands
+// are kstride apart, batch entries zin apart in part.
 struct ReduceJob {
   const float* part;
   float* dst;
+  float* dst2;               // optional second copy
   uint32_t N4, per, count;   // N/4; M N/4; batches M N/4
   int64_t ld, dst_zstride;
-  int splits, start;         // start: first block of this job
+  int64_t kstride, zin;
+  int splits, start;         // splits: summands; start: first block of this job
 };
 struct ReduceGroup {
   ReduceJob j[KC_MAX_GROUP];
@@ -167,21 +181,30 @@ static __global__ __launch_bounds__(256) void splitk_reduce_group_kernel(const R
   if (e >= r.count) return;
   const uint32_t z = e / r.per, rem = e - z * r.per;
   const uint32_t m = rem / r.N4, n = (rem - m * r.N4) * 4;
-  const int64_t mn = (int64_t)r.per * 4;
-  const float* p = r.part + (int64_t)z * r.splits * mn + (int64_t)m * r.N4 * 4 + n;
+  const float* p = r.part + (int64_t)z * r.zin + (int64_t)m * r.N4 * 4 + n;
   float4 acc = *(const float4*)p;
   for (int k = 1; k < r.splits; ++k) {
-    const float4 v = *(const float4*)(p + (int64_t)k * mn);
+    const float4 v = *(const float4*)(p + (int64_t)k * r.kstride);
     acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
   }
-  *(float4*)(r.dst + (int64_t)z * r.dst_zstride + (int64_t)m * r.ld + n) = acc;
+  const int64_t o = (int64_t)z * r.dst_zstride + (int64_t)m * r.ld + n;
+  *(float4*)(r.dst + o) = acc;
+  if (r.dst2) *(float4*)(r.dst2 + o) = acc;
+}
+
+static inline bool colsum_job_ok(const ColSumJob& c) {
+  return c.N % 4 == 0 && c.kstride % 4 == 0 && c.zin % 4 == 0 && c.dst_zstride % 4 == 0 && c.rows >= 1 &&
+         ((uintptr_t)c.part & 15) == 0 && ((uintptr_t)c.dst & 15) == 0 && ((uintptr_t)c.dst2 & 15) == 0 &&
+         (int64_t)c.batches * c.N / 4 < ((int64_t)1 << 31);
 }
 
 // bf16 products only (the direct-to-LDS kernel); false and nothing launched
 // if a product cannot take that path or its reduction needs unaligned rows.
+// cs (optional): column sums added to the reduction launch.
 template <bool AKC, bool BKC>
-static inline bool gemm_f32_group(const char* name, hipStream_t s, int n, const F32Job* jb) {
-  if (n < 1 || n > KC_MAX_GROUP) return false;
+static inline bool gemm_f32_group(const char* name, hipStream_t s, int n, const F32Job* jb,
+                                  const ColSumJob* cs = nullptr) {
+  if (n < 1 || n > KC_MAX_GROUP || (cs && (n == KC_MAX_GROUP || !colsum_job_ok(*cs)))) return false;
   KcItem it[KC_MAX_GROUP];
   EpiStore<float> e[KC_MAX_GROUP];
   ReduceGroup rg;
@@ -200,9 +223,21 @@ static inline bool gemm_f32_group(const char* name, hipStream_t s, int n, const 
       return false;
     e[i] = epi_store<float>(j.part, j.N, j.M, j.N, (int64_t)j.splits * j.M * j.N, j.M * j.N);
     ReduceJob& r = rg.j[rg.n++];
-    r.part = j.part; r.dst = j.dst;
+    r.part = j.part; r.dst = j.dst; r.dst2 = nullptr;
     r.N4 = (uint32_t)(j.N / 4); r.per = (uint32_t)(j.M * j.N / 4); r.count = (uint32_t)count;
-    r.ld = j.ld; r.dst_zstride = j.dst_zstride; r.splits = j.splits; r.start = rblocks;
+    r.ld = j.ld; r.dst_zstride = j.dst_zstride;
+    r.kstride = j.M * j.N; r.zin = (int64_t)j.splits * j.M * j.N;
+    r.splits = j.splits; r.start = rblocks;
+    rblocks += (int)cdiv(count, 256);
+  }
+  if (cs) {
+    const int64_t count = (int64_t)cs->batches * cs->N / 4;
+    ReduceJob& r = rg.j[rg.n++];
+    r.part = cs->part; r.dst = cs->dst; r.dst2 = cs->dst2;
+    r.N4 = (uint32_t)(cs->N / 4); r.per = r.N4; r.count = (uint32_t)count;
+    r.ld = 0; r.dst_zstride = cs->dst_zstride;
+    r.kstride = cs->kstride; r.zin = cs->zin;
+    r.splits = cs->rows; r.start = rblocks;
     rblocks += (int)cdiv(count, 256);
   }
   if (!gemm_kc_group_launch<AKC, BKC>(name, s, n, it, e)) return false;
