@@ -494,7 +494,8 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
   float* csp = (float*)(ws + lo.CSP);
   constexpr bool lp = std::is_same<T, bf16>::value;
   // W_hh^T (bf16 and float32 paths): the per-step BPTT kernels' operand and
-  // the persistent kernel's staging source.  One launch makes all layers'.
+  // the persistent kernel's LDS staging source when a workgroup takes more
+  // than one 16-row block.  One launch makes all layers'.
   bool have_wt = false;
   auto make_copies = [&]() {
     if constexpr (lp) {
@@ -516,7 +517,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     }
     have_wt = true;
   };
-  make_copies();
+  if (!use_persistent<T>(H, lo.T, true, s) || persist_bwd_needs_wt(H, B)) make_copies();
   // weight gradients on the side stream (bf16 per-step BPTT writing da^T):
   // layer l's buffers (da^T, bias partials, split-K partials) alternate by
   // layer parity, so BPTT of layer l waits only for the side work of l+2
@@ -545,7 +546,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     if (use_persistent<T>(H, lo.T, true, s)) {
       PersistArgs pa = persist_args(lo, (const bf16*)W, ws, l);
       pa.DA = (bf16*)DA; pa.DY = dY; pa.C = (float*)Cl; pa.G = (bf16*)Gl;
-      pa.WT = (const bf16*)(WT + (int64_t)(2 * l) * 4 * H * H);
+      pa.WT = have_wt ? (const bf16*)(WT + (int64_t)(2 * l) * 4 * H * H) : nullptr;
       pa.DAT = lo.write_dat ? (bf16*)DATl : nullptr;
       pa.DBP = DBPl;
       pa.M = M;

@@ -37,6 +37,8 @@
 #include "xpose.hpp"
 #include "dma.hpp"
 
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
 #define PU 32
 #define SPIN_LIMIT (1u << 18)
 #define H_MAX_MEMBERS 16   // H / 32 for the largest H whose W_hh slice fits in LDS
@@ -390,31 +392,44 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int NB = H / 16;
   // MB == 1: B fragments of the unit blocks nb = 16*bi + w + 4*j of this
   // wave, k-step ks (lane l: own rows ks*32 + (l/16)*8 .. +8, unit
-  // nb*16 + l%16), from W_hh^T (16 contiguous bytes) or else W_hh
+  // nb*16 + l%16), read from W_hh as it lies: the own rows are staged into
+  // LDS by direct-to-LDS loads ([kk][512 units], 1 KB rows, the 16-byte chunk
+  // c of row kk in slot c ^ wswz(kk); units past H read as zeros), and each
+  // lane takes its fragments with transposing LDS reads (ds_read_b64_tr_b16:
+  // in a 16-lane group lane r addresses 4 consecutive units of k row r/4 and
+  // receives unit column r's values over those 4 rows; two reads give the 8
+  // consecutive k of the MFMA B operand).  The swizzle spreads the 16 rows of
+  // one read over distinct chunk pairs.
   bf16x8 bw[WREG ? 2 : 1][4][4];
   if constexpr (WREG) {
-    const bf16* WTd = a.WT ? a.WT + (int64_t)d * H * 4 * H : nullptr;
-    const bf16* Wd = a.W + (d ? a.whh1 : a.whh0);
+    auto wswz = [](int k) { return 2 * ((k & 3) | (((k >> 3) & 1) << 2)); };
+    char* stg = (char*)lds;
+    const __amdgpu_buffer_rsrc_t rw = dma_rsrc(a.W + (d ? a.whh1 : a.whh0));
+#pragma unroll
+    for (int q = 0; q < 32; ++q) {
+      const int kk = q * 4 + w;   // one 1 KB row per load instruction
+      const int c = lane ^ wswz(kk);
+      const int64_t grow = (int64_t)((kk >> 4) & 3) * H + u0 + (kk >> 6) * 16 + (kk & 15);
+      dma16(rw, c * 8 < H ? (uint32_t)((grow * H + c * 8) * 2) : DMA_OFF_NONE, stg + kk * 1024);
+    }
+    dma_wait_all();
+    __syncthreads();
+    const int gq = lane >> 4, r = lane & 15;
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int nb = bi * 16 + w + 4 * j;
-          const int kk = ks * 32 + (lane >> 4) * 8;
-          const int64_t grow = (int64_t)((kk >> 4) & 3) * H + u0 + (kk >> 6) * 16 + (kk & 15);
-          const int64_t n = (int64_t)nb * 16 + (lane & 15);
-          bf16x8 v{};
-          if (nb < NB) {
-            if (WTd) {
-              v = *(const bf16x8*)(WTd + n * 4 * H + grow);
-            } else {
+          const int mn = (bi * 16 + w + 4 * j) * 16 + 4 * (r & 3);
+          bf16x4 h[2];
 #pragma unroll
-              for (int i = 0; i < 8; ++i) v[i] = Wd[(grow + i) * H + n];
-            }
+          for (int hh = 0; hh < 2; ++hh) {
+            const int k = ks * 32 + 8 * gq + 4 * hh + (r >> 2);
+            const char* pa = stg + k * 1024 + ((mn >> 3) ^ wswz(k)) * 16 + (mn & 7) * 2;
+            h[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((__attribute__((address_space(3))) bf16x4*)(pa));
           }
-          bw[bi][ks][j] = v;
+          bw[bi][ks][j] = bf16x8{h[0][0], h[0][1], h[0][2], h[0][3], h[1][0], h[1][1], h[1][2], h[1][3]};
         }
   } else if (a.WT && H % 64 == 0) {
     // from W_hh^T [H][4H] (made by the caller): the 8 own rows of k group kg
@@ -698,9 +713,11 @@ __global__ __launch_bounds__(256) void clear_exchange_kernel(uint4* p, int64_t n
 // Host side.
 // ---------------------------------------------------------------------------
 size_t persist_lds_bytes(int H, bool backward, int MB) {
-  if (backward)   // MB == 1 keeps W_hh in registers
-    return (MB == 1 ? (size_t)0 : (size_t)16 * (H + 1) * 16) + (size_t)16 * (16 * MB + 1) * 16 +
-           (size_t)16 * MB * PU * 4;
+  if (backward) {   // MB == 1 keeps W_hh in registers, staged through 128 KB of LDS
+    const size_t run = (MB == 1 ? (size_t)0 : (size_t)16 * (H + 1) * 16) + (size_t)16 * (16 * MB + 1) * 16 +
+                       (size_t)16 * MB * PU * 4;
+    return MB == 1 ? std::max(run, (size_t)128 * 1024) : run;
+  }
   // MB == 1 keeps W_hh in registers: reduction buffer and gathered h only
   if (MB == 1) return (size_t)8 * 64 * 16 + (size_t)(H / 8) * 17 * 16;
   return (size_t)(H / 8) * (128 + 1) * 16 + 8 * 64 * 16;
@@ -800,6 +817,11 @@ static bool persist_plan(bool backward, int H, int B, int* MBo, int* chunko) {
   *MBo = MB;
   *chunko = std::min(B, max_ns * 16 * MB);
   return (B + *chunko - 1) / *chunko <= 255;
+}
+
+bool persist_bwd_needs_wt(int H, int B) {
+  int MB, chunk;
+  return !persist_plan(true, H, B, &MB, &chunk) || MB > 1;
 }
 
 hipError_t persist_clear(bool backward, const PersistArgs& a, hipStream_t s) {

@@ -7,7 +7,8 @@ struct PersistArgs {
   bf16* Y;            // layer output [M][2H] (forward: read h_prev, write h)
   const bf16* W;      // bf16 parameter copy (flat layout)
   int64_t whh0, whh1; // element offsets of W_hh for the two directions
-  const bf16* WT;     // backward, optional: W_hh^T of this layer, [2][H][4H] (directions)
+  const bf16* WT;     // backward with more than one 16-row block per workgroup: W_hh^T of
+                      // this layer, [2][H][4H] (directions)
   const bf16* Gx;     // forward: input projection [M][8H]
   float* C;           // cell states [M][2H] (forward writes, backward reads)
   bf16* G;            // activated gates [M][8H] (forward writes, backward reads)
@@ -41,6 +42,9 @@ static inline size_t persist_xch_bytes(int B, int H) {
 // True if the persistent kernels can hold a W_hh slice for this H in LDS
 // (and T fits the 8-bit step numbers).
 bool persist_supported(int H, int T);
+// Whether the persistent BPTT of a layer reads W_hh^T (PersistArgs::WT): only
+// when its workgroups take more than one 16-row block (W_hh slice in LDS).
+bool persist_bwd_needs_wt(int H, int B);
 // Clears the exchange words; once per forward or backward call, before its
 // first persist_layer.
 hipError_t persist_clear(bool backward, const PersistArgs& a, hipStream_t s);
