@@ -163,17 +163,36 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int ks_end = KSPLIT ? (wx ? nks : nks / 2) : nks;
   // MB == 1: B fragments of the k half (at most H_MAX_MEMBERS / 2 k-steps;
   // lane l: gate row q*H + unit, k = ks*32 + (l/16)*8 .. +8); k-steps past
-  // the half's end hold a valid k-step and meet a zero A fragment
+  // the half's end hold a valid k-step and meet a zero A fragment.  The 128
+  // own gate rows (gate q, unit u0 + i at local row q*32 + i) are staged by
+  // direct-to-LDS loads, 1 KB rows (units past H read as zeros), the 16-byte
+  // chunk c of local row lr in slot c ^ (lr & 15) so that the 16 rows of one
+  // fragment read land in distinct bank groups.
   constexpr int KH = H_MAX_MEMBERS / 2;
   bf16x8 bw[KSPLIT ? KH : 1][4];
   if constexpr (KSPLIT) {
+    char* stg = (char*)lds;
+    const __amdgpu_buffer_rsrc_t rw = dma_rsrc(Wd);
+#pragma unroll
+    for (int q = 0; q < 32; ++q) {
+      const int lr = q * 4 + w;   // one 1 KB row per load instruction
+      const int c = lane ^ (lr & 15);
+      const int64_t grow = (int64_t)(lr >> 5) * H + u0 + (lr & 31);
+      dma16(rw, c * 8 < H ? (uint32_t)((grow * H + c * 8) * 2) : DMA_OFF_NONE, stg + lr * 1024);
+    }
+    dma_wait_all();
+    __syncthreads();
 #pragma unroll
     for (int i = 0; i < KH; ++i) {
       const int ks = max(0, min(ks_beg + i, ks_end - 1));
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        bw[i][q] = *(const bf16x8*)(Wd + (int64_t)(q * H + unit) * H + ks * 32 + (lane >> 4) * 8);
+      for (int q = 0; q < 4; ++q) {
+        const int lr = q * 32 + ub * 16 + (lane & 15);
+        const int c = ks * 4 + (lane >> 4);
+        bw[i][q] = *(const bf16x8*)(stg + lr * 1024 + (c ^ (lr & 15)) * 16);
+      }
     }
+    __syncthreads();   // the reduction buffer and gathered h reuse this LDS
   }
   const int wpr = H / 2;                        // exchange words per row
   const int64_t slot_stride = (int64_t)2 * a.rows * wpr;
@@ -718,8 +737,9 @@ size_t persist_lds_bytes(int H, bool backward, int MB) {
                        (size_t)16 * MB * PU * 4;
     return MB == 1 ? std::max(run, (size_t)128 * 1024) : run;
   }
-  // MB == 1 keeps W_hh in registers: reduction buffer and gathered h only
-  if (MB == 1) return (size_t)8 * 64 * 16 + (size_t)(H / 8) * 17 * 16;
+  // MB == 1 keeps W_hh in registers (staged through 128 KB of LDS at the
+  // start): reduction buffer and gathered h after that
+  if (MB == 1) return std::max((size_t)8 * 64 * 16 + (size_t)(H / 8) * 17 * 16, (size_t)128 * 1024);
   return (size_t)(H / 8) * (128 + 1) * 16 + 8 * 64 * 16;
 }
 
