@@ -342,6 +342,15 @@ typedef KcCfg<128, 128, 2, 4, 2> KcTile;
 typedef KcCfg<192, 128, 2, 4, 2> KcTileTall;
 static constexpr int64_t kc_round_blocks = 2 * 256;   // two blocks on each of 256 CUs
 
+// Whether a product with K-contiguous A goes to the 192-row blocks.
+static inline bool kc_tall(int64_t M, int64_t N, int batches, int splits) {
+  return M >= KcTileTall::BM && cdiv(M, 128) * cdiv(N, 128) * batches * splits > kc_round_blocks;
+}
+// Whether a product can take the direct-to-LDS kernel.
+static inline bool kc_eligible(const Opnd& A, const Opnd& B, int64_t K, bool akc, bool bkc) {
+  return K % 8 == 0 && kc_operand_ok(A, K, akc) && kc_operand_ok(B, K, bkc);
+}
+
 // GEMM dispatch: bf16 operands with 16-byte aligned rows go to the
 // direct-to-LDS kernel, everything else to the generic kernel.
 template <typename T, bool AKC, bool BKC, int VA, int VB, class Epi>
@@ -349,9 +358,9 @@ static inline void gemm_launch(const char* name, hipStream_t s, const Opnd& A, c
                                int64_t M, int64_t N, int64_t K, int batches, int splits,
                                const Epi& epi) {
   if constexpr (std::is_same<T, bf16>::value) {
-    if (K % 8 == 0 && kc_operand_ok(A, K, AKC) && kc_operand_ok(B, K, BKC)) {
+    if (kc_eligible(A, B, K, AKC, BKC)) {
       if constexpr (AKC) {
-        if (M >= KcTileTall::BM && cdiv(M, 128) * cdiv(N, 128) * batches * splits > kc_round_blocks) {
+        if (kc_tall(M, N, batches, splits)) {
           gemm_kc_launch<KcTileTall, AKC, BKC>(name, s, A, B, M, N, K, batches, splits, epi);
           return;
         }
