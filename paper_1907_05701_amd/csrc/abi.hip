@@ -105,6 +105,8 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   L.DYb = a; a = align256(a + (size_t)M * 2 * H * 4);
   L.DC = a; a = align256(a + (size_t)2 * d->B * H * 4);
   L.WT = a; a = align256(a + (size_t)2 * d->L * 4 * H * H * es);
+  L.WP0_bytes = es == 2 && d->D % 8 != 0 ? (size_t)2 * 4 * H * L.Dp0 * es : 0;
+  L.WP0 = a; a = align256(a + L.WP0_bytes);
   // bf16 with B % 8 == 0: the BPTT kernels also write da frame-contiguous
   // (da^T), the A operand of the weight gradients
   L.write_dat = es == 2 && d->B % 8 == 0;

@@ -80,6 +80,7 @@ struct Layout {
   int64_t Wl, bl, Ws, bs;
   // act_ws byte offsets
   size_t X0, Y[MAX_LAYERS], G[MAX_LAYERS], C[MAX_LAYERS], GX, DYa, DYb, DC, WT, DAT, DBP, CSP, SKP, SKP2, SYNC, XCH;
+  size_t WP0, WP0_bytes;   // bf16 with D % 8 != 0: layer-0 W_ih padded to Dp0 columns (else 0 bytes)
   size_t dat_bytes, dbp_bytes;   // one of the two alternating da^T / bias-partial buffers
   bool write_dat;     // bf16 with B % 8 == 0: BPTT also writes da^T [8H][M] for the weight gradients
   size_t act_bytes;

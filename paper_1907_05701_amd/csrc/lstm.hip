@@ -307,15 +307,28 @@ __global__ __launch_bounds__(256) void lstm_rec_bwd_step(const RecBwdArgs<T> a) 
 // --------------------------------------------------------------------------
 // Small helpers: feature conversion, W_hh transposition, column sums.
 // --------------------------------------------------------------------------
+// The input in the operand precision, rows padded from D to Dp columns
+// (zeros).  bf16 with D not a multiple of 8 also gets a copy of the layer-0
+// W_ih of both directions padded the same way (wp non-null), so that the
+// gate projection's k range (Dp) takes the direct-to-LDS product.
 template <typename T>
 __global__ __launch_bounds__(256) void convert_input_kernel(const float* __restrict__ x, int64_t M,
-                                                            int D, int Dp, T* __restrict__ X) {
-  const int64_t total = M * Dp;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+                                                            int D, int Dp, T* __restrict__ X,
+                                                            const bf16* __restrict__ w0, int64_t wz, int wrows,
+                                                            bf16* __restrict__ wp) {
+  const int64_t total = M * Dp, wtotal = wp ? (int64_t)2 * wrows * Dp : 0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total + wtotal;
        i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t m = i / Dp;
-    const int k = (int)(i % Dp);
-    X[i] = from_f32<T>(k < D ? x[m * D + k] : 0.f);
+    if (i < total) {
+      const int64_t m = i / Dp;
+      const int k = (int)(i % Dp);
+      X[i] = from_f32<T>(k < D ? x[m * D + k] : 0.f);
+    } else {
+      const int64_t j = i - total, zr = j / Dp;
+      const int k = (int)(j % Dp);
+      const int64_t z = zr / wrows, r = zr % wrows;
+      wp[j] = k < D ? w0[z * wz + r * D + k] : (bf16)0.f;
+    }
   }
 }
 
@@ -403,11 +416,12 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
   const int H = lo.H, B = lo.B;
   T* X0 = (T*)(ws + lo.X0);
   T* GX = (T*)(ws + lo.GX);
+  bf16* WP0 = lo.WP0_bytes ? (bf16*)(ws + lo.WP0) : nullptr;
   {
-    const int64_t total = M * lo.Dp0;
+    const int64_t total = M * lo.Dp0 + (WP0 ? (int64_t)2 * 4 * H * lo.Dp0 : 0);
     const unsigned grid = (unsigned)std::min<int64_t>(cdiv(total, 256), 16384);
     BLSTM_LAUNCH("convert_input", convert_input_kernel<T>, dim3(grid), dim3(256), 0, s, x, M, lo.D,
-                 lo.Dp0, X0);
+                 lo.Dp0, X0, (const bf16*)W + lo.Wih[0][0], lo.Wih[0][1] - lo.Wih[0][0], 4 * H, WP0);
   }
   for (int l = 0; l < lo.L; ++l) {
     const T* Xl = l == 0 ? X0 : (const T*)(ws + lo.Y[l - 1]);
@@ -417,10 +431,14 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
     float* Cl = (float*)(ws + lo.C[l]);
     // G_x = X W_ih^T + b_ih + b_hh for both directions (batch z = direction)
     const Opnd A = opnd(Xl, Dpl, Dpl, M);
-    const Opnd Bw = opnd(W + lo.Wih[l][0], Dl, Dl, 4 * H, lo.Wih[l][1] - lo.Wih[l][0]);
+    Opnd Bw = opnd(W + lo.Wih[l][0], Dl, Dl, 4 * H, lo.Wih[l][1] - lo.Wih[l][0]);
     const auto epi = epi_store<T>(GX, 8 * H, M, 4 * H, 4 * H, 0, theta + lo.bih[l][0],
                                   theta + lo.bhh[l][0], lo.bih[l][1] - lo.bih[l][0]);
-    if (Dl % V == 0)
+    if (l == 0 && WP0) {
+      // bf16 with D not a multiple of 8: W_ih padded to the input's pitch
+      Bw = opnd(WP0, Dpl, Dpl, 4 * H, (int64_t)4 * H * Dpl);
+      gemm_launch<T, true, true, V, V>("gemm_gx", s, A, Bw, M, 4 * H, Dpl, 2, 1, epi);
+    } else if (Dl % V == 0)
       gemm_launch<T, true, true, V, V>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
     else
       gemm_launch<T, true, true, V, 4>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
