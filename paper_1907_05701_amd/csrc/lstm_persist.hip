@@ -1,6 +1,7 @@
-// Persistent recurrent kernels (bf16 operands): one cooperative launch runs
-// all T steps of one layer, for both directions at once, with each
-// workgroup's slice of W_hh held in LDS for the whole chunk.
+// Persistent recurrent kernels (bf16 operands): one launch runs all T steps
+// of one layer, for both directions at once, with each workgroup's slice of
+// W_hh on chip for the whole chunk (in registers at one 16-row block per
+// workgroup, staged there through LDS; in LDS for more rows).
 //
 // Work split.  The batch is cut into slices of 16*MB rows; a group of
 // H/32 workgroups owns one (direction, slice) pair and each member owns 32
@@ -8,27 +9,30 @@
 // the half splits the reduction dimension when MB == 1 and the m-blocks
 // otherwise.  Per step a member
 //   forward : gathers h_prev of its slice (all H units), multiplies by its
-//             LDS-resident W_hh rows (4 gates x 32 units), adds the
-//             precomputed input projection and applies the cell; c stays in
-//             registers, h/c/gates are written for BPTT;
-//   backward: gathers da of the previously processed step (all 4H gate
-//             columns), multiplies by its LDS-resident W_hh columns to get
-//             dh_rec for its units, applies the gate derivatives (dc stays in
-//             registers) and writes da of this step.
+//             W_hh rows (4 gates x 32 units), adds the precomputed input
+//             projection and applies the cell; c stays in registers, h/c/gates
+//             are written for BPTT;
+//   backward: applies the gate derivatives for its units (dc stays in
+//             registers), multiplies its own da block by its W_hh rows to get
+//             partial dh_rec for all H units, publishes them, and sums the
+//             partials of all members for its own units.
 //
 // Step-to-step exchange without barriers or cache maintenance.  The values
-// one member needs from the others (h, or da) are also published in an
-// exchange buffer as 8-byte words holding two bf16 values and the step
-// number + 1, written and read with agent-scope relaxed atomic stores and
-// loads.  Atomic accesses to one location are coherent across the whole
-// GPU, so a reader that sees the expected step number in a word also sees
-// that word's payload; readers simply poll the words they need (bounded; the
+// one member needs from the others (h, or partial dh) are published in an
+// exchange buffer as 8-byte words holding two bf16 values and a step number
+// (launch tag and step + 1), written and read with agent-scope relaxed atomic
+// stores and loads.  Atomic accesses to one location are coherent across the
+// whole GPU, so a reader that sees the expected step number in a word also
+// sees that word's payload; readers poll the words they need (bounded; the
 // status word is set if a poll ever gives up).  Two slots alternate by step
 // parity: a member overwrites a slot only after it has consumed the next
 // step from every member, which those members produce only after they have
-// consumed the slot's current contents.  The buffer is cleared before each
-// launch, so no word from an earlier launch can carry a valid step number.
-// The launch is cooperative, so every member of a group is resident.
+// consumed the slot's current contents.  The buffer is cleared once per
+// forward or backward call and every launch of a call has its own tag, so no
+// word from an earlier launch carries a valid step number.  Every member of a
+// group must be resident at once: the launch is plain when the occupancy
+// query shows the whole grid fits on the device, cooperative otherwise (see
+// launch_one).
 #include <stdlib.h>
 #include <string.h>
 
