@@ -155,6 +155,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   }
   f32x4* red = (f32x4*)(lds + (KSPLIT ? (size_t)0 : (size_t)kcn * LDN * 8));
   bf16* hl = (bf16*)(red + 8 * 64);   // MB == 1: gathered h [H/8][16 + 1][8]
+  // MB == 1: a step's c [16][32] (float), h [16][32] and gates [16][4][32]
+  // (bf16) of the own units, staged for 16-byte stores
+  float* sC = (float*)(hl + (size_t)(H / 8) * 17 * 8);
+  bf16* sY = (bf16*)(sC + 16 * 32);
+  bf16* sG = sY + 16 * 32;
   __syncthreads();
 
   const int rend = a.b0 + a.rows;
@@ -358,22 +363,61 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 2, pack_bf16x2(hv[m][r], h_next_unit),
                      fb | (uint32_t)(tau + 1));
         }
-#pragma unroll
-      for (int m = 0; m < MBW; ++m)
+      if constexpr (KSPLIT) {
+        // into LDS; the whole workgroup writes them out after the barrier
+        const int ul = ub * 16 + (lane & 15);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int row = rowbase + (mb0 + m) * 16 + (lane >> 4) * 4 + r;
-          if (row >= rend) continue;
-          const int64_t fr = (int64_t)t * B + row;
-          a.C[fr * 2 * H + (int64_t)d * H + unit] = creg[m][r];
-          a.Y[fr * 2 * H + (int64_t)d * H + unit] = (bf16)hv[m][r];
-          bf16* gs = a.G + fr * 8 * H + (int64_t)d * 4 * H + unit;
+          const int rl = (lane >> 4) * 4 + r;
+          sC[rl * 32 + ul] = creg[0][r];
+          sY[rl * 32 + ul] = (bf16)hv[0][r];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) gs[q * H] = (bf16)gv[m][r][q];
+          for (int q = 0; q < 4; ++q) sG[(rl * 4 + q) * 32 + ul] = (bf16)gv[0][r][q];
         }
+      } else {
+#pragma unroll
+        for (int m = 0; m < MBW; ++m)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int row = rowbase + (mb0 + m) * 16 + (lane >> 4) * 4 + r;
+            if (row >= rend) continue;
+            const int64_t fr = (int64_t)t * B + row;
+            a.C[fr * 2 * H + (int64_t)d * H + unit] = creg[m][r];
+            a.Y[fr * 2 * H + (int64_t)d * H + unit] = (bf16)hv[m][r];
+            bf16* gs = a.G + fr * 8 * H + (int64_t)d * 4 * H + unit;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) gs[q * H] = (bf16)gv[m][r][q];
+          }
+      }
     }
     if (epi && tau + 1 < Tn) load_gx(d ? Tn - 2 - tau : tau + 1);
     __syncthreads();   // the reduction buffer is reused by the next step
+    if constexpr (KSPLIT) {
+      // c, h and the gates of the step in 16-byte pieces (448 per step
+      // instead of 24 two- or four-byte stores per lane of the two cell
+      // waves): gates by every thread, c by threads 0-127, h by 128-191.
+      // The next step's gather barrier comes before the LDS is rewritten.
+      {
+        const int rl = tid >> 4, q = (tid >> 2) & 3, c = tid & 3;
+        const int row = rowbase + rl;
+        if (row < rend)
+          *(uint4*)(a.G + ((int64_t)t * B + row) * 8 * H + (int64_t)d * 4 * H + (int64_t)q * H + u0 + c * 8) =
+              *(const uint4*)&sG[(rl * 4 + q) * 32 + c * 8];
+      }
+      if (tid < 128) {
+        const int rl = tid >> 3, c = tid & 7;
+        const int row = rowbase + rl;
+        if (row < rend)
+          *(float4*)(a.C + ((int64_t)t * B + row) * 2 * H + (int64_t)d * H + u0 + c * 4) =
+              *(const float4*)&sC[rl * 32 + c * 4];
+      } else if (tid < 192) {
+        const int rl = (tid - 128) >> 2, c = (tid - 128) & 3;
+        const int row = rowbase + rl;
+        if (row < rend)
+          *(uint4*)(a.Y + ((int64_t)t * B + row) * 2 * H + (int64_t)d * H + u0 + c * 8) =
+              *(const uint4*)&sY[rl * 32 + c * 8];
+      }
+    }
   }
 }
 
@@ -742,8 +786,9 @@ size_t persist_lds_bytes(int H, bool backward, int MB) {
     return MB == 1 ? std::max(run, (size_t)128 * 1024) : run;
   }
   // MB == 1 keeps W_hh in registers (staged through 128 KB of LDS at the
-  // start): reduction buffer and gathered h after that
-  if (MB == 1) return std::max((size_t)8 * 64 * 16 + (size_t)(H / 8) * 17 * 16, (size_t)128 * 1024);
+  // start): reduction buffer, gathered h and the step's staged c/h/gates
+  // (7 KB) after that
+  if (MB == 1) return std::max((size_t)8 * 64 * 16 + (size_t)(H / 8) * 17 * 16 + 7 * 1024, (size_t)128 * 1024);
   return (size_t)(H / 8) * (128 + 1) * 16 + 8 * 64 * 16;
 }
 
