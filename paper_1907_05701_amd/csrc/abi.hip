@@ -151,6 +151,8 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   L.DZT = h; h = align256(h + (size_t)M * P * es);
   L.HCSP = h; h = align256(h + (size_t)COLSUM_MAX_CHUNKS * std::max<int64_t>(L.Kp, P) * 4);
   size_t hsk = 0;
+  L.sp_z = es == 2 ? plan_splits(M, P, 2 * H, BMt, BNt, BKt, 1, true, true) : 1;
+  if (L.sp_z > 1) hsk = std::max(hsk, (size_t)L.sp_z * M * P * 4);
   L.sp_dz = plan_splits(M, P, d->K, BMt, BNt, BKt, 1, es == 2, true);
   hsk = std::max(hsk, (size_t)L.sp_dz * M * P * 4);  // dz always goes through partials
   L.sp_dWs = plan_splits(d->K, P, M, BMt, BNt, BKt, 1, es == 2, true);

@@ -192,9 +192,18 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
   float* csp = (float*)(hws + lo.HCSP);
   float* part = (float*)(hws + lo.HSKP);
 
-  // z = y W_l^T + b_l
-  gemm_launch<T, true, true, V, V>("gemm_z", s, opnd(ytop, H2, H2, M), opnd(W + lo.Wl, H2, H2, P), M,
-                                   P, H2, 1, 1, epi_store<T>(Z, P, M, P, 0, 0, theta + lo.bl));
+  // z = y W_l^T + b_l.  bf16: split over k (only P/128 column blocks), the
+  // fixed-order reduction adds b_l and writes the bf16 z
+  if (std::is_same<T, bf16>::value && lo.sp_z > 1) {
+    gemm_launch<T, true, true, V, V>("gemm_z", s, opnd(ytop, H2, H2, M), opnd(W + lo.Wl, H2, H2, P), M, P, H2, 1,
+                                     lo.sp_z, epi_store<float>(part, P, M, P, (int64_t)lo.sp_z * M * P, M * P));
+    BLSTM_LAUNCH("splitk_reduce", splitk_reduce4_kernel<T>, dim3((unsigned)M, (unsigned)cdiv(P, 256), 1), dim3(64), 0,
+                 s, (const float*)part, lo.sp_z, M, (int64_t)P, (float*)nullptr, (int64_t)P, (int64_t)0, Z, (int64_t)P,
+                 theta + lo.bl);
+  } else {
+    gemm_launch<T, true, true, V, V>("gemm_z", s, opnd(ytop, H2, H2, M), opnd(W + lo.Wl, H2, H2, P), M,
+                                     P, H2, 1, 1, epi_store<T>(Z, P, M, P, 0, 0, theta + lo.bl));
+  }
   // s = z W_s^T + b_s
   gemm_launch<T, true, true, V, V>("gemm_logits", s, opnd(Z, P, P, M), opnd(W + lo.Ws, P, P, K), M,
                                    K, P, 1, 1, epi_store<T>(S, Kp, M, K, 0, 0, theta + lo.bs));

@@ -408,12 +408,18 @@ static PersistArgs persist_args(const Layout& lo, const bf16* W, char* ws, int l
 template <typename T>
 static int fwd_impl(const Layout& lo, const float* theta, const T* W, const float* x, char* ws,
                     T* ytop, hipStream_t s) {
-  bool xch_cleared = false;   // exchange words cleared once per call (persist_clear)
-  // the recurrence status covers this forward call and the backward call after it
-  if (persist_status_clear((int*)(ws + lo.SYNC), s) != hipSuccess) return blstm_check_launch("blstm_fwd");
   constexpr int V = VecW<T>::v;
   const int64_t M = lo.M;
   const int H = lo.H, B = lo.B;
+  bool xch_cleared = false;   // exchange words cleared once per call (persist_clear)
+  // the recurrence status covers this forward call and the backward call
+  // after it: reset by the persistent path's exchange clear, else here
+  const bool persist = use_persistent<T>(H, lo.T, false, s);
+  bool status_cleared = false;
+  if (!persist) {
+    if (persist_status_clear((int*)(ws + lo.SYNC), s) != hipSuccess) return blstm_check_launch("blstm_fwd");
+    status_cleared = true;
+  }
   T* X0 = (T*)(ws + lo.X0);
   T* GX = (T*)(ws + lo.GX);
   bf16* WP0 = lo.WP0_bytes ? (bf16*)(ws + lo.WP0) : nullptr;
@@ -442,10 +448,18 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
       gemm_launch<T, true, true, V, V>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
     else
       gemm_launch<T, true, true, V, 4>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
-    if (use_persistent<T>(H, lo.T, false, s)) {
+    if (persist) {
       PersistArgs pa = persist_args(lo, (const bf16*)W, ws, l);
       pa.Y = (bf16*)Yl; pa.Gx = (const bf16*)GX; pa.C = Cl; pa.G = (bf16*)Gl;
-      if (!xch_cleared) xch_cleared = persist_clear(false, pa, s) == hipSuccess;
+      if (!xch_cleared) {
+        xch_cleared = persist_clear(false, pa, s) == hipSuccess;
+        status_cleared = status_cleared || xch_cleared;
+      }
+      if (!status_cleared) {
+        (void)hipGetLastError();
+        if (persist_status_clear((int*)(ws + lo.SYNC), s) != hipSuccess) return blstm_check_launch("blstm_fwd");
+        status_cleared = true;
+      }
       if (xch_cleared && persist_layer(false, pa, s) == hipSuccess) continue;
       (void)hipGetLastError();   // cooperative launch refused: take the per-step path
     }

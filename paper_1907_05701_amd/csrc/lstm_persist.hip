@@ -896,12 +896,14 @@ bool persist_bwd_needs_wt(int H, int B) {
 hipError_t persist_clear(bool backward, const PersistArgs& a, hipStream_t s) {
   int MB, chunk;
   if (!persist_plan(backward, a.H, a.B, &MB, &chunk)) return hipErrorInvalidValue;
-  // both exchange slots start without any valid step number
+  // both exchange slots start without any valid step number; the forward's
+  // clear also resets the status word (it covers the forward call and the
+  // backward call after it)
   const int64_t words = backward ? (int64_t)2 * 2 * ((chunk + 1) / 2) * (a.H / PU) * a.H
                                  : (int64_t)2 * 2 * chunk * (a.H / 2);
   const int64_t n16 = words / 2;
   hipLaunchKernelGGL(clear_exchange_kernel, dim3((unsigned)std::min<int64_t>(cdiv(n16, 256), 2048)), dim3(256), 0,
-                     s, (uint4*)a.X, n16, nullptr);
+                     s, (uint4*)a.X, n16, backward ? nullptr : a.status);
   return hipGetLastError();
 }
 

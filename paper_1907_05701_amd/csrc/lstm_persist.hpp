@@ -45,10 +45,11 @@ bool persist_supported(int H, int T);
 // Whether the persistent BPTT of a layer reads W_hh^T (PersistArgs::WT): only
 // when its workgroups take more than one 16-row block (W_hh slice in LDS).
 bool persist_bwd_needs_wt(int H, int B);
-// Clears the exchange words; once per forward or backward call, before its
-// first persist_layer.
+// Clears the exchange words (and, for the forward, the status word); once
+// per forward or backward call, before its first persist_layer.
 hipError_t persist_clear(bool backward, const PersistArgs& a, hipStream_t s);
-// Clears the status word (once per forward call, whatever path it takes).
+// Clears the status word alone (a forward call that does not take the
+// persistent path, or whose exchange clear failed).
 hipError_t persist_status_clear(int* status, hipStream_t s);
 // Runs every step of one layer, both directions; hipSuccess or the error of
 // the launch that failed.  Layers of one call need distinct tags.

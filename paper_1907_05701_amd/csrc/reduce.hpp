@@ -87,11 +87,12 @@ static inline void colsum(const char* name, hipStream_t s, const T* X, int64_t M
 
 // The same reduction, 4 adjacent columns per thread: block (m, column block
 // of 256, batch), 64 threads.  Needs N, ld, ldc multiples of 4 and aligned
-// destinations.
+// destinations.  Optional: a per-column bias added to the sum, and no
+// float32 destination (dst null) when only the low-precision copy is wanted.
 template <typename TC>
 __global__ __launch_bounds__(64) void splitk_reduce4_kernel(const float* __restrict__ part, int splits, int64_t M,
                                                             int64_t N, float* dst, int64_t ld, int64_t dst_zstride,
-                                                            TC* dstc, int64_t ldc) {
+                                                            TC* dstc, int64_t ldc, const float* __restrict__ bias) {
   const int64_t m = blockIdx.x, n = ((int64_t)blockIdx.y * 64 + threadIdx.x) * 4;
   const int z = blockIdx.z;
   if (n >= N) return;
@@ -101,7 +102,8 @@ __global__ __launch_bounds__(64) void splitk_reduce4_kernel(const float* __restr
     const float4 v = *(const float4*)(p + (int64_t)k * M * N);
     acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
   }
-  *(float4*)(dst + z * dst_zstride + m * ld + n) = acc;
+  if (bias) { acc.x += bias[n]; acc.y += bias[n + 1]; acc.z += bias[n + 2]; acc.w += bias[n + 3]; }
+  if (dst) *(float4*)(dst + z * dst_zstride + m * ld + n) = acc;
   if (dstc) {
     TC* c = dstc + m * ldc + n;
     c[0] = from_f32<TC>(acc.x); c[1] = from_f32<TC>(acc.y); c[2] = from_f32<TC>(acc.z); c[3] = from_f32<TC>(acc.w);
@@ -125,7 +127,7 @@ static inline void gemm_f32(const char* name, hipStream_t s, const Opnd& A, cons
   if (N % 4 == 0 && ld % 4 == 0 && dst_zstride % 4 == 0 && ((uintptr_t)dst & 15) == 0 &&
       (!dstc || (ldc % 4 == 0 && ((uintptr_t)dstc & 7) == 0))) {
     BLSTM_LAUNCH("splitk_reduce", splitk_reduce4_kernel<T>, dim3((unsigned)M, (unsigned)cdiv(N, 256), batches),
-                 dim3(64), 0, s, part, splits, M, N, dst, ld, dst_zstride, dstc, ldc);
+                 dim3(64), 0, s, part, splits, M, N, dst, ld, dst_zstride, dstc, ldc, (const float*)nullptr);
     return;
   }
   const int64_t total = (int64_t)batches * M * N;
