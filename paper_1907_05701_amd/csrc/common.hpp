@@ -89,7 +89,7 @@ struct Layout {
   size_t head_bytes;
   size_t ytop_bytes;
   // split-K factors of the weight/input-gradient GEMMs (1 = direct store)
-  int sp_dWih[MAX_LAYERS], sp_dWhh, sp_dX[MAX_LAYERS], sp_z, sp_dz, sp_dWs, sp_dWl, sp_dy;
+  int sp_dWih[MAX_LAYERS], sp_dWhh[MAX_LAYERS], sp_dX[MAX_LAYERS], sp_z, sp_dz, sp_dWs, sp_dWl, sp_dy;
   size_t skp_hh[MAX_LAYERS], skp_dx[MAX_LAYERS];   // byte offsets of the dW_hh / dX partials in SKP
   int layer_in(int l) const { return l == 0 ? D : 2 * H; }
   int layer_in_pitch(int l) const { return l == 0 ? Dp0 : 2 * H; }

@@ -631,7 +631,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
         g[0] = F32Job{opnd(DAT, M, (int)M, 4 * H, 4 * H * M), opnd(Xl, Dpl, Dpl, M), 4 * H, Dl, M, 2,
                       lo.sp_dWih[l], grad + lo.Wih[l][0], Dl, lo.Wih[l][1] - lo.Wih[l][0], part_ih};
         g[1] = F32Job{opnd(DAT + B, M, (int)Kr, 4 * H, 4 * H * M - B), opnd(Yl, 2 * H, H, Kr, (int64_t)B * 2 * H + H),
-                      4 * H, H, Kr, 2, lo.sp_dWhh, grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part_hh};
+                      4 * H, H, Kr, 2, lo.sp_dWhh[l], grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part_hh};
         int ng = 2;
         if (!side && l > 0)
           g[ng++] = F32Job{opnd(DA, 8 * H, 8 * H, M), Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0, part_dx};
@@ -662,7 +662,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       // forward direction pairing t with t-1 and the reverse direction t with t+1
       const Opnd Ad = opnd(DA + (int64_t)B * 8 * H, 8 * H, 4 * H, Kr, 4 * H - (int64_t)B * 8 * H);
       const Opnd Bh = opnd(Yl, 2 * H, H, Kr, (int64_t)B * 2 * H + H);
-      gemm_f32<T, false, false, V, V>("gemm_dwhh", s, Ad, Bh, 4 * H, H, Kr, 2, lo.sp_dWhh,
+      gemm_f32<T, false, false, V, V>("gemm_dwhh", s, Ad, Bh, 4 * H, H, Kr, 2, lo.sp_dWhh[l],
                                       grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part_hh);
     }
     // db_ih = db_hh = sum over frames of da (unless the reduction above did it)
