@@ -122,11 +122,11 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   const int BKt = es == 2 ? GemmCfg<bf16>::BK : GemmCfg<float>::BK;
   // each layer's three products own disjoint partial regions (dW_ih, dW_hh,
   // dX), so that they can run as one grouped launch.  bf16, measured on
-  // MI355X at the learner-step shapes: where dX is in the group it splits to
-  // fill one round of two blocks per CU by itself and dW_hh is not split (its
-  // partial pass costs more than the parallelism gains: 1.207 -> 1.253 M
-  // frames/s); layer 0's group (no dX) keeps both weight products at half a
-  // round each.
+  // MI355X at the learner-step shapes: dX splits to fill one round of two
+  // blocks per CU by itself and dW_hh is not split (its partial pass costs
+  // more than the parallelism gains: 1.207 -> 1.253 M frames/s); dW_ih keeps
+  // half a round.  A sweep of the other products' splits and of the tile
+  // order's row grouping found the defaults at the optimum.
   size_t skp = 0;
   const bool lp = es == 2;
   for (int l = 0; l < d->L; ++l) {
@@ -134,7 +134,7 @@ int make_layout(const blstm_dims* d, Layout* lo) {
     const bool with_dx = l > 0;
     L.sp_dWih[l] = plan_splits(4 * H, Dl, M, BMt, BNt, BKt, 2, lp, false);
     const size_t ih_bytes = L.sp_dWih[l] > 1 ? align256((size_t)L.sp_dWih[l] * 2 * 4 * H * Dl * 4) : 0;
-    L.sp_dWhh[l] = lp && with_dx ? 1 : plan_splits(4 * H, H, (int64_t)(d->T - 1) * d->B, BMt, BNt, BKt, 2, lp, false);
+    L.sp_dWhh[l] = lp ? 1 : plan_splits(4 * H, H, (int64_t)(d->T - 1) * d->B, BMt, BNt, BKt, 2, lp, false);
     const size_t hh_bytes = L.sp_dWhh[l] > 1 ? align256((size_t)L.sp_dWhh[l] * 2 * 4 * H * H * 4) : 0;
     L.sp_dX[l] = with_dx ? plan_splits(M, Dl, 8 * H, BMt, BNt, BKt, 1, lp, lp) : 1;
     const size_t dx_bytes = L.sp_dX[l] > 1 ? align256((size_t)L.sp_dX[l] * M * Dl * 4) : 0;
