@@ -119,10 +119,10 @@ static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 static bool aligned8(const void* p) { return ((uintptr_t)p & 7) == 0; }
 
 static unsigned stream_grid(int64_t n) {
-  // enough waves to keep every CU's memory pipeline full, bounded so that
-  // each thread handles a few vectors
+  // one 4-element vector per thread up to 64 Ki workgroups (measured on
+  // MI355X at n = 43 M: 5.98 TB/s with a 4 Ki cap, 6.14 TB/s without it)
   const int64_t blocks = cdiv(cdiv(n, 4), 256);
-  return (unsigned)std::max<int64_t>(1, std::min<int64_t>(blocks, 256 * 16));
+  return (unsigned)std::max<int64_t>(1, std::min<int64_t>(blocks, 65536));
 }
 
 static int fill_grads(const float* const* grads, int32_t R, GradPtrs* g, bool* all16) {
