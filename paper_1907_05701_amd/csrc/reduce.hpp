@@ -74,7 +74,9 @@ static inline void colsum(const char* name, hipStream_t s, const T* X, int64_t M
   constexpr int VEC = 16 / (int)sizeof(T);
   const bool vec = N % VEC == 0 && ld % VEC == 0 && ((uintptr_t)X & 15) == 0;
   const int64_t xb = cdiv(N, 256 * (vec ? VEC : 1));
-  int chunks = (int)std::min<int64_t>(COLSUM_MAX_CHUNKS, std::max<int64_t>(16, cdiv(2048, xb)));
+  // about one workgroup per CU (measured at the logits' 32000 columns: 16
+  // row ranges, fewer partials to combine, slightly ahead of 128)
+  int chunks = (int)std::min<int64_t>(COLSUM_MAX_CHUNKS, std::max<int64_t>(16, cdiv(256, xb)));
   chunks = (int)std::max<int64_t>(1, std::min<int64_t>(chunks, M));
   if (vec)
     BLSTM_LAUNCH(name, (colsum_partial_kernel<T, VEC>), dim3((unsigned)xb, (unsigned)chunks), dim3(256), 0, s, X,
