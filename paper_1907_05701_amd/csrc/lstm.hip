@@ -58,7 +58,7 @@ struct RecFwdArgs {
   const T* Whh1;     // W_hh of the reverse direction
   const T* Gx;       // input projection incl. both biases [M][8H]
   float* C;          // cell states [M][2H]
-  T* G;              // saved activated gates i, f, g, o [M][8H]
+  T* G;              // saved activated gates [M][2][H][4] (direction, unit, gate i/f/g/o)
   int Tn, B, H, tau;
 };
 
@@ -149,11 +149,11 @@ __global__ __launch_bounds__(256) void lstm_rec_fwd_step(const RecFwdArgs<T> a) 
     const float h = og * tanhf_(c);
     a.C[row * 2 * H + (int64_t)d * H + u] = c;
     a.Y[row * 2 * H + (int64_t)d * H + u] = from_f32<T>(h);
-    T* gs = a.G + row * 8 * H + (int64_t)d * 4 * H + u;
+    T* gs = a.G + row * 8 * H + (int64_t)d * 4 * H + (int64_t)u * 4;   // the unit's four gates together
     gs[0] = from_f32<T>(ig);
-    gs[H] = from_f32<T>(fg);
-    gs[2 * H] = from_f32<T>(gg);
-    gs[3 * H] = from_f32<T>(og);
+    gs[1] = from_f32<T>(fg);
+    gs[2] = from_f32<T>(gg);
+    gs[3] = from_f32<T>(og);
   }
 }
 
@@ -167,7 +167,7 @@ struct RecBwdArgs {
   const T* WT0;      // W_hh^T of the forward direction [H][4H]
   const T* WT1;      // W_hh^T of the reverse direction
   const float* DY;   // gradient reaching the layer output [M][2H]
-  const T* G;        // saved gates [M][8H]
+  const T* G;        // saved gates [M][2][H][4]
   const float* C;    // saved cell states [M][2H]
   float* DC;         // carried cell gradient [2][B][H]
   T* DAT;            // optional: da also written frame-contiguous, [8H][M]
@@ -232,9 +232,9 @@ __global__ __launch_bounds__(256) void lstm_rec_bwd_step(const RecBwdArgs<T> a) 
       b = b < B ? b : 0;
       const int64_t row = (int64_t)t * B + b;
       dy[r] = a.DY[row * 2 * H + (int64_t)d * H + u];
-      const T* gs = a.G + row * 8 * H + (int64_t)d * 4 * H + u;
+      const T* gs = a.G + row * 8 * H + (int64_t)d * 4 * H + (int64_t)u * 4;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) graw[r][g] = gs[g * H];
+      for (int g = 0; g < 4; ++g) graw[r][g] = gs[g];
       cc[r] = a.C[row * 2 * H + (int64_t)d * H + u];
       cpv[r] = (tp >= 0 && tp < Tn) ? a.C[((int64_t)tp * B + b) * 2 * H + (int64_t)d * H + u] : 0.f;
       dcn[r] = a.tau > 0 ? a.DC[((int64_t)d * B + b) * H + u] : 0.f;

@@ -155,7 +155,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   }
   f32x4* red = (f32x4*)(lds + (KSPLIT ? (size_t)0 : (size_t)kcn * LDN * 8));
   bf16* hl = (bf16*)(red + 8 * 64);   // MB == 1: gathered h [H/8][16 + 1][8]
-  // MB == 1: a step's c [16][32] (float), h [16][32] and gates [16][4][32]
+  // MB == 1: a step's c [16][32] (float), h [16][32] and gates [16][32][4]
   // (bf16) of the own units, staged for 16-byte stores
   float* sC = (float*)(hl + (size_t)(H / 8) * 17 * 8);
   bf16* sY = (bf16*)(sC + 16 * 32);
@@ -371,8 +371,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
           const int rl = (lane >> 4) * 4 + r;
           sC[rl * 32 + ul] = creg[0][r];
           sY[rl * 32 + ul] = (bf16)hv[0][r];
+          bf16x4 g4;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) sG[(rl * 4 + q) * 32 + ul] = (bf16)gv[0][r][q];
+          for (int q = 0; q < 4; ++q) g4[q] = (bf16)gv[0][r][q];
+          *(bf16x4*)&sG[(rl * 32 + ul) * 4] = g4;
         }
       } else {
 #pragma unroll
@@ -384,9 +386,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             const int64_t fr = (int64_t)t * B + row;
             a.C[fr * 2 * H + (int64_t)d * H + unit] = creg[m][r];
             a.Y[fr * 2 * H + (int64_t)d * H + unit] = (bf16)hv[m][r];
-            bf16* gs = a.G + fr * 8 * H + (int64_t)d * 4 * H + unit;
+            bf16* gs = a.G + fr * 8 * H + (int64_t)d * 4 * H + (int64_t)unit * 4;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) gs[q * H] = (bf16)gv[m][r][q];
+            for (int q = 0; q < 4; ++q) gs[q] = (bf16)gv[m][r][q];
           }
       }
     }
@@ -395,14 +397,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     if constexpr (KSPLIT) {
       // c, h and the gates of the step in 16-byte pieces (448 per step
       // instead of 24 two- or four-byte stores per lane of the two cell
-      // waves): gates by every thread, c by threads 0-127, h by 128-191.
-      // The next step's gather barrier comes before the LDS is rewritten.
+      // waves): gates by every thread (a row's 32 units x 4 gates are 256
+      // contiguous bytes), c by threads 0-127, h by 128-191.  The next step's
+      // gather barrier comes before the LDS is rewritten.
       {
-        const int rl = tid >> 4, q = (tid >> 2) & 3, c = tid & 3;
+        const int rl = tid >> 4, c = tid & 15;
         const int row = rowbase + rl;
         if (row < rend)
-          *(uint4*)(a.G + ((int64_t)t * B + row) * 8 * H + (int64_t)d * 4 * H + (int64_t)q * H + u0 + c * 8) =
-              *(const uint4*)&sG[(rl * 4 + q) * 32 + c * 8];
+          *(uint4*)(a.G + ((int64_t)t * B + row) * 8 * H + (int64_t)d * 4 * H + (int64_t)u0 * 4 + c * 8) =
+              *(const uint4*)&sG[rl * 128 + c * 8];
       }
       if (tid < 128) {
         const int rl = tid >> 3, c = tid & 7;
@@ -566,9 +569,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       const int unit = u0 + cu;
       dyn[i] = a.DY[fr * 2 * H + (int64_t)d * H + unit];
       cpn[i] = hp ? a.C[((int64_t)tp_ * B + row) * 2 * H + (int64_t)d * H + unit] : 0.f;
-      const bf16* gs = a.G + fr * 8 * H + (int64_t)d * 4 * H + unit;
+      // the unit's four gates are adjacent: one 8-byte load
+      const bf16x4 g4 = *(const bf16x4*)(a.G + fr * 8 * H + (int64_t)d * 4 * H + (int64_t)unit * 4);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) gtn[i][q] = gs[q * H];
+      for (int q = 0; q < 4; ++q) gtn[i][q] = g4[q];
     }
   };
   {
