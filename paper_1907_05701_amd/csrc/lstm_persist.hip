@@ -20,7 +20,8 @@
 // Step-to-step exchange without barriers or cache maintenance.  The values
 // one member needs from the others (h, or partial dh) are published in an
 // exchange buffer as 8-byte words holding two bf16 values and a step number
-// (launch tag and step + 1), written and read with agent-scope relaxed atomic
+// (launch tag and step + 1; the forward at one 16-row block per workgroup
+// packs four values and a 4-bit tag instead, see h4_tag), written and read with agent-scope relaxed atomic
 // stores and loads.  Atomic accesses to one location are coherent across the
 // whole GPU, so a reader that sees the expected step number in a word also
 // sees that word's payload; readers poll the words they need (bounded; the
@@ -55,9 +56,35 @@ __device__ __forceinline__ void ll_store(uint64_t* p, uint32_t payload, uint32_t
   __hip_atomic_store(p, ((uint64_t)flag << 32) | payload, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+__device__ __forceinline__ void ll_store64(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // the value of lane l ^ 1 (a DPP quad permutation, no LDS round trip)
 __device__ __forceinline__ float lane_xor1(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+}
+
+// the value of lane l ^ 2
+__device__ __forceinline__ uint32_t lane_xor2(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
+}
+
+// Forward words at one 16-row block per workgroup: four bf16 h of one row
+// (units 4i .. 4i+3, the first in the low half-word).  |h| = |o tanh(c)| <= 1,
+// and a bf16 below 2 in magnitude has a zero top exponent bit (bit 14), so
+// the four such bits carry a 4-bit tag: bit 0 always set (a cleared word
+// never matches), bit 1 = bit 1 of the step number (a slot alternates
+// between steps n and n - 2), bits 2-3 = the launch's sequence number in
+// its call modulo 4 (a word can be left by one of the two launches before).
+// Readers clear the four bits, so the exchanged values are exactly the bf16
+// of h; a non-finite h (bit 14 set) reaches the other members clipped, while
+// the layer output keeps it.
+#define H4_TAG_BITS 0x4000400040004000ull
+__device__ __forceinline__ uint64_t h4_tag(uint32_t seq, int n) {
+  const uint32_t t = 1u | (((uint32_t)n >> 1 & 1u) << 1) | ((seq & 3u) << 2);
+  return ((uint64_t)(t & 1u) << 14) | ((uint64_t)(t >> 1 & 1u) << 30) | ((uint64_t)(t >> 2 & 1u) << 46) |
+         ((uint64_t)(t >> 3 & 1u) << 62);
 }
 
 // two bf16 values in one dword, `lo` in the low half
@@ -203,7 +230,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
     __syncthreads();   // the reduction buffer and gathered h reuse this LDS
   }
-  const int wpr = H / 2;                        // exchange words per row
+  const int wpr = KSPLIT ? H / 4 : H / 2;       // exchange words per row
+  constexpr int NJ4 = H_MAX_MEMBERS * PU / 64;  // MB == 1: words per thread and row (16 threads)
   const int64_t slot_stride = (int64_t)2 * a.rows * wpr;
 
   float creg[MBW][4];
@@ -251,15 +279,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       const int tr = tid >> 4, tw = tid & 15;
       const int row = rowbase + tr;
       const bool rok = row < rend;
-      const int nj = H / 32;
       const uint64_t* src = a.X + ((tau - 1) & 1) * slot_stride + ((int64_t)d * a.rows + (rok ? row - a.b0 : 0)) * wpr + tw;
-      uint64_t wv[16];
+      const uint64_t want = h4_tag(a.seq, tau);
+      uint64_t wv[NJ4];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) wv[j] = (rok && j < nj) ? ll_load(src + 16 * j) : ((uint64_t)(fb | (uint32_t)tau) << 32);
+      for (int j = 0; j < NJ4; ++j) wv[j] = (rok && tw + 16 * j < wpr) ? ll_load(src + 16 * j) : want;
       for (unsigned it = 0;; ++it) {
         bool bad = false;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) bad |= (uint32_t)(wv[j] >> 32)  != (fb | (uint32_t)tau);
+        for (int j = 0; j < NJ4; ++j) bad |= (wv[j] & H4_TAG_BITS) != want;
         if (!bad) break;
         if (it > SPIN_LIMIT ||
             ((it & 63) == 63 && __hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
@@ -268,14 +296,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         }
         __builtin_amdgcn_s_sleep(1);
 #pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if ((uint32_t)(wv[j] >> 32)  != (fb | (uint32_t)tau)) wv[j] = ll_load(src + 16 * j);
+        for (int j = 0; j < NJ4; ++j)
+          if ((wv[j] & H4_TAG_BITS) != want) wv[j] = ll_load(src + 16 * j);
       }
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        if (j >= nj) break;
-        const int k = 2 * (tw + 16 * j);   // units k, k+1
-        *(uint32_t*)&hl[((k >> 3) * 17 + tr) * 8 + (k & 7)] = rok ? (uint32_t)wv[j] : 0u;
+      for (int j = 0; j < NJ4; ++j) {
+        if (tw + 16 * j >= wpr) break;
+        const int k = 4 * (tw + 16 * j);   // units k .. k+3
+        *(uint64_t*)&hl[((k >> 3) * 17 + tr) * 8 + (k & 7)] = rok ? (wv[j] & ~H4_TAG_BITS) : 0ull;
       }
       __syncthreads();
       // A fragments of the half (W is in registers), then the products
@@ -359,9 +387,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         for (int r = 0; r < 4; ++r) {
           const int row = rowbase + (mb0 + m) * 16 + (lane >> 4) * 4 + r;
           const float h_next_unit = lane_xor1(hv[m][r]);   // lanes of one row, units u and u^1
-          if (row < rend && (lane & 1) == 0)
+          if constexpr (KSPLIT) {
+            // lane 4i stores units 4i .. 4i+3 (the pairs of lanes 4i and 4i+2)
+            const uint32_t p2 = pack_bf16x2(hv[m][r], h_next_unit);
+            const uint32_t p4 = lane_xor2(p2);
+            if (row < rend && (lane & 3) == 0)
+              ll_store64(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 4,
+                         ((((uint64_t)p4 << 32) | p2) & ~H4_TAG_BITS) | h4_tag(a.seq, tau + 1));
+          } else if (row < rend && (lane & 1) == 0) {
             ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 2, pack_bf16x2(hv[m][r], h_next_unit),
                      fb | (uint32_t)(tau + 1));
+          }
         }
       if constexpr (KSPLIT) {
         // into LDS; the whole workgroup writes them out after the barrier
@@ -927,6 +963,7 @@ hipError_t persist_layer(bool backward, PersistArgs a, hipStream_t s) {
     // step numbers of this launch: tag = layer * 256 + chunk above the 8-bit
     // step, so no word left by an earlier launch of the same call matches
     c.tag = a.tag * 256 + (uint32_t)(b0 / chunk);
+    c.seq = a.tag * (uint32_t)cdiv(a.B, chunk) + (uint32_t)(b0 / chunk);
     hipError_t e;
     if (backward)
       e = MB == 1 ? launch_one<1, true>(c, s) : MB == 2 ? launch_one<2, true>(c, s) : launch_one<4, true>(c, s);

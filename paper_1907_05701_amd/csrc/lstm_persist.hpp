@@ -23,6 +23,7 @@ struct PersistArgs {
                       // earlier layers of the same call never match)
   int Tn, B, H;
   int b0, rows, NS;   // batch chunk handled by one launch (filled in by persist_layer)
+  uint32_t seq;       // the launch's position among the call's launches (filled in by persist_layer)
 };
 
 // At most this many batch slices of 16*MB rows per launch (MB <= 8), so one
