@@ -20,8 +20,9 @@
 // Step-to-step exchange without barriers or cache maintenance.  The values
 // one member needs from the others (h, or partial dh) are published in an
 // exchange buffer as 8-byte words holding two bf16 values and a step number
-// (launch tag and step + 1; the forward at one 16-row block per workgroup
-// packs four values and a 4-bit tag instead, see h4_tag), written and read with agent-scope relaxed atomic
+// (launch tag and step + 1; at one 16-row block per workgroup, which means
+// one launch per layer, words pack four values and a 4-bit tag instead, see
+// h4_tag), written and read with agent-scope relaxed atomic
 // stores and loads.  Atomic accesses to one location are coherent across the
 // whole GPU, so a reader that sees the expected step number in a word also
 // sees that word's payload; readers poll the words they need (bounded; the
@@ -81,6 +82,21 @@ __device__ __forceinline__ uint32_t lane_xor2(uint32_t v) {
 // of h; a non-finite h (bit 14 set) reaches the other members clipped, while
 // the layer output keeps it.
 #define H4_TAG_BITS 0x4000400040004000ull
+//
+// BPTT words at one 16-row block per workgroup: four partial sums (rows 4i
+// .. 4i+3 of one unit) in a 15-bit form that frees the same bits: the bf16
+// of x * 2^-64 (so bf16 exponents 65 .. 190, i.e. 2^-62 <= |x| < 2^65, keep
+// bit 14 clear and the 8-bit significand of the bf16 of x), magnitudes from
+// 2^65 and non-finite values saturated to 2^64; tiny values become bf16
+// subnormals.  Decoding multiplies by 2^64 (exact).
+__device__ __forceinline__ uint32_t p15_encode(float x) {
+  uint32_t b = __builtin_bit_cast(uint16_t, (bf16)(x * 0x1p-64f));
+  if (b & 0x4000u) b = (b & 0x8000u) | 0x3F80u;
+  return b;
+}
+__device__ __forceinline__ float p15_decode(uint32_t c) {
+  return __builtin_bit_cast(float, (c & 0xBFFFu) << 16) * 0x1p64f;
+}
 __device__ __forceinline__ uint64_t h4_tag(uint32_t seq, int n) {
   const uint32_t t = 1u | (((uint32_t)n >> 1 & 1u) << 1) | ((seq & 3u) << 2);
   return ((uint64_t)(t & 1u) << 14) | ((uint64_t)(t >> 1 & 1u) << 30) | ((uint64_t)(t >> 2 & 1u) << 46) |
@@ -571,7 +587,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int rend = a.b0 + a.rows;
   const int rowbase = a.b0 + s * R;
   const int rpairs = (a.rows + 1) / 2;             // row pairs of this launch
-  const int64_t slot_stride = (int64_t)2 * rpairs * NM * H;
+  const int rquads = (a.rows + 3) / 4;             // row quads (MB == 1 words)
+  const int64_t slot_stride = (int64_t)2 * (WREG ? rquads : rpairs) * NM * H;
   // cell items: unit cu = tid % 32, rows tid/32 + 8*i
   const int cu = tid & 31;
   float dcreg[ITEMS];
@@ -627,9 +644,47 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     float dy[ITEMS], cp[ITEMS];
     bf16 gt[ITEMS][4];
 
-    // gather dh_rec for the own units: items (row pair, unit), unit = tid % 32;
-    // the 32 threads of a row pair read 32 adjacent words (256 bytes) per member
-    if (tau > 0) {
+    // gather dh_rec for the own units.  MB == 1: items (row quad, unit,
+    // member parity), unit = tid % 32, quad (tid / 32) % 4; each thread sums
+    // the members of its parity in order into its half of the LDS sums.
+    // MB > 1: items (row pair, unit); the 32 threads of a row pair read 32
+    // adjacent words (256 bytes) per member.
+    if (WREG && tau > 0) {
+      const uint64_t* xs = a.X + ((tau - 1) & 1) * slot_stride;
+      const int qd = (tid >> 5) & 3, mh = tid >> 7;
+      float sum[4] = {0.f, 0.f, 0.f, 0.f};
+      if (rowbase + 4 * qd < rend) {
+        const uint64_t want = h4_tag(a.seq, tau);
+        const uint64_t* src = xs + ((int64_t)d * rquads + (rowbase - a.b0) / 4 + qd) * NM * H + u0 + cu;
+        constexpr int KM = H_MAX_MEMBERS / 2;
+        uint64_t wv[KM];
+#pragma unroll
+        for (int k = 0; k < KM; ++k) wv[k] = 2 * k + mh < NM ? ll_load(src + (int64_t)(2 * k + mh) * H) : want;
+        for (unsigned it = 0;; ++it) {
+          bool bad = false;
+#pragma unroll
+          for (int k = 0; k < KM; ++k) bad |= (wv[k] & H4_TAG_BITS) != want;
+          if (!bad) break;
+          if (it > SPIN_LIMIT ||
+              ((it & 63) == 63 && __hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
+            __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+          for (int k = 0; k < KM; ++k)
+            if ((wv[k] & H4_TAG_BITS) != want) wv[k] = ll_load(src + (int64_t)(2 * k + mh) * H);
+        }
+#pragma unroll
+        for (int k = 0; k < KM; ++k) {
+          if (2 * k + mh >= NM) break;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sum[r] += p15_decode((uint32_t)(wv[k] >> (16 * r)) & 0xffffu);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dhl[mh * R * PU + (4 * qd + r) * PU + cu] = sum[r];
+    } else if (tau > 0) {
       const uint64_t* xs = a.X + ((tau - 1) & 1) * slot_stride;
 #pragma unroll
       for (int i = 0; i < MB; ++i) {
@@ -668,7 +723,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         dhl[(2 * rp + 1) * PU + cu] = hi;
       }
     } else {
-      for (int i = tid; i < R * PU; i += 256) dhl[i] = 0.f;
+      for (int i = tid; i < (WREG ? 2 : 1) * R * PU; i += 256) dhl[i] = 0.f;
     }
     __syncthreads();
 #pragma unroll
@@ -687,7 +742,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       const int r = (tid >> 5) + 8 * i;
       const int row = rowbase + r;
       const float ig = (float)gt[i][0], fg = (float)gt[i][1], gg = (float)gt[i][2], og = (float)gt[i][3];
-      const float dh = dhl[r * PU + cu] + dy[i];
+      const float dh = (WREG ? dhl[r * PU + cu] + dhl[R * PU + r * PU + cu] : dhl[r * PU + cu]) + dy[i];
       const float tc = tanhf_(cc[i]);
       const float dc = dh * og * (1.f - tc * tc) + dcreg[i];
       dcreg[i] = dc * fg;
@@ -751,20 +806,35 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
           for (int m = 0; m < MB; ++m)
 #pragma unroll
             for (int j = 0; j < JP; ++j) acc[m][j] = Mfma<bf16>::mma(af[m][ks], bfr[ks][j], acc[m][j]);
-        // publish: word (row pair, member, unit), the lane's rows 2r2, 2r2+1
+        // publish.  MB == 1: word (row quad, member, unit), the lane's four
+        // rows; MB > 1: word (row pair, member, unit), the lane's rows 2r2, 2r2+1
+        if constexpr (WREG) {
+          const uint64_t tg = h4_tag(a.seq, tau + 1);
 #pragma unroll
-        for (int m = 0; m < MB; ++m)
+          for (int j = 0; j < JP; ++j) {
+            const int rl = (lane >> 4) * 4;
+            const int nb = base + w + 4 * j;
+            const int unit = nb * 16 + (lane & 15);
+            const uint64_t v = (uint64_t)p15_encode(acc[0][j][0]) | ((uint64_t)p15_encode(acc[0][j][1]) << 16) |
+                               ((uint64_t)p15_encode(acc[0][j][2]) << 32) | ((uint64_t)p15_encode(acc[0][j][3]) << 48);
+            if (rowbase + rl < rend && nb < NB)
+              ll_store64(xo + (((int64_t)d * rquads + (rowbase - a.b0 + rl) / 4) * NM + mem) * H + unit, v | tg);
+          }
+        } else {
 #pragma unroll
-          for (int j = 0; j < JP; ++j)
+          for (int m = 0; m < MB; ++m)
 #pragma unroll
-            for (int r2 = 0; r2 < 2; ++r2) {
-              const int rl = m * 16 + (lane >> 4) * 4 + 2 * r2;   // even row within this member
-              const int nb = base + w + 4 * j;
-              const int unit = nb * 16 + (lane & 15);
-              if (rowbase + rl < rend && nb < NB)
-                ll_store(xo + (((int64_t)d * rpairs + (rowbase - a.b0 + rl) / 2) * NM + mem) * H + unit,
-                         pack_bf16x2(acc[m][j][2 * r2], acc[m][j][2 * r2 + 1]), fb | (uint32_t)(tau + 1));
-            }
+            for (int j = 0; j < JP; ++j)
+#pragma unroll
+              for (int r2 = 0; r2 < 2; ++r2) {
+                const int rl = m * 16 + (lane >> 4) * 4 + 2 * r2;   // even row within this member
+                const int nb = base + w + 4 * j;
+                const int unit = nb * 16 + (lane & 15);
+                if (rowbase + rl < rend && nb < NB)
+                  ll_store(xo + (((int64_t)d * rpairs + (rowbase - a.b0 + rl) / 2) * NM + mem) * H + unit,
+                           pack_bf16x2(acc[m][j][2 * r2], acc[m][j][2 * r2 + 1]), fb | (uint32_t)(tau + 1));
+              }
+        }
       }
     }
 
@@ -822,7 +892,7 @@ __global__ __launch_bounds__(256) void clear_exchange_kernel(uint4* p, int64_t n
 size_t persist_lds_bytes(int H, bool backward, int MB) {
   if (backward) {   // MB == 1 keeps W_hh in registers, staged through 128 KB of LDS
     const size_t run = (MB == 1 ? (size_t)0 : (size_t)16 * (H + 1) * 16) + (size_t)16 * (16 * MB + 1) * 16 +
-                       (size_t)16 * MB * PU * 4;
+                       (size_t)2 * 16 * MB * PU * 4;
     return MB == 1 ? std::max(run, (size_t)128 * 1024) : run;
   }
   // MB == 1 keeps W_hh in registers (staged through 128 KB of LDS at the
