@@ -577,6 +577,7 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     bool done = false, step_fused = false;
     if (use_persistent<T>(H, lo.T, true, s)) {
       PersistArgs pa = persist_args(lo, (const bf16*)W, ws, l);
+      pa.tag = (uint32_t)(lo.L - 1 - l);   // the backward runs the layers top-down
       pa.DA = (bf16*)DA; pa.DY = dY; pa.C = (float*)Cl; pa.G = (bf16*)Gl;
       pa.WT = have_wt ? (const bf16*)(WT + (int64_t)(2 * l) * 4 * H * H) : nullptr;
       pa.DAT = lo.write_dat ? (bf16*)DATl : nullptr;

@@ -19,10 +19,8 @@
 //
 // Step-to-step exchange without barriers or cache maintenance.  The values
 // one member needs from the others (h, or partial dh) are published in an
-// exchange buffer as 8-byte words holding two bf16 values and a step number
-// (launch tag and step + 1; at one 16-row block per workgroup, which means
-// one launch per layer, words pack four values and a 4-bit tag instead, see
-// h4_tag), written and read with agent-scope relaxed atomic
+// exchange buffer as 8-byte words holding four 15-bit values and a 4-bit
+// tag (see h4_tag), written and read with agent-scope relaxed atomic
 // stores and loads.  Atomic accesses to one location are coherent across the
 // whole GPU, so a reader that sees the expected step number in a word also
 // sees that word's payload; readers poll the words they need (bounded; the
@@ -30,8 +28,9 @@
 // parity: a member overwrites a slot only after it has consumed the next
 // step from every member, which those members produce only after they have
 // consumed the slot's current contents.  The buffer is cleared once per
-// forward or backward call and every launch of a call has its own tag, so no
-// word from an earlier launch carries a valid step number.  Every member of a
+// forward or backward call, and the tag tells a word of the expected step
+// from one of step n - 2 and from one left by either of the two previous
+// launches of the call.  Every member of a
 // group must be resident at once: the launch is plain when the occupancy
 // query shows the whole grid fits on the device, cooperative otherwise (see
 // launch_one).
@@ -53,10 +52,6 @@ __device__ __forceinline__ uint64_t ll_load(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ __forceinline__ void ll_store(uint64_t* p, uint32_t payload, uint32_t flag) {
-  __hip_atomic_store(p, ((uint64_t)flag << 32) | payload, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
 __device__ __forceinline__ void ll_store64(uint64_t* p, uint64_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -71,7 +66,7 @@ __device__ __forceinline__ uint32_t lane_xor2(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
 }
 
-// Forward words at one 16-row block per workgroup: four bf16 h of one row
+// Forward words: four bf16 h of one row
 // (units 4i .. 4i+3, the first in the low half-word).  |h| = |o tanh(c)| <= 1,
 // and a bf16 below 2 in magnitude has a zero top exponent bit (bit 14), so
 // the four such bits carry a 4-bit tag: bit 0 always set (a cleared word
@@ -83,7 +78,7 @@ __device__ __forceinline__ uint32_t lane_xor2(uint32_t v) {
 // the layer output keeps it.
 #define H4_TAG_BITS 0x4000400040004000ull
 //
-// BPTT words at one 16-row block per workgroup: four partial sums (rows 4i
+// BPTT words: four partial sums (rows 4i
 // .. 4i+3 of one unit) in a 15-bit form that frees the same bits: the bf16
 // of x * 2^-64 (so bf16 exponents 65 .. 190, i.e. 2^-62 <= |x| < 2^65, keep
 // bit 14 clear and the 8-bit significand of the bf16 of x), magnitudes from
@@ -111,21 +106,20 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 // MFMA A-fragments for k-steps ks0 .. ks0+nk-1 (nk <= KC) of MBW m-blocks,
 // gathered from exchange rows rp[m] (nullptr: row outside the batch, zeros).
-// Lane l takes row l % 16 and 8 k values = 4 words at word (ks*16 + (l/16)*4).
+// Lane l takes row l % 16 and 8 k values = 2 words at word (ks*8 + (l/16)*2).
 template <int MBW, int KC>
 __device__ __forceinline__ void ll_fragments(const uint64_t* const (&rp)[MBW], int ks0, int nk,
-                                             uint32_t flag, int lane, bf16x8 (&af)[MBW][KC],
+                                             uint64_t want, int lane, bf16x8 (&af)[MBW][KC],
                                              int* status) {
-  uint64_t w[MBW][KC][4];
-  const int woff = (lane >> 4) * 4;
+  uint64_t w[MBW][KC][2];
+  const int woff = (lane >> 4) * 2;
 #pragma unroll
   for (int m = 0; m < MBW; ++m)
 #pragma unroll
     for (int kk = 0; kk < KC; ++kk)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        w[m][kk][i] = (rp[m] && kk < nk) ? ll_load(rp[m] + (ks0 + kk) * 16 + woff + i)
-                                         : ((uint64_t)flag << 32);
+      for (int i = 0; i < 2; ++i)
+        w[m][kk][i] = (rp[m] && kk < nk) ? ll_load(rp[m] + (ks0 + kk) * 8 + woff + i) : want;
   for (unsigned it = 0;; ++it) {
     bool bad = false;
 #pragma unroll
@@ -133,7 +127,7 @@ __device__ __forceinline__ void ll_fragments(const uint64_t* const (&rp)[MBW], i
 #pragma unroll
       for (int kk = 0; kk < KC; ++kk)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) bad |= (uint32_t)(w[m][kk][i] >> 32) != flag;
+        for (int i = 0; i < 2; ++i) bad |= (w[m][kk][i] & H4_TAG_BITS) != want;
     if (!bad) break;
     // give up after SPIN_LIMIT polls, or at once when any lane anywhere has
     // given up before (then every later poll returns immediately too)
@@ -148,16 +142,15 @@ __device__ __forceinline__ void ll_fragments(const uint64_t* const (&rp)[MBW], i
 #pragma unroll
       for (int kk = 0; kk < KC; ++kk)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if ((uint32_t)(w[m][kk][i] >> 32) != flag)
-            w[m][kk][i] = ll_load(rp[m] + (ks0 + kk) * 16 + woff + i);
+        for (int i = 0; i < 2; ++i)
+          if ((w[m][kk][i] & H4_TAG_BITS) != want) w[m][kk][i] = ll_load(rp[m] + (ks0 + kk) * 8 + woff + i);
   }
 #pragma unroll
   for (int m = 0; m < MBW; ++m)
 #pragma unroll
     for (int kk = 0; kk < KC; ++kk) {
-      const uint4 v = make_uint4((uint32_t)w[m][kk][0], (uint32_t)w[m][kk][1], (uint32_t)w[m][kk][2],
-                                 (uint32_t)w[m][kk][3]);
+      const uint64_t lo = w[m][kk][0] & ~H4_TAG_BITS, hi = w[m][kk][1] & ~H4_TAG_BITS;
+      const uint4 v = make_uint4((uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32));
       af[m][kk] = __builtin_bit_cast(bf16x8, v);
     }
 }
@@ -178,7 +171,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int d = g & 1, s = g >> 1;
   const int u0 = mem * PU;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const uint32_t fb = a.tag << 8;   // step-number base of this launch (see persist_layer)
   const int ub = w & 1, wx = w >> 1;
 
   // W_hh rows of this member.  MB > 1: in LDS, row n = ub*64 + gate*16 + u,
@@ -246,7 +238,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
     __syncthreads();   // the reduction buffer and gathered h reuse this LDS
   }
-  const int wpr = KSPLIT ? H / 4 : H / 2;       // exchange words per row
+  const int wpr = H / 4;                        // exchange words per row
   constexpr int NJ4 = H_MAX_MEMBERS * PU / 64;  // MB == 1: words per thread and row (16 threads)
   const int64_t slot_stride = (int64_t)2 * a.rows * wpr;
 
@@ -347,7 +339,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       for (int ks0 = ks_beg; ks0 < ks_end; ks0 += KC) {
         const int nk = min(KC, ks_end - ks0);
         bf16x8 af[MBW][KC];
-        ll_fragments<MBW, KC>(rp, ks0, nk, fb | (uint32_t)tau, lane, af, a.status);
+        ll_fragments<MBW, KC>(rp, ks0, nk, h4_tag(a.seq, tau), lane, af, a.status);
 #pragma unroll
         for (int kk = 0; kk < KC; ++kk) {
           if (kk >= nk) break;
@@ -403,17 +395,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         for (int r = 0; r < 4; ++r) {
           const int row = rowbase + (mb0 + m) * 16 + (lane >> 4) * 4 + r;
           const float h_next_unit = lane_xor1(hv[m][r]);   // lanes of one row, units u and u^1
-          if constexpr (KSPLIT) {
-            // lane 4i stores units 4i .. 4i+3 (the pairs of lanes 4i and 4i+2)
-            const uint32_t p2 = pack_bf16x2(hv[m][r], h_next_unit);
-            const uint32_t p4 = lane_xor2(p2);
-            if (row < rend && (lane & 3) == 0)
-              ll_store64(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 4,
-                         ((((uint64_t)p4 << 32) | p2) & ~H4_TAG_BITS) | h4_tag(a.seq, tau + 1));
-          } else if (row < rend && (lane & 1) == 0) {
-            ll_store(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 2, pack_bf16x2(hv[m][r], h_next_unit),
-                     fb | (uint32_t)(tau + 1));
-          }
+          // lane 4i stores units 4i .. 4i+3 (the pairs of lanes 4i and 4i+2)
+          const uint32_t p2 = pack_bf16x2(hv[m][r], h_next_unit);
+          const uint32_t p4 = lane_xor2(p2);
+          if (row < rend && (lane & 3) == 0)
+            ll_store64(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 4,
+                       ((((uint64_t)p4 << 32) | p2) & ~H4_TAG_BITS) | h4_tag(a.seq, tau + 1));
         }
       if constexpr (KSPLIT) {
         // into LDS; the whole workgroup writes them out after the barrier
@@ -501,7 +488,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int d = g & 1, s = g >> 1;
   const int u0 = mem * PU;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const uint32_t fb = a.tag << 8;   // step-number base of this launch (see persist_layer)
 
   // LDS: W_hh of the 128 own gate rows, as the B operand [k/8][unit][8]
   // (k = own row kk: gate (kk>>4)&3, unit u0 + (kk>>6)*16 + (kk&15)), for
@@ -586,9 +572,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 
   const int rend = a.b0 + a.rows;
   const int rowbase = a.b0 + s * R;
-  const int rpairs = (a.rows + 1) / 2;             // row pairs of this launch
-  const int rquads = (a.rows + 3) / 4;             // row quads (MB == 1 words)
-  const int64_t slot_stride = (int64_t)2 * (WREG ? rquads : rpairs) * NM * H;
+  const int rquads = (a.rows + 3) / 4;             // row quads of this launch
+  const int64_t slot_stride = (int64_t)2 * rquads * NM * H;
   // cell items: unit cu = tid % 32, rows tid/32 + 8*i
   const int cu = tid & 31;
   float dcreg[ITEMS];
@@ -686,20 +671,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       for (int r = 0; r < 4; ++r) dhl[mh * R * PU + (4 * qd + r) * PU + cu] = sum[r];
     } else if (tau > 0) {
       const uint64_t* xs = a.X + ((tau - 1) & 1) * slot_stride;
+      const uint64_t want = h4_tag(a.seq, tau);
 #pragma unroll
-      for (int i = 0; i < MB; ++i) {
-        const int rp = (tid >> 5) + 8 * i;   // row pair within this member's rows
-        float lo = 0.f, hi = 0.f;
-        if (rowbase + 2 * rp < rend) {
-          const uint64_t* src = xs + ((int64_t)d * rpairs + (rowbase - a.b0) / 2 + rp) * NM * H + u0 + cu;
+      for (int i = 0; i < (MB + 1) / 2; ++i) {
+        const int qd = (tid >> 5) + 8 * i;   // row quad within this member's rows
+        float sum[4] = {0.f, 0.f, 0.f, 0.f};
+        if (qd < 4 * MB && rowbase + 4 * qd < rend) {
+          const uint64_t* src = xs + ((int64_t)d * rquads + (rowbase - a.b0) / 4 + qd) * NM * H + u0 + cu;
           uint64_t wv[H_MAX_MEMBERS];
 #pragma unroll
-          for (int k = 0; k < H_MAX_MEMBERS; ++k)
-            wv[k] = k < NM ? ll_load(src + (int64_t)k * H) : ((uint64_t)(fb | (uint32_t)tau) << 32);
+          for (int k = 0; k < H_MAX_MEMBERS; ++k) wv[k] = k < NM ? ll_load(src + (int64_t)k * H) : want;
           for (unsigned it = 0;; ++it) {
             bool bad = false;
 #pragma unroll
-            for (int k = 0; k < H_MAX_MEMBERS; ++k) bad |= (uint32_t)(wv[k] >> 32)  != (fb | (uint32_t)tau);
+            for (int k = 0; k < H_MAX_MEMBERS; ++k) bad |= (wv[k] & H4_TAG_BITS) != want;
             if (!bad) break;
             if (it > SPIN_LIMIT ||
                 ((it & 63) == 63 && __hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
@@ -709,18 +694,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             __builtin_amdgcn_s_sleep(1);
 #pragma unroll
             for (int k = 0; k < H_MAX_MEMBERS; ++k)
-              if ((uint32_t)(wv[k] >> 32)  != (fb | (uint32_t)tau)) wv[k] = ll_load(src + (int64_t)k * H);
+              if ((wv[k] & H4_TAG_BITS) != want) wv[k] = ll_load(src + (int64_t)k * H);
           }
 #pragma unroll
           for (int k = 0; k < H_MAX_MEMBERS; ++k) {
             if (k >= NM) break;
-            const uint32_t v = (uint32_t)wv[k];
-            lo += __builtin_bit_cast(float, v << 16);
-            hi += __builtin_bit_cast(float, v & 0xffff0000u);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sum[r] += p15_decode((uint32_t)(wv[k] >> (16 * r)) & 0xffffu);
           }
         }
-        dhl[(2 * rp) * PU + cu] = lo;
-        dhl[(2 * rp + 1) * PU + cu] = hi;
+        if (qd < 4 * MB) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) dhl[(4 * qd + r) * PU + cu] = sum[r];
+        }
       }
     } else {
       for (int i = tid; i < (WREG ? 2 : 1) * R * PU; i += 256) dhl[i] = 0.f;
@@ -806,35 +792,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
           for (int m = 0; m < MB; ++m)
 #pragma unroll
             for (int j = 0; j < JP; ++j) acc[m][j] = Mfma<bf16>::mma(af[m][ks], bfr[ks][j], acc[m][j]);
-        // publish.  MB == 1: word (row quad, member, unit), the lane's four
-        // rows; MB > 1: word (row pair, member, unit), the lane's rows 2r2, 2r2+1
-        if constexpr (WREG) {
-          const uint64_t tg = h4_tag(a.seq, tau + 1);
+        // publish: word (row quad, member, unit), the lane's four rows
+        const uint64_t tg = h4_tag(a.seq, tau + 1);
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
 #pragma unroll
           for (int j = 0; j < JP; ++j) {
-            const int rl = (lane >> 4) * 4;
+            const int rl = m * 16 + (lane >> 4) * 4;
             const int nb = base + w + 4 * j;
             const int unit = nb * 16 + (lane & 15);
-            const uint64_t v = (uint64_t)p15_encode(acc[0][j][0]) | ((uint64_t)p15_encode(acc[0][j][1]) << 16) |
-                               ((uint64_t)p15_encode(acc[0][j][2]) << 32) | ((uint64_t)p15_encode(acc[0][j][3]) << 48);
+            const uint64_t v = (uint64_t)p15_encode(acc[m][j][0]) | ((uint64_t)p15_encode(acc[m][j][1]) << 16) |
+                               ((uint64_t)p15_encode(acc[m][j][2]) << 32) | ((uint64_t)p15_encode(acc[m][j][3]) << 48);
             if (rowbase + rl < rend && nb < NB)
               ll_store64(xo + (((int64_t)d * rquads + (rowbase - a.b0 + rl) / 4) * NM + mem) * H + unit, v | tg);
           }
-        } else {
-#pragma unroll
-          for (int m = 0; m < MB; ++m)
-#pragma unroll
-            for (int j = 0; j < JP; ++j)
-#pragma unroll
-              for (int r2 = 0; r2 < 2; ++r2) {
-                const int rl = m * 16 + (lane >> 4) * 4 + 2 * r2;   // even row within this member
-                const int nb = base + w + 4 * j;
-                const int unit = nb * 16 + (lane & 15);
-                if (rowbase + rl < rend && nb < NB)
-                  ll_store(xo + (((int64_t)d * rpairs + (rowbase - a.b0 + rl) / 2) * NM + mem) * H + unit,
-                           pack_bf16x2(acc[m][j][2 * r2], acc[m][j][2 * r2 + 1]), fb | (uint32_t)(tau + 1));
-              }
-        }
       }
     }
 
@@ -1009,8 +980,8 @@ hipError_t persist_clear(bool backward, const PersistArgs& a, hipStream_t s) {
   // both exchange slots start without any valid step number; the forward's
   // clear also resets the status word (it covers the forward call and the
   // backward call after it)
-  const int64_t words = backward ? (int64_t)2 * 2 * ((chunk + 1) / 2) * (a.H / PU) * a.H
-                                 : (int64_t)2 * 2 * chunk * (a.H / 2);
+  const int64_t words = backward ? (int64_t)2 * 2 * ((chunk + 3) / 4) * (a.H / PU) * a.H
+                                 : (int64_t)2 * 2 * chunk * (a.H / 4);
   const int64_t n16 = words / 2;
   hipLaunchKernelGGL(clear_exchange_kernel, dim3((unsigned)std::min<int64_t>(cdiv(n16, 256), 2048)), dim3(256), 0,
                      s, (uint4*)a.X, n16, backward ? nullptr : a.status);
@@ -1030,9 +1001,8 @@ hipError_t persist_layer(bool backward, PersistArgs a, hipStream_t s) {
     c.b0 = b0;
     c.rows = std::min(chunk, a.B - b0);
     c.NS = (c.rows + 16 * MB - 1) / (16 * MB);
-    // step numbers of this launch: tag = layer * 256 + chunk above the 8-bit
-    // step, so no word left by an earlier launch of the same call matches
-    c.tag = a.tag * 256 + (uint32_t)(b0 / chunk);
+    // the launch's position in the call (the caller's tag numbers the layers
+    // in the order the call runs them)
     c.seq = a.tag * (uint32_t)cdiv(a.B, chunk) + (uint32_t)(b0 / chunk);
     hipError_t e;
     if (backward)

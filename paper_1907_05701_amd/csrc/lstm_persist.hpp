@@ -19,8 +19,7 @@ struct PersistArgs {
   float* DBP;         // backward, optional: sums of da over 16-row blocks and all steps [cdiv(B,16)][8H]
   int64_t M;          // frames, T*B (DAT row length)
   int* status;        // cleared by the forward pass's persist_clear; 1 if a wait ever gave up
-  uint32_t tag;       // caller: layer index; step numbers carry it (exchange words of
-                      // earlier layers of the same call never match)
+  uint32_t tag;       // caller: the layer's position in the order the call runs the layers
   int Tn, B, H;
   int b0, rows, NS;   // batch chunk handled by one launch (filled in by persist_layer)
   uint32_t seq;       // the launch's position among the call's launches (filled in by persist_layer)
@@ -30,14 +29,13 @@ struct PersistArgs {
 // launch covers at most PERSIST_MAX_SLICES*128 rows.
 #define PERSIST_MAX_SLICES 32
 #define PERSIST_MAX_ROWS (PERSIST_MAX_SLICES * 16 * 8)
-// Exchange buffer: 2 slots x 2 directions x row pairs x (H/32 members) x H
-// units words of 8 bytes (the backward's partial sums; the forward uses H/2
-// words per row).
+// Exchange buffer: 2 slots x 2 directions x row quads x (H/32 members) x H
+// units words of 8 bytes (the backward's partial sums, four rows per word;
+// the forward uses H/4 words per row).
 static inline size_t persist_xch_bytes(int B, int H) {
-  size_t rows = B < PERSIST_MAX_ROWS ? B : PERSIST_MAX_ROWS;
-  rows += rows & 1;
+  const size_t rows = B < PERSIST_MAX_ROWS ? B : PERSIST_MAX_ROWS;
   const size_t members = H / 32 > 0 ? H / 32 : 1;
-  return (size_t)2 * 2 * rows * (H / 2) * members * 8;
+  return (size_t)2 * 2 * ((rows + 3) / 4) * members * H * 8;
 }
 
 // True if the persistent kernels can hold a W_hh slice for this H in LDS
@@ -53,5 +51,7 @@ hipError_t persist_clear(bool backward, const PersistArgs& a, hipStream_t s);
 // persistent path, or whose exchange clear failed).
 hipError_t persist_status_clear(int* status, hipStream_t s);
 // Runs every step of one layer, both directions; hipSuccess or the error of
-// the launch that failed.  Layers of one call need distinct tags.
+// the launch that failed.  The layers of one call carry tags 0, 1, 2, ...
+// in the order they run (an exchange word tells its launch from the two
+// before it by the launch's position modulo 4).
 hipError_t persist_layer(bool backward, PersistArgs a, hipStream_t s);

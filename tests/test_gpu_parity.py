@@ -173,8 +173,10 @@ def test_stress_t64_b1024_replicated(gpu_lib):
 @pytest.mark.parametrize("B", [200, 300, 1100], ids=["mb2", "mb4", "mb8_two_chunks"])
 def test_recurrence_batch_regimes_bf16(gpu_lib, B):
     """Batches large enough that each recurrent workgroup covers 2, 4 or 8
-    row blocks, and (B=1100) that the batch is processed in two chunks."""
-    run_step_and_compare(dict(L=1, D=40, H=512, P=32, K=50, T=3, B=B), "bf16", BF16_TOL, seed=11,
+    row blocks, and (B=1100) that the batch is processed in two chunks.  Two
+    layers, so that exchange words left by the previous layer's launches
+    (forward bottom-up, backward top-down) are met and must not match."""
+    run_step_and_compare(dict(L=2, D=40, H=512, P=32, K=50, T=3, B=B), "bf16", BF16_TOL, seed=11,
                          check_update=False)
 
 
