@@ -58,7 +58,7 @@ struct RecFwdArgs {
   const T* Whh1;     // W_hh of the reverse direction
   const T* Gx;       // input projection incl. both biases [M][8H]
   float* C;          // cell states [M][2H]
-  T* G;              // saved activated gates [M][2][H][4] (direction, unit, gate i/f/g/o)
+  T* G;              // saved gate pre-activations [M][2][H][4] (direction, unit, gate i/f/g/o)
   int Tn, B, H, tau;
 };
 
@@ -143,17 +143,19 @@ __global__ __launch_bounds__(256) void lstm_rec_fwd_step(const RecFwdArgs<T> a) 
     const int b = rb * 16 * MBK + mb * 16 + (lane >> 4) * 4 + r;
     if (b >= B) continue;
     const int64_t row = (int64_t)t * B + b;
-    const float ig = sigmoidf_(acc[0][r] + gx[r][0]), fg = sigmoidf_(acc[1][r] + gx[r][1]);
-    const float gg = tanhf_(acc[2][r] + gx[r][2]), og = sigmoidf_(acc[3][r] + gx[r][3]);
+    const float pre[4] = {acc[0][r] + gx[r][0], acc[1][r] + gx[r][1], acc[2][r] + gx[r][2], acc[3][r] + gx[r][3]};
+    const float ig = sigmoidf_(pre[0]), fg = sigmoidf_(pre[1]);
+    const float gg = tanhf_(pre[2]), og = sigmoidf_(pre[3]);
     const float c = fg * cp[r] + ig * gg;
     const float h = og * tanhf_(c);
     a.C[row * 2 * H + (int64_t)d * H + u] = c;
     a.Y[row * 2 * H + (int64_t)d * H + u] = from_f32<T>(h);
-    T* gs = a.G + row * 8 * H + (int64_t)d * 4 * H + (int64_t)u * 4;   // the unit's four gates together
-    gs[0] = from_f32<T>(ig);
-    gs[1] = from_f32<T>(fg);
-    gs[2] = from_f32<T>(gg);
-    gs[3] = from_f32<T>(og);
+    // the unit's four gate pre-activations together (the backward evaluates
+    // the activations from them: stored activations near 1 in bf16 would
+    // lose sigma' = sigma (1 - sigma))
+    T* gs = a.G + row * 8 * H + (int64_t)d * 4 * H + (int64_t)u * 4;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) gs[g] = from_f32<T>(pre[g]);
   }
 }
 
@@ -167,7 +169,7 @@ struct RecBwdArgs {
   const T* WT0;      // W_hh^T of the forward direction [H][4H]
   const T* WT1;      // W_hh^T of the reverse direction
   const float* DY;   // gradient reaching the layer output [M][2H]
-  const T* G;        // saved gates [M][2][H][4]
+  const T* G;        // saved gate pre-activations [M][2][H][4]
   const float* C;    // saved cell states [M][2H]
   float* DC;         // carried cell gradient [2][B][H]
   T* DAT;            // optional: da also written frame-contiguous, [8H][M]
@@ -260,7 +262,8 @@ __global__ __launch_bounds__(256) void lstm_rec_bwd_step(const RecBwdArgs<T> a) 
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int b = rb * 16 * MBK + mb * 16 + (lane >> 4) * 4 + r;
-    const float ig = to_f32(graw[r][0]), fg = to_f32(graw[r][1]), gg = to_f32(graw[r][2]), og = to_f32(graw[r][3]);
+    const float ig = sigmoidf_(to_f32(graw[r][0])), fg = sigmoidf_(to_f32(graw[r][1]));
+    const float gg = tanhf_(to_f32(graw[r][2])), og = sigmoidf_(to_f32(graw[r][3]));
     const float dh = acc[r] + dy[r];
     const float tc = tanhf_(cc[r]);
     const float dc = dh * og * (1.f - tc * tc) + dcn[r];

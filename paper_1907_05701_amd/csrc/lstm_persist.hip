@@ -190,7 +190,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   }
   f32x4* red = (f32x4*)(lds + (KSPLIT ? (size_t)0 : (size_t)kcn * LDN * 8));
   bf16* hl = (bf16*)(red + 8 * 64);   // MB == 1: gathered h [H/8][16 + 1][8]
-  // MB == 1: a step's c [16][32] (float), h [16][32] and gates [16][32][4]
+  // MB == 1: a step's c [16][32] (float), h [16][32] and gate pre-activations [16][32][4]
   // (bf16) of the own units, staged for 16-byte stores
   float* sC = (float*)(hl + (size_t)(H / 8) * 17 * 8);
   bf16* sY = (bf16*)(sC + 16 * 32);
@@ -375,13 +375,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       for (int m = 0; m < MBW; ++m)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          gv[m][r][0] = sigmoidf_(acc[m][0][r] + (float)gx[m][r][0]);
-          gv[m][r][1] = sigmoidf_(acc[m][1][r] + (float)gx[m][r][1]);
-          gv[m][r][2] = tanhf_(acc[m][2][r] + (float)gx[m][r][2]);
-          gv[m][r][3] = sigmoidf_(acc[m][3][r] + (float)gx[m][r][3]);
-          const float c = gv[m][r][1] * creg[m][r] + gv[m][r][0] * gv[m][r][2];
+          // gv: pre-activations, saved for the backward
+#pragma unroll
+          for (int q = 0; q < 4; ++q) gv[m][r][q] = acc[m][q][r] + (float)gx[m][r][q];
+          const float ig = sigmoidf_(gv[m][r][0]), fg = sigmoidf_(gv[m][r][1]);
+          const float gg = tanhf_(gv[m][r][2]), og = sigmoidf_(gv[m][r][3]);
+          const float c = fg * creg[m][r] + ig * gg;
           creg[m][r] = c;
-          hv[m][r] = gv[m][r][3] * tanhf_(c);
+          hv[m][r] = og * tanhf_(c);
         }
       // every row's h before the first publish (the empty asm pins the
       // values here, so the compiler cannot sink their math past a publish)
@@ -588,7 +589,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
   for (int m = 0; m < MB; ++m) dbacc[m] = 0.f;
 
-  // everything the cell derivative needs besides dh_rec: dy, the gates and
+  // everything the cell derivative needs besides dh_rec: dy, the gate pre-activations and
   // c at t, c at the step's predecessor in forward time (which is the next
   // step's t).  Fetched one step ahead, right after the previous step's
   // gather, so that no gather waits for them; c at t is the previous step's
@@ -627,7 +628,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   for (int tau = 0; tau < Tn; ++tau) {
     const int t = d ? tau : Tn - 1 - tau;
     float dy[ITEMS], cp[ITEMS];
-    bf16 gt[ITEMS][4];
+    // the step's gate activations from the prefetched pre-activations,
+    // before the gather (whose polls wait for the other members anyway)
+    float ga[ITEMS][4];
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      ga[i][0] = sigmoidf_((float)gtn[i][0]);
+      ga[i][1] = sigmoidf_((float)gtn[i][1]);
+      ga[i][2] = tanhf_((float)gtn[i][2]);
+      ga[i][3] = sigmoidf_((float)gtn[i][3]);
+    }
 
     // gather dh_rec for the own units.  MB == 1: items (row quad, unit,
     // member parity), unit = tid % 32, quad (tid / 32) % 4; each thread sums
@@ -716,8 +726,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     for (int i = 0; i < ITEMS; ++i) {
       dy[i] = dyn[i];
       cp[i] = cpn[i];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) gt[i][q] = gtn[i][q];
     }
     if (tau + 1 < Tn) fetch(tau + 1);
 
@@ -727,7 +735,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     for (int i = 0; i < ITEMS; ++i) {
       const int r = (tid >> 5) + 8 * i;
       const int row = rowbase + r;
-      const float ig = (float)gt[i][0], fg = (float)gt[i][1], gg = (float)gt[i][2], og = (float)gt[i][3];
+      const float ig = ga[i][0], fg = ga[i][1], gg = ga[i][2], og = ga[i][3];
       const float dh = (WREG ? dhl[r * PU + cu] + dhl[R * PU + r * PU + cu] : dhl[r * PU + cu]) + dy[i];
       const float tc = tanhf_(cc[i]);
       const float dc = dh * og * (1.f - tc * tc) + dcreg[i];

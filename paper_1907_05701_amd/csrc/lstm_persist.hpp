@@ -11,7 +11,7 @@ struct PersistArgs {
                       // this layer, [2][H][4H] (directions)
   const bf16* Gx;     // forward: input projection [M][8H]
   float* C;           // cell states [M][2H] (forward writes, backward reads)
-  bf16* G;            // activated gates [M][2][H][4] (direction, unit, gate i/f/g/o; forward writes, backward reads)
+  bf16* G;            // gate pre-activations [M][2][H][4] (direction, unit, gate i/f/g/o; forward writes, backward reads)
   bf16* DA;           // backward: gate pre-activation gradients [M][8H]
   const float* DY;    // backward: gradient reaching the layer output [M][2H]
   uint64_t* X;        // step-exchange words (see lstm_persist.hip), PERSIST_XCH_BYTES

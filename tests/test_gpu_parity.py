@@ -44,12 +44,15 @@ def block_errors(g_gpu, g_ref, dims):
     return out
 
 
-def run_step_and_compare(shape, precision, tol, dist="uniform", seed=0, check_update=True):
+def run_step_and_compare(shape, precision, tol, dist="uniform", seed=0, check_update=True, edit_theta=None,
+                         check=None, only=None):
     from paper_1907_05701_amd.step import LearnerStep
     say(f"[parity] shape={shape} precision={precision} seed={seed}")
     dims = ref.Dims(**shape)
     n = ref.param_count(dims)
     theta = inputs.params(n, seed=seed)
+    if edit_theta is not None:
+        theta = edit_theta(theta.copy(), dims)
     x = inputs.features(dims.T, dims.B, dims.D, seed=seed + 1)
     lab = inputs.labels(dims.T, dims.B, dims.K, seed=seed + 2, dist=dist)
     peer = inputs.peer(theta, seed=seed + 3)
@@ -67,9 +70,11 @@ def run_step_and_compare(shape, precision, tol, dist="uniform", seed=0, check_up
     grad = st.grad.cpu().numpy()
     errs.update({str(k): v for k, v in block_errors(grad, want["grad"], dims).items()})
     errs["grad"] = rel(grad, want["grad"])
+    if check is not None:
+        check(st)
     worst = max(errs.items(), key=lambda kv: kv[1])
     say(f"[parity] loss gpu={loss:.7f} ref={want['loss']:.7f}; worst {worst[0]}={worst[1]:.3e}")
-    bad = {k: v for k, v in errs.items() if not v <= tol}
+    bad = {k: v for k, v in errs.items() if (only is None or k in only) and not v <= tol}
     assert not bad, bad
     if check_update:
         lr = 0.1
@@ -168,6 +173,41 @@ def test_full_model_b512_replicated(gpu_lib):
 def test_stress_t64_b1024_replicated(gpu_lib):
     """The stress workload (T = 64, B = 1024) as 64 copies of 16 sequences."""
     run_replicated_and_compare(dict(L=6, D=260, H=512, P=256, K=32000, T=64, B=16), 64, BF16_TOL, seed=21)
+
+
+def test_saturated_cells_bf16(gpu_lib):
+    """Cells driven into saturation so that most outputs h are +-1.0 in bf16
+    (gate biases i, f: +6, g: +2, o: +7: the cells charge by about one per
+    step and o tanh c rounds to 1): the recurrent exchange packs h with a tag
+    in bit 14 of each bf16, which is free for |h| <= 1.  The forward outputs,
+    which the exchanged h determine, are compared with the oracle (the
+    saturated recurrence is contractive: a 2^-9 relative perturbation of the
+    parameters moves y_top by 4e-5 in the float64 oracle).  The gradients are
+    not: in this regime they are small differences of large terms, and the
+    bf16 forward alone moves them by several per cent (float64 emulation of
+    the oracle: the input projection rounded to bf16 moves the layer-0 W_ih
+    gradient by 5 %, the recurrent h by 3.7 %; measured here: the persistent
+    and the per-step kernels agree with each other, 15 % from the oracle,
+    and the float32 path is within 2e-5)."""
+    def edit(theta, dims):
+        blocks, _ = ref.param_layout(dims)
+        H = dims.H
+        for key, (off, shp) in blocks.items():
+            if key[0] == "b_ih":   # gates i, f, g, o
+                b = theta[off:off + int(np.prod(shp))]
+                b[0:2 * H] = 6.0
+                b[2 * H:3 * H] = 2.0
+                b[3 * H:4 * H] = 7.0
+        return theta
+
+    def saturated(st):
+        frac = float((st.y_top.float().abs() == 1.0).float().mean())
+        say(f"[parity] fraction of top-layer h equal to +-1: {frac:.3f}")
+        assert frac > 0.3
+
+    errs = run_step_and_compare(dict(L=2, D=40, H=512, P=32, K=100, T=21, B=16), "bf16", BF16_TOL, seed=31,
+                                edit_theta=edit, check=saturated, only=("loss", "y_top"), check_update=False)
+    say(f"[parity] saturated: loss {errs['loss']:.2e}, y_top {errs['y_top']:.2e}")
 
 
 @pytest.mark.parametrize("B", [200, 300, 1100], ids=["mb2", "mb4", "mb8_two_chunks"])
