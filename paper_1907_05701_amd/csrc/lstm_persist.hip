@@ -891,7 +891,8 @@ static int persist_max_wg() {
 }
 
 bool persist_supported(int H, int T) {
-  return H % PU == 0 && H / PU <= H_MAX_MEMBERS && T <= 255 && persist_lds_bytes(H, false, 2) <= 160 * 1024 &&
+  (void)T;   // any length: the tag holds only bit 1 of the step number
+  return H % PU == 0 && H / PU <= H_MAX_MEMBERS && persist_lds_bytes(H, false, 2) <= 160 * 1024 &&
          persist_lds_bytes(H, true, 2) <= 160 * 1024;
 }
 
@@ -974,7 +975,7 @@ static bool persist_plan(bool backward, int H, int B, int* MBo, int* chunko) {
   while (MB > 1 && persist_lds_bytes(H, backward, MB) > 160 * 1024) MB /= 2;
   *MBo = MB;
   *chunko = std::min(B, max_ns * 16 * MB);
-  return (B + *chunko - 1) / *chunko <= 255;
+  return true;
 }
 
 bool persist_bwd_needs_wt(int H, int B) {

@@ -210,6 +210,13 @@ def test_saturated_cells_bf16(gpu_lib):
     say(f"[parity] saturated: loss {errs['loss']:.2e}, y_top {errs['y_top']:.2e}")
 
 
+def test_long_sequence_bf16(gpu_lib):
+    """T = 300 on the persistent kernels: the exchange tag carries only bit 1
+    of the step number, so the sequence length is not bounded by it."""
+    run_step_and_compare(dict(L=2, D=24, H=64, P=16, K=30, T=300, B=8), "bf16", BF16_TOL, seed=41,
+                         check_update=False)
+
+
 @pytest.mark.parametrize("B", [200, 300, 1100], ids=["mb2", "mb4", "mb8_two_chunks"])
 def test_recurrence_batch_regimes_bf16(gpu_lib, B):
     """Batches large enough that each recurrent workgroup covers 2, 4 or 8
