@@ -319,19 +319,15 @@ __global__ __launch_bounds__(256) void convert_input_kernel(const float* __restr
                                                             int D, int Dp, T* __restrict__ X,
                                                             const bf16* __restrict__ w0, int64_t wz, int wrows,
                                                             bf16* __restrict__ wp) {
-  const int64_t total = M * Dp, wtotal = wp ? (int64_t)2 * wrows * Dp : 0;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total + wtotal;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    if (i < total) {
-      const int64_t m = i / Dp;
-      const int k = (int)(i % Dp);
-      X[i] = from_f32<T>(k < D ? x[m * D + k] : 0.f);
-    } else {
-      const int64_t j = i - total, zr = j / Dp;
-      const int k = (int)(j % Dp);
-      const int64_t z = zr / wrows, r = zr % wrows;
-      wp[j] = k < D ? w0[z * wz + r * D + k] : (bf16)0.f;
-    }
+  // one row per workgroup: the M frames, then (with wp) the 2*wrows rows of
+  // both directions' W_ih
+  const int64_t row = blockIdx.x;
+  if (row < M) {
+    for (int k = threadIdx.x; k < Dp; k += 256) X[row * Dp + k] = from_f32<T>(k < D ? x[row * D + k] : 0.f);
+  } else {
+    const int zr = (int)(row - M), z = zr / wrows, r = zr % wrows;
+    for (int k = threadIdx.x; k < Dp; k += 256)
+      wp[(int64_t)zr * Dp + k] = k < D ? w0[z * wz + (int64_t)r * D + k] : (bf16)0.f;
   }
 }
 
@@ -427,8 +423,7 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
   T* GX = (T*)(ws + lo.GX);
   bf16* WP0 = lo.WP0_bytes ? (bf16*)(ws + lo.WP0) : nullptr;
   {
-    const int64_t total = M * lo.Dp0 + (WP0 ? (int64_t)2 * 4 * H * lo.Dp0 : 0);
-    const unsigned grid = (unsigned)std::min<int64_t>(cdiv(total, 256), 16384);
+    const unsigned grid = (unsigned)(M + (WP0 ? 2 * 4 * H : 0));
     BLSTM_LAUNCH("convert_input", convert_input_kernel<T>, dim3(grid), dim3(256), 0, s, x, M, lo.D,
                  lo.Dp0, X0, (const bf16*)W + lo.Wih[0][0], lo.Wih[0][1] - lo.Wih[0][0], 4 * H, WP0);
   }
