@@ -88,7 +88,7 @@ int blstm_pack_params(const blstm_dims* dims, const float* theta, void* theta_lp
  * chunk starting from h = c = 0).
  *   theta    [n] float32;  theta_lp [n] bf16 (BF16; ignored for FP32)
  *   x        [T][B][D] float32 features
- *   act_ws   workspace, written (saved gates, cell states, hidden states)
+ *   act_ws   workspace, written (saved gate pre-activations, cell states, hidden states)
  *   y_top    [T][B][2H] output of the top layer, forward half first. */
 int blstm_fwd(const blstm_dims* dims, const float* theta, const void* theta_lp,
               const float* x, void* act_ws, void* y_top, hipStream_t stream);
