@@ -51,7 +51,7 @@ def kernel_work(name, c, n_params):
         return "mfma", (L - 1) * 2 * M * 2 * H * 8 * H, "flop", L - 1
     if name == "gemm_z":
         return "mfma", 2 * M * P * 2 * H, "flop", 1
-    if name in ("gemm_logits", "gemm_dws", "gemm_dz"):
+    if name in ("gemm_logits", "gemm_logits_ds", "gemm_dws", "gemm_dz"):
         return "mfma", 2 * M * K * P, "flop", 1
     if name in ("gemm_dwl", "gemm_dy"):
         return "mfma", 2 * M * P * 2 * H, "flop", 1

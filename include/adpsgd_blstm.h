@@ -12,8 +12,12 @@
  *
  * Conventions shared by every call:
  *   - All pointers named theta/grad/x/y/dy/... are DEVICE pointers allocated by
- *     the caller; the library never allocates device memory and keeps no
- *     device state between calls.  Workspace sizes come from
+ *     the caller; the library never allocates device memory.  State carried
+ *     between calls lives in the caller's act_ws (saved activations, the
+ *     recurrence status flag).  Host-side, the library keeps a per-device
+ *     side stream with its events (created on first use by an eager
+ *     blstm_bwd that overlaps work, see there) and the bookkeeping of the
+ *     optional timing hooks.  Workspace sizes come from
  *     blstm_workspace_bytes().
  *   - Every call only enqueues work on `stream` (no host synchronisation) and
  *     returns 0 on success or a negative BLSTM_E* code; blstm_last_error()
@@ -71,7 +75,9 @@ int64_t blstm_param_count(const blstm_dims* dims);
 
 /* Sizes in bytes of the caller-allocated buffers for these dims:
  *   act_ws   -- activations saved by blstm_fwd for blstm_bwd, plus the
- *               backward's scratch; owned by the caller, opaque layout.
+ *               backward's scratch; owned by the caller, opaque layout except
+ *               for its last 256 bytes (the recurrence status flag, see
+ *               blstm_recurrence_ok).
  *   head_ws  -- scratch of softmax_ce_fwd_bwd (logits, partial sums).
  *   theta_lp -- the bf16 operand copy of theta (n * 2 bytes; 0 for FP32).
  *   y_top    -- blstm_fwd output [T][B][2H] in the precision's element type.
@@ -107,27 +113,42 @@ int softmax_ce_fwd_bwd(const blstm_dims* dims, const float* theta, const void* t
                        float* loss, float* dy_top, float* grad, void* head_ws,
                        hipStream_t stream);
 
-/* Back-propagation through time of the LSTM stack given dy_top; act_ws and
- * y_top must come from blstm_fwd with the same theta and dims.  Overwrites
- * the LSTM slots of grad (both b_ih and b_hh receive the same bias
- * gradient); head slots are not touched.  act_ws is also used as scratch.
- * When not under stream capture the call may also run work on an internal
- * stream of the current device (created once, default priority); that work
- * is joined into `stream` before the call returns, so stream order holds as
- * for any other call.  ADPSGD_BLSTM_OVERLAP=0 disables it. */
+/* Back-propagation through time of the LSTM stack (Section 5.2 model; the
+ * gradient g of eq. 4 for the LSTM parameters) given dy_top = dloss/dy_top.
+ * Per layer, top-down: the gate-gradient recurrence in reverse time
+ * (dh = dy + W_hh^T da of the next step, dc, da for gates i, f, g, o), then
+ * dW_ih = sum_t da x^T, dW_hh = sum_t da h_prev^T, db = sum_t da and the
+ * gradient reaching the layer below, dX = W_ih^T da.
+ *   theta, theta_lp  as for blstm_fwd
+ *   act_ws  from blstm_fwd with the same theta and dims (saved gate
+ *           pre-activations, cell and hidden states); also used as scratch,
+ *           so a second blstm_bwd needs a new blstm_fwd first
+ *   y_top   [T][B][2H] in the precision's type, from that blstm_fwd
+ *   dy_top  [T][B][2H] float32
+ *   grad    [n] float32: the LSTM slots are overwritten (b_ih and b_hh
+ *           receive the same bias gradient); head slots are not touched.
+ * Returns 0, BLSTM_EINVAL (NULL pointer, bad dims) or BLSTM_EHIP (launch
+ * failure).  When not under stream capture the call may also run work on an
+ * internal stream of the current device (created once, default priority);
+ * that work is joined into `stream` before the call returns, so stream order
+ * holds as for any other call.  ADPSGD_BLSTM_OVERLAP=0 disables it. */
 int blstm_bwd(const blstm_dims* dims, const float* theta, const void* theta_lp,
               void* act_ws, const void* y_top, const float* dy_top, float* grad,
               hipStream_t stream);
 
 /* Whether every recurrent exchange wait of the persistent kernels completed
- * since the last blstm_fwd on act_ws (covering that call and the blstm_bwd
- * after it).  The persistent kernels are plain launches when the occupancy
- * query shows the whole grid resident at once; if other streams or
- * processes occupy CUs, a wait gives up after its bound instead of hanging
- * and the result of that call is not valid.  Returns BLSTM_OK, or
- * BLSTM_EHIP with a message.  Synchronises `stream`; not during stream
- * capture.  ADPSGD_BLSTM_COOPERATIVE=1 makes every persistent launch
- * cooperative (guaranteed residency, about 15 us more per launch). */
+ * since the previous blstm_recurrence_ok on act_ws (or since act_ws was first
+ * used): the flag is sticky, so one query after many steps (or after replays
+ * of a captured graph) covers all of them.  The persistent kernels are plain
+ * launches when the occupancy query shows the whole grid resident at once;
+ * if other streams or processes occupy CUs, a wait gives up after its bound
+ * instead of hanging and the results of that call are not valid.  The flag
+ * lives in the last 256 bytes of act_ws (an int32 at offset act_ws_bytes -
+ * 256, nonzero after a give-up, and an initialisation tag); the query reads
+ * it, clears it, and returns BLSTM_OK or BLSTM_EHIP with a message.
+ * Synchronises `stream`; not during stream capture.
+ * ADPSGD_BLSTM_COOPERATIVE=1 makes every persistent launch cooperative
+ * (guaranteed residency, about 15 us more per launch). */
 int blstm_recurrence_ok(const blstm_dims* dims, const void* act_ws, hipStream_t stream);
 
 /* Super-learner reduction (eq. 6): out = scale * sum_{r=0}^{R-1} grads[r],

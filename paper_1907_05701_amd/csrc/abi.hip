@@ -144,15 +144,22 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   }
   L.SKP = a; a = align256(a + skp);
   L.SKP2 = a; a = align256(a + skp);   // split-K partials of the side-stream products
-  L.SYNC = a; a = align256(a + 256);                            // status word
   L.XCH = a; a = align256(a + persist_xch_bytes(d->B, d->H));   // recurrent step exchange
+  // recurrence status block, the last PERSIST_STATUS_BYTES of act_ws
+  L.SYNC = a; a += PERSIST_STATUS_BYTES;
   L.act_bytes = a;
 
   // head_ws
   size_t h = 0;
   const int64_t P = d->P;
   L.Z = h; h = align256(h + (size_t)M * P * es);
+  // float32: the logits, overwritten by ds; bf16: ds only (the logits stay
+  // in the products' accumulators) plus the per-(frame, class strip)
+  // statistics and the per-frame log-sum-exp
   L.S = h; h = align256(h + (size_t)M * L.Kp * es);
+  L.LST = h; h = align256(h + (es == 2 ? (size_t)M * cdiv(d->K, 64) * 8 : 0));
+  L.LSE = h; h = align256(h + (es == 2 ? (size_t)M * 4 : 0));
+  L.LDB = h; h = align256(h + (es == 2 ? (size_t)cdiv(M, 32) * L.Kp * 4 : 0));   // db_s partials per 32+ frames
   L.RL = h; h = align256(h + (size_t)M * 4);
   L.DZ = h; h = align256(h + (size_t)M * P * 4);
   L.DZT = h; h = align256(h + (size_t)M * P * es);

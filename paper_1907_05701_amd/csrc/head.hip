@@ -3,11 +3,11 @@
 // context-dependent HMM states, and the frame cross-entropy averaged over the
 // mini-batch (eqs. 1-2, 4), together with its backward pass.
 //
-// The logits are produced once by an MFMA GEMM with the bias fused in; one
-// workgroup per frame then computes max and sum-of-exponentials with an
-// online (running-max) reduction across 64-lane wavefronts, the frame loss,
-// and overwrites the logits in place with ds = scale * (softmax - onehot),
-// which feeds the three backward GEMMs (dW_s, dz, and via dz dW_l and dy).
+// bf16 path: the logits are float32 values that stay in the product's
+// accumulators (see the fused products below); ds = scale * (softmax -
+// onehot) leaves in bf16 and feeds the three backward GEMMs (dW_s, dz, and
+// via dz dW_l and dy).  float32 path: one product writes the logits, then
+// one workgroup per frame reduces the row and overwrites it with ds.
 #include <math.h>
 
 #include <type_traits>
@@ -24,16 +24,22 @@ __device__ __forceinline__ void lse_combine(float& m, float& s, float m2, float 
   s = a + b;
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void softmax_ce_rows_kernel(T* __restrict__ S, int K, int Kp,
+// float32 path, any K: logits S (row pitch Kp) -> ds of type TO written in
+// place at the start of each row (for TO = float, ds replaces the logits).  Three passes over the row: (max, sum) with a
+// running maximum, the frame loss, then ds in 256-wide chunks with a barrier
+// between a chunk's reads and its writes (a bf16 write at column k overlaps
+// float column k/2, which an earlier or the same chunk has read).
+template <typename TO>
+__global__ __launch_bounds__(256) void softmax_ce_rows_kernel(float* __restrict__ S, int K, int Kp,
                                                               const int32_t* __restrict__ labels,
                                                               float scale, float* __restrict__ rowloss) {
   const int64_t m = blockIdx.x;
-  T* s = S + m * Kp;
+  const float* s = S + m * Kp;
+  TO* o = (TO*)(S + m * Kp);
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   float mx = -INFINITY, sm = 0.f;
   for (int k = tid; k < K; k += 256) {
-    const float v = to_f32(s[k]);
+    const float v = s[k];
     if (v > mx) {
       sm = sm * __expf(mx - v) + 1.f;
       mx = v;
@@ -47,7 +53,7 @@ __global__ __launch_bounds__(256) void softmax_ce_rows_kernel(T* __restrict__ S,
     const float s2 = __shfl_xor(sm, off);
     lse_combine(mx, sm, m2, s2);
   }
-  __shared__ float wm[4], ws[4], sh_lse, sh_sl;
+  __shared__ float wm[4], ws[4], sh_lse;
   if (lane == 0) { wm[wid] = mx; ws[wid] = sm; }
   __syncthreads();
   if (tid == 0) {
@@ -56,116 +62,203 @@ __global__ __launch_bounds__(256) void softmax_ce_rows_kernel(T* __restrict__ S,
     const float lse = M0 + __logf(S0);
     const int lab = labels[m];
     // an out-of-range label is not read (the loss becomes NaN instead)
-    const float sl = (lab >= 0 && lab < K) ? to_f32(s[lab]) : __int_as_float(0x7fc00000);
+    const float sl = (lab >= 0 && lab < K) ? s[lab] : __int_as_float(0x7fc00000);
     sh_lse = lse;
-    sh_sl = sl;
     rowloss[m] = lse - sl;
   }
   __syncthreads();
   const float lse = sh_lse;
   const int lab = labels[m];
-  for (int k = tid; k < Kp; k += 256) {
+  for (int k0 = 0; k0 < Kp; k0 += 256) {
+    const int k = k0 + tid;
     float g = 0.f;
-    if (k < K) g = scale * (__expf(to_f32(s[k]) - lse) - (k == lab ? 1.f : 0.f));
-    s[k] = from_f32<T>(g);
+    if (k < K) g = scale * (__expf(s[k] - lse) - (k == lab ? 1.f : 0.f));
+    __syncthreads();
+    if (k < Kp) o[k] = from_f32<TO>(g);
   }
 }
 
-// Single-pass variant for rows of up to SM_TPB*8*NV classes: each thread
-// keeps its NV 8-element vectors of the row in registers, so the logits are
-// read once and ds written once.  512 threads per row (eight waves, 64
-// values each at 32000 classes) measured 25% faster on MI355X than 256
-// threads with twice the registers, and than 1024.  The row is held as
-// loaded (bf16) and the exponentials are evaluated twice, which halves the
-// registers: at eight waves per SIMD (64 VGPRs, a few spilled) four rows
-// per CU are in flight, 96 -> 79 us for 2688 rows of 32000 classes (the
-// float32 exponentials held instead: 118 VGPRs, two rows per CU).
-#define SM_TPB 512
-template <typename T, int NV>
-__global__ __launch_bounds__(SM_TPB) __attribute__((amdgpu_waves_per_eu(8, 8))) void softmax_ce_rows_reg_kernel(T* __restrict__ S, int K, int Kp,
-                                                                     const int32_t* __restrict__ labels,
-                                                                     float scale, float* __restrict__ rowloss) {
-  // One pass over the row: each thread keeps its logits' exponentials
-  // e = exp(s - m_t) against its own maximum m_t and their sum; the
-  // (maximum, sum) pairs are combined across the workgroup (one barrier), and
-  // ds = scale * (e * exp(m_t - m) / sum - [k == label]).  The thread holding
-  // the label's logit writes the frame loss logsumexp - s[label].
-  const int64_t m = blockIdx.x;
-  T* s = S + m * Kp;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int nvec = Kp / 8;
-  const int lab = labels[m];
-  // the row stays in registers as loaded (eight bf16 per vector, half the
-  // registers of float32 exponentials, so twice the rows per CU); the
-  // exponentials are evaluated again for the output
-  uint4 raw[NV];
-  auto logit = [&](int i, int j) {   // -inf past the K classes
-    const int k = (tid + SM_TPB * i) * 8 + j;
-    return k < K ? to_f32(((const T*)&raw[i])[j]) : -INFINITY;
-  };
-  float mt = -INFINITY, slab = 0.f;
-  bool have_lab = false;
+// ---------------------------------------------------------------------------
+// bf16 path: the logits never leave the product's accumulators.
+//
+// Two products with the same tiling compute the logits transposed, s^T =
+// W_s z^T (rows: classes, columns: frames), so that each lane holds four
+// consecutive classes of one frame.  The first product's epilogue reduces
+// each wave's tile to (max, sum of exp(s - max)) per frame and class strip
+// (the wave's rows); a small kernel combines the strips into each frame's
+// log-sum-exp; the second product's epilogue recomputes the same float32
+// logits and writes ds = scale * (softmax - onehot) as bf16 (8 bytes per
+// lane) and the frame loss lse - s[label].  The logits are thus exact
+// float32 values (bf16 storage of a logit of 20 would carry an error of up
+// to 0.06 into the loss and softmax) and 344 MB of float32 logits are neither
+// written nor read back.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void lse_pair(float& m, float& s, float m2, float s2) {
+  const float mx = fmaxf(m, m2);
+  s = (m == -INFINITY ? 0.f : s * __expf(m - mx)) + (m2 == -INFINITY ? 0.f : s2 * __expf(m2 - mx));
+  m = mx;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+// sum over the 16 lanes of a DPP row, in every lane of the row
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_mov<0xB1>(v);    // quad_perm [1,0,3,2]
+  v += dpp_mov<0x4E>(v);    // quad_perm [2,3,0,1]
+  v += dpp_mov<0x141>(v);   // row_half_mirror
+  v += dpp_mov<0x140>(v);   // row_mirror
+  return v;
+}
+
+// First product: per (frame, strip of `srows` classes) maximum and sum.
+struct EpiLogitStats {
+  const float* bias;   // b_s [K]
+  float2* stats;       // [M][nstrip] (maximum, sum of exp(s - maximum))
+  int64_t K, M;        // classes (product rows), frames (product columns)
+  int nstrip, srows;
+  template <int FM, int FN>
+  __device__ __forceinline__ void apply(int, int, int64_t mw, int64_t nw, f32x4 (&acc)[FM][FN], int lane) const {
+    if (mw >= K) return;
+    const int strip = (int)(mw / srows);
+    float bv[FM][4];
 #pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const int c = tid + SM_TPB * i;
-    raw[i] = c < nvec ? *(const uint4*)(s + (int64_t)c * 8) : make_uint4(0u, 0u, 0u, 0u);
-  }
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    if (tid + SM_TPB * i >= nvec) continue;
+      for (int r = 0; r < 4; ++r) {
+        const int64_t k = mw + i * 16 + (lane >> 4) * 4 + r;
+        bv[i][r] = k < K ? bias[k] : -INFINITY;
+      }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float x = logit(i, j);
-      mt = fmaxf(mt, x);
-      if ((tid + SM_TPB * i) * 8 + j == lab) { slab = x; have_lab = true; }
+    for (int j = 0; j < FN; ++j) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, acc[i][j][r] + bv[i][r]);
+      float sm = 0.f;
+      if (mx != -INFINITY) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sm += __expf(acc[i][j][r] + bv[i][r] - mx);
+      }
+      // the four lane groups hold the other classes of the same frame
+      lse_pair(mx, sm, __shfl_xor(mx, 16), __shfl_xor(sm, 16));
+      lse_pair(mx, sm, __shfl_xor(mx, 32), __shfl_xor(sm, 32));
+      const int64_t f = nw + j * 16 + (lane & 15);
+      if ((lane >> 4) == 0 && f < M) stats[f * nstrip + strip] = make_float2(mx, sm);
     }
   }
-  float st = 0.f;
-  const float mref = mt == -INFINITY ? 0.f : mt;   // a thread with padding only
-#pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    if (tid + SM_TPB * i >= nvec) continue;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) st += __expf(logit(i, j) - mref);   // exp(-inf) = 0 for padding
+};
+
+// Per frame: log-sum-exp of its strips (one wave per frame); a frame whose
+// label is outside [0, K) gets a NaN loss (its label is never read).
+__global__ __launch_bounds__(256) void logit_lse_kernel(const float2* __restrict__ stats, int nstrip, int64_t M,
+                                                        const int32_t* __restrict__ labels, int K,
+                                                        float* __restrict__ lse, float* __restrict__ rowloss) {
+  const int64_t m = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (m >= M) return;
+  float mx = -INFINITY, sm = 0.f;
+  for (int i = lane; i < nstrip; i += 64) {
+    const float2 p = stats[m * nstrip + i];
+    lse_pair(mx, sm, p.x, p.y);
   }
-  // combine (max, sum) pairs: within the wave by shuffles, then the waves
-  float mw = mt, sw = st;
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    const float mo = __shfl_xor(mw, off), so = __shfl_xor(sw, off);
-    const float mn = fmaxf(mw, mo);
-    sw = (mw == -INFINITY ? 0.f : sw * __expf(mw - mn)) + (mo == -INFINITY ? 0.f : so * __expf(mo - mn));
-    mw = mn;
-  }
-  constexpr int NW = SM_TPB / 64;
-  __shared__ float rm[NW], rs[NW];
-  if (lane == 0) { rm[wid] = mw; rs[wid] = sw; }
-  __syncthreads();
-  float mx = -INFINITY;
-#pragma unroll
-  for (int q = 0; q < NW; ++q) mx = fmaxf(mx, rm[q]);
-  float sum = 0.f;
-#pragma unroll
-  for (int q = 0; q < NW; ++q) sum += rm[q] == -INFINITY ? 0.f : rs[q] * __expf(rm[q] - mx);
-  const float lse = mx + __logf(sum);
-  if (have_lab) rowloss[m] = lse - slab;
-  // an out-of-range label is not read (the loss becomes NaN instead)
-  if (tid == 0 && !(lab >= 0 && lab < K)) rowloss[m] = __int_as_float(0x7fc00000);
-  const float f = scale * __expf(mref - mx) / sum;
-#pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const int c = tid + SM_TPB * i;
-    if (c >= nvec) continue;
-    uint4 out;
-    T* e = (T*)&out;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int k = c * 8 + j;
-      e[j] = from_f32<T>(k < K ? __expf(logit(i, j) - mref) * f - (k == lab ? scale : 0.f) : 0.f);
-    }
-    *(uint4*)(s + (int64_t)c * 8) = out;
+  for (int off = 32; off > 0; off >>= 1) lse_pair(mx, sm, __shfl_xor(mx, off), __shfl_xor(sm, off));
+  if (lane == 0) {
+    lse[m] = mx + __logf(sm);
+    const int lab = labels[m];
+    if (!(lab >= 0 && lab < K)) rowloss[m] = __int_as_float(0x7fc00000);
   }
 }
+
+// Second product: ds (bf16, [M][Kp], zero in the padding classes), the
+// frame loss at the label's class, and the column sums of ds over the wave's
+// frames (db_s partials, one row per block of `fcols` frames, summed in a
+// fixed order).  Lane group g = lane / 16 holds classes 4g .. 4g+3 of each
+// 16-class fragment; for a fragment pair (i, i+1) the groups g and g ^ 1
+// swap halves so that each lane stores 8 consecutive classes (16 bytes):
+// even groups classes 8(g/2) .. +7 of fragment i, odd groups those of i+1.
+struct EpiSoftmaxDs {
+  const float* bias;
+  const float* lse;
+  const int32_t* labels;
+  bf16* ds;
+  float* rowloss;
+  float* dbp;          // [cdiv(M, fcols)][K] column-sum partials
+  float scale;
+  int64_t K, Kp, M;
+  int fcols;
+  template <int FM, int FN>
+  __device__ __forceinline__ void apply(int, int, int64_t mw, int64_t nw, f32x4 (&acc)[FM][FN], int lane) const {
+    static_assert(FM % 2 == 0, "fragment pairs");
+    const int g = lane >> 4;
+    float bv[FM][4];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t k = mw + i * 16 + g * 4 + r;
+        bv[i][r] = k < K ? bias[k] : 0.f;
+      }
+    float csum[FM][4];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) csum[i][r] = 0.f;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int64_t f = nw + j * 16 + (lane & 15);
+      const bool fok = f < M;
+      const float L = fok ? lse[f] : 0.f;
+      const int lab = fok ? labels[f] : -1;
+      uint2 pk[FM];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        bf16 e[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t k = mw + i * 16 + g * 4 + r;
+          const float sv = acc[i][j][r] + bv[i][r];
+          const float v = (fok && k < K) ? __expf(sv - L) * scale - (k == lab ? scale : 0.f) : 0.f;
+          csum[i][r] += v;
+          e[r] = (bf16)v;
+          if (fok && k == lab) rowloss[f] = L - sv;
+        }
+        pk[i] = *(const uint2*)e;
+      }
+#pragma unroll
+      for (int i = 0; i < FM; i += 2) {
+        const uint2 send = (g & 1) ? pk[i] : pk[i + 1];
+        const uint2 got = make_uint2((uint32_t)__shfl_xor((int)send.x, 16), (uint32_t)__shfl_xor((int)send.y, 16));
+        const uint4 v = (g & 1) ? make_uint4(got.x, got.y, pk[i + 1].x, pk[i + 1].y)
+                                : make_uint4(pk[i].x, pk[i].y, got.x, got.y);
+        const int64_t k0 = mw + (i + (g & 1)) * 16 + (g >> 1) * 8;
+        if (fok && k0 < Kp) *(uint4*)(ds + f * Kp + k0) = v;
+      }
+    }
+    // column sums over the wave's frames: across the 16 lanes of a group
+    // with DPP adds (lane ^ 1, lane ^ 2 within quads, then the half-row and
+    // row mirrors), a fixed order that leaves the sum in every lane
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) csum[i][r] = row16_sum(csum[i][r]);
+    if ((lane & 15) == 0 && nw < M) {
+      float* row = dbp + (nw / fcols) * K;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t k = mw + i * 16 + g * 4 + r;
+          if (k < K) row[k] = csum[i][r];
+        }
+    }
+  }
+};
 
 // loss = scale * sum of per-frame losses, in a fixed order.
 __global__ __launch_bounds__(256) void loss_sum_kernel(const float* __restrict__ rowloss, int64_t M,
@@ -193,7 +286,6 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
   const int64_t M = lo.M;
   const int P = lo.P, K = lo.K, Kp = lo.Kp, H2 = 2 * lo.H;
   T* Z = (T*)(hws + lo.Z);
-  T* S = (T*)(hws + lo.S);
   float* RL = (float*)(hws + lo.RL);
   float* DZ = (float*)(hws + lo.DZ);
   T* DZT = (T*)(hws + lo.DZT);
@@ -212,39 +304,50 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
     gemm_launch<T, true, true, V, V>("gemm_z", s, opnd(ytop, H2, H2, M), opnd(W + lo.Wl, H2, H2, P), M,
                                      P, H2, 1, 1, epi_store<T>(Z, P, M, P, 0, 0, theta + lo.bl));
   }
-  // s = z W_s^T + b_s
-  gemm_launch<T, true, true, V, V>("gemm_logits", s, opnd(Z, P, P, M), opnd(W + lo.Ws, P, P, K), M,
-                                   K, P, 1, 1, epi_store<T>(S, Kp, M, K, 0, 0, theta + lo.bs));
-  // per-frame loss and ds (in place)
-  {
-    // ds in place; rows of up to 32768 classes stay in registers (bf16, 16 B vectors)
-    const int nv = (int)cdiv(Kp / 8, SM_TPB);
-    const dim3 g((unsigned)M), b(SM_TPB), b256(256);
-    if (std::is_same<T, bf16>::value && nv <= 8) {
-      if (nv <= 1)
-        BLSTM_LAUNCH("softmax_ce_rows", (softmax_ce_rows_reg_kernel<bf16, 1>), g, b, 0, s, (bf16*)S, K, Kp, labels, scale, RL);
-      else if (nv <= 2)
-        BLSTM_LAUNCH("softmax_ce_rows", (softmax_ce_rows_reg_kernel<bf16, 2>), g, b, 0, s, (bf16*)S, K, Kp, labels, scale, RL);
-      else if (nv <= 4)
-        BLSTM_LAUNCH("softmax_ce_rows", (softmax_ce_rows_reg_kernel<bf16, 4>), g, b, 0, s, (bf16*)S, K, Kp, labels, scale, RL);
-      else
-        BLSTM_LAUNCH("softmax_ce_rows", (softmax_ce_rows_reg_kernel<bf16, 8>), g, b, 0, s, (bf16*)S, K, Kp, labels, scale, RL);
-    } else {
-      BLSTM_LAUNCH("softmax_ce_rows", softmax_ce_rows_kernel<T>, g, b256, 0, s, S, K, Kp, labels, scale, RL);
-    }
+  constexpr bool lp = std::is_same<T, bf16>::value;
+  T* DS = (T*)(hws + lo.S);
+  if constexpr (lp) {
+    // logits transposed (classes x frames) twice: strip statistics, then ds,
+    // the frame losses and the db_s partials
+    const Opnd Aw = opnd(W + lo.Ws, P, P, K), Bz = opnd(Z, P, P, M);
+    const bool kc = kc_eligible(Aw, Bz, P, true, true);
+    const int srows = (kc && kc_tall(K, M, 1, 1)) ? KcTileTall::BM / KcTileTall::WM : KcTile::BM / KcTile::WM;
+    const int fcols = kc ? KcTile::BN / KcTile::WN : GemmCfgK32::BN / GemmCfgK32::WN;
+    static_assert(KcTile::BM / KcTile::WM == GemmCfgK32::BM / GemmCfgK32::WM, "strip rows of the fallback tiles");
+    static_assert(KcTile::BN / KcTile::WN == KcTileTall::BN / KcTileTall::WN, "frame columns of the kc tiles");
+    const int nstrip = (int)cdiv(K, srows);
+    float2* stats = (float2*)(hws + lo.LST);
+    float* lse = (float*)(hws + lo.LSE);
+    float* dbp = (float*)(hws + lo.LDB);
+    EpiLogitStats e1{theta + lo.bs, stats, K, M, nstrip, srows};
+    gemm_launch<T, true, true, V, V>("gemm_logits", s, Aw, Bz, K, M, P, 1, 1, e1);
+    BLSTM_LAUNCH("logit_lse", logit_lse_kernel, dim3((unsigned)cdiv(M, 4)), dim3(256), 0, s, stats, nstrip, M, labels,
+                 K, lse, RL);
+    EpiSoftmaxDs e2{theta + lo.bs, lse, labels, (bf16*)DS, RL, dbp, scale, K, Kp, M, fcols};
+    gemm_launch<T, true, true, V, V>("gemm_logits_ds", s, Aw, Bz, K, M, P, 1, 1, e2);
+    BLSTM_LAUNCH("loss_sum", loss_sum_kernel, dim3(1), dim3(256), 0, s, RL, M, scale, loss);
+    // db_s = sum of the per-frame-block partials, in order
+    colsum_parts("colsum_dbs", s, dbp, (int)cdiv(M, fcols), K, K, 0, grad + lo.bs, nullptr);
+  } else {
+    // s = z W_s^T + b_s, then loss and ds in place
+    float* S = (float*)(hws + lo.S);
+    gemm_launch<T, true, true, V, V>("gemm_logits", s, opnd(Z, P, P, M), opnd(W + lo.Ws, P, P, K), M,
+                                     K, P, 1, 1, epi_store<float>(S, Kp, M, K, 0, 0, theta + lo.bs));
+    BLSTM_LAUNCH("softmax_ce_rows", softmax_ce_rows_kernel<T>, dim3((unsigned)M), dim3(256), 0, s, S, K, Kp, labels,
+                 scale, RL);
+    BLSTM_LAUNCH("loss_sum", loss_sum_kernel, dim3(1), dim3(256), 0, s, RL, M, scale, loss);
+    // db_s = sum over frames of ds
+    colsum<T>("colsum_dbs", s, DS, M, K, Kp, csp, K, 0, grad + lo.bs, nullptr);
   }
-  BLSTM_LAUNCH("loss_sum", loss_sum_kernel, dim3(1), dim3(256), 0, s, RL, M, scale, loss);
-  // db_s = sum over frames of ds
-  colsum<T>("colsum_dbs", s, S, M, K, Kp, csp, K, 0, grad + lo.bs, nullptr);
   // dW_s = ds^T z
-  gemm_f32<T, false, false, V, V>("gemm_dws", s, opnd(S, Kp, Kp, M), opnd(Z, P, P, M), K, P, M, 1,
+  gemm_f32<T, false, false, V, V>("gemm_dws", s, opnd(DS, Kp, Kp, M), opnd(Z, P, P, M), K, P, M, 1,
                                   lo.sp_dWs, grad + lo.Ws, P, 0, part);
   // bf16: W_s^T and W_l^T copies make dz and dy K-contiguous products
   // dz = ds W_s (float32 and a low-precision copy for the next products);
   // W_s [K][P] is the MN-contiguous operand as it lies (the direct-to-LDS
   // kernel reads it with transposing LDS reads; measured faster than
   // transposing W_s each step first)
-  gemm_f32<T, true, false, V, V>("gemm_dz", s, opnd(S, Kp, Kp, M), opnd(W + lo.Ws, P, P, K), M, P,
+  gemm_f32<T, true, false, V, V>("gemm_dz", s, opnd(DS, Kp, Kp, M), opnd(W + lo.Ws, P, P, K), M, P,
                                  K, 1, lo.sp_dz, DZ, P, 0, part, DZT, P);
   // db_l = sum over frames of dz
   colsum<float>("colsum_dbl", s, DZ, M, P, P, csp, P, 0, grad + lo.bl, nullptr);

@@ -411,12 +411,13 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
   const int64_t M = lo.M;
   const int H = lo.H, B = lo.B;
   bool xch_cleared = false;   // exchange words cleared once per call (persist_clear)
-  // the recurrence status covers this forward call and the backward call
-  // after it: reset by the persistent path's exchange clear, else here
+  // the recurrence status block is initialised on first use (by the
+  // persistent path's exchange clear, else here); its flag is sticky until
+  // blstm_recurrence_ok reads it
   const bool persist = use_persistent<T>(H, lo.T, false, s);
   bool status_cleared = false;
   if (!persist) {
-    if (persist_status_clear((int*)(ws + lo.SYNC), s) != hipSuccess) return blstm_check_launch("blstm_fwd");
+    if (persist_status_init((int*)(ws + lo.SYNC), s) != hipSuccess) return blstm_check_launch("blstm_fwd");
     status_cleared = true;
   }
   T* X0 = (T*)(ws + lo.X0);
@@ -455,7 +456,7 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
       }
       if (!status_cleared) {
         (void)hipGetLastError();
-        if (persist_status_clear((int*)(ws + lo.SYNC), s) != hipSuccess) return blstm_check_launch("blstm_fwd");
+        if (persist_status_init((int*)(ws + lo.SYNC), s) != hipSuccess) return blstm_check_launch("blstm_fwd");
         status_cleared = true;
       }
       if (xch_cleared && persist_layer(false, pa, s) == hipSuccess) continue;
@@ -691,14 +692,17 @@ extern "C" int blstm_recurrence_ok(const blstm_dims* dims, const void* act_ws, h
   if (rc) return rc;
   if (!act_ws) return blstm_fail(BLSTM_EINVAL, "blstm_recurrence_ok: NULL act_ws");
   int gave_up = 0;
-  if (hipMemcpyAsync(&gave_up, (const char*)act_ws + lo.SYNC, sizeof(int), hipMemcpyDeviceToHost, stream) !=
-          hipSuccess ||
+  int* status = (int*)((char*)act_ws + lo.SYNC);
+  if (hipMemcpyAsync(&gave_up, status, sizeof(int), hipMemcpyDeviceToHost, stream) != hipSuccess ||
       hipStreamSynchronize(stream) != hipSuccess)
+    return blstm_fail(BLSTM_EHIP, "blstm_recurrence_ok: %s", hipGetErrorString(hipGetLastError()));
+  if (persist_status_reset(status, stream) != hipSuccess)
     return blstm_fail(BLSTM_EHIP, "blstm_recurrence_ok: %s", hipGetErrorString(hipGetLastError()));
   if (gave_up)
     return blstm_fail(BLSTM_EHIP,
-                      "blstm_recurrence_ok: a recurrent exchange wait gave up (the workgroups of a persistent "
-                      "launch were not all resident; set ADPSGD_BLSTM_COOPERATIVE=1 on a shared device)");
+                      "blstm_recurrence_ok: a recurrent exchange wait gave up since the last query (the workgroups "
+                      "of a persistent launch were not all resident; set ADPSGD_BLSTM_COOPERATIVE=1 on a shared "
+                      "device)");
   return BLSTM_OK;
 }
 

@@ -857,12 +857,33 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   }
 }
 
-// status: cleared too when non-null
+// The recurrence status block (at the end of the activation workspace): an
+// int set to 1 by any exchange wait that gives up, and a 64-bit tag that
+// says whether the block has been initialised.  The flag is sticky: only
+// status_reset_kernel (blstm_recurrence_ok) clears it, and the forward pass
+// initialises it only when the tag is missing (a fresh workspace), so one
+// query covers every call since the previous query.
+#define STATUS_TAG 0x5354415455535f31ull   // "STATUS_1"
+
+__device__ __forceinline__ void status_init_if_fresh(int* status) {
+  uint64_t* tag = (uint64_t*)(status + 2);
+  if (*tag != STATUS_TAG) {
+    *status = 0;
+    *tag = STATUS_TAG;
+  }
+}
+
+// exchange words cleared; status (if non-null) initialised when fresh
 __global__ __launch_bounds__(256) void clear_exchange_kernel(uint4* p, int64_t n16, int* status) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
     p[i] = make_uint4(0u, 0u, 0u, 0u);
-  if (status && blockIdx.x == 0 && threadIdx.x == 0) *status = 0;
+  if (status && blockIdx.x == 0 && threadIdx.x == 0) status_init_if_fresh(status);
+}
+
+__global__ void status_reset_kernel(int* status) {
+  *status = 0;
+  *(uint64_t*)(status + 2) = STATUS_TAG;
 }
 
 // ---------------------------------------------------------------------------
@@ -987,8 +1008,7 @@ hipError_t persist_clear(bool backward, const PersistArgs& a, hipStream_t s) {
   int MB, chunk;
   if (!persist_plan(backward, a.H, a.B, &MB, &chunk)) return hipErrorInvalidValue;
   // both exchange slots start without any valid step number; the forward's
-  // clear also resets the status word (it covers the forward call and the
-  // backward call after it)
+  // clear also initialises the status block of a fresh workspace
   const int64_t words = backward ? (int64_t)2 * 2 * ((chunk + 3) / 4) * (a.H / PU) * a.H
                                  : (int64_t)2 * 2 * chunk * (a.H / 4);
   const int64_t n16 = words / 2;
@@ -997,8 +1017,13 @@ hipError_t persist_clear(bool backward, const PersistArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t persist_status_clear(int* status, hipStream_t s) {
+hipError_t persist_status_init(int* status, hipStream_t s) {
   hipLaunchKernelGGL(clear_exchange_kernel, dim3(1), dim3(64), 0, s, (uint4*)nullptr, (int64_t)0, status);
+  return hipGetLastError();
+}
+
+hipError_t persist_status_reset(int* status, hipStream_t s) {
+  hipLaunchKernelGGL(status_reset_kernel, dim3(1), dim3(1), 0, s, status);
   return hipGetLastError();
 }
 

@@ -18,7 +18,7 @@ struct PersistArgs {
   bf16* DAT;          // backward, optional: da also frame-contiguous [8H][M] (needs B % 8 == 0)
   float* DBP;         // backward, optional: sums of da over 16-row blocks and all steps [cdiv(B,16)][8H]
   int64_t M;          // frames, T*B (DAT row length)
-  int* status;        // cleared by the forward pass's persist_clear; 1 if a wait ever gave up
+  int* status;        // recurrence status block (sticky flag, see persist_status_reset)
   uint32_t tag;       // caller: the layer's position in the order the call runs the layers
   int Tn, B, H;
   int b0, rows, NS;   // batch chunk handled by one launch (filled in by persist_layer)
@@ -44,12 +44,19 @@ bool persist_supported(int H, int T);
 // Whether the persistent BPTT of a layer reads W_hh^T (PersistArgs::WT): only
 // when its workgroups take more than one 16-row block (W_hh slice in LDS).
 bool persist_bwd_needs_wt(int H, int B);
-// Clears the exchange words (and, for the forward, the status word); once
-// per forward or backward call, before its first persist_layer.
+// Status block (PERSIST_STATUS_BYTES at the end of the activation
+// workspace): an int flag set by any exchange wait that gives up, and a tag
+// that marks the block initialised.  The flag is sticky across calls.
+#define PERSIST_STATUS_BYTES 256
+// Clears the exchange words (and, for the forward, initialises the status
+// block of a fresh workspace); once per forward or backward call, before
+// its first persist_layer.
 hipError_t persist_clear(bool backward, const PersistArgs& a, hipStream_t s);
-// Clears the status word alone (a forward call that does not take the
-// persistent path, or whose exchange clear failed).
-hipError_t persist_status_clear(int* status, hipStream_t s);
+// Initialises the status block if it is fresh (a forward call that does not
+// take the persistent path, or whose exchange clear failed).
+hipError_t persist_status_init(int* status, hipStream_t s);
+// Clears the flag (after blstm_recurrence_ok has read it).
+hipError_t persist_status_reset(int* status, hipStream_t s);
 // Runs every step of one layer, both directions; hipSuccess or the error of
 // the launch that failed.  The layers of one call carry tags 0, 1, 2, ...
 // in the order they run (an exchange word tells its launch from the two

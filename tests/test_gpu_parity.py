@@ -45,7 +45,7 @@ def block_errors(g_gpu, g_ref, dims):
 
 
 def run_step_and_compare(shape, precision, tol, dist="uniform", seed=0, check_update=True, edit_theta=None,
-                         check=None, only=None):
+                         check=None):
     from paper_1907_05701_amd.step import LearnerStep
     say(f"[parity] shape={shape} precision={precision} seed={seed}")
     dims = ref.Dims(**shape)
@@ -74,7 +74,7 @@ def run_step_and_compare(shape, precision, tol, dist="uniform", seed=0, check_up
         check(st)
     worst = max(errs.items(), key=lambda kv: kv[1])
     say(f"[parity] loss gpu={loss:.7f} ref={want['loss']:.7f}; worst {worst[0]}={worst[1]:.3e}")
-    bad = {k: v for k, v in errs.items() if (only is None or k in only) and not v <= tol}
+    bad = {k: v for k, v in errs.items() if not v <= tol}
     assert not bad, bad
     if check_update:
         lr = 0.1
@@ -175,23 +175,38 @@ def test_stress_t64_b1024_replicated(gpu_lib):
     run_replicated_and_compare(dict(L=6, D=260, H=512, P=256, K=32000, T=64, B=16), 64, BF16_TOL, seed=21)
 
 
+def _bf16_model():
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    import bf16_path_model
+    return bf16_path_model
+
+
+def _blockwise(g, want, blocks):
+    return {str(k): rel(g[o:o + int(np.prod(s))], want[o:o + int(np.prod(s))]) for k, (o, s) in blocks.items()}
+
+
 def test_saturated_cells_bf16(gpu_lib):
     """Cells driven into saturation so that most outputs h are +-1.0 in bf16
     (gate biases i, f: +6, g: +2, o: +7: the cells charge by about one per
     step and o tanh c rounds to 1): the recurrent exchange packs h with a tag
-    in bit 14 of each bf16, which is free for |h| <= 1.  The forward outputs,
-    which the exchanged h determine, are compared with the oracle (the
-    saturated recurrence is contractive: a 2^-9 relative perturbation of the
-    parameters moves y_top by 4e-5 in the float64 oracle).  The gradients are
-    not: in this regime they are small differences of large terms, and the
-    bf16 forward alone moves them by several per cent (float64 emulation of
-    the oracle: the input projection rounded to bf16 moves the layer-0 W_ih
-    gradient by 5 %, the recurrent h by 3.7 %; measured here: the persistent
-    and the per-step kernels agree with each other, 15 % from the oracle,
-    and the float32 path is within 2e-5)."""
+    in bit 14 of each bf16, which is free for |h| <= 1.
+
+    At this point the gradient is badly conditioned: the exact gradient at
+    the bf16 copy of the weights is several per cent from the one at theta
+    (pinned on the CPU in test_bf16_model.py), so no path with bf16 operands
+    meets the 2e-2 bar here.  Every block is compared instead with the bound
+    that the bf16 rounding points themselves give: a float64 model of the
+    path's rounding points (tests/bf16_path_model.py) is E from the oracle
+    per block; the GPU must be within max(2e-2, 1.25 E) of the oracle in
+    every block, and closer to that model than the model is to the oracle
+    (so what remains is the rounding the model names, not a defect)."""
+    bm = _bf16_model()
+    shape = dict(L=2, D=40, H=512, P=32, K=100, T=21, B=16)
+    dims = ref.Dims(**shape)
+    H = dims.H
+
     def edit(theta, dims):
         blocks, _ = ref.param_layout(dims)
-        H = dims.H
         for key, (off, shp) in blocks.items():
             if key[0] == "b_ih":   # gates i, f, g, o
                 b = theta[off:off + int(np.prod(shp))]
@@ -200,14 +215,107 @@ def test_saturated_cells_bf16(gpu_lib):
                 b[3 * H:4 * H] = 7.0
         return theta
 
-    def saturated(st):
+    got = {}
+
+    def keep(st):
         frac = float((st.y_top.float().abs() == 1.0).float().mean())
         say(f"[parity] fraction of top-layer h equal to +-1: {frac:.3f}")
         assert frac > 0.3
+        got["grad"] = st.grad.cpu().numpy()
+        got["loss"] = float(st.loss.cpu()[0])
 
-    errs = run_step_and_compare(dict(L=2, D=40, H=512, P=32, K=100, T=21, B=16), "bf16", BF16_TOL, seed=31,
-                                edit_theta=edit, check=saturated, only=("loss", "y_top"), check_update=False)
-    say(f"[parity] saturated: loss {errs['loss']:.2e}, y_top {errs['y_top']:.2e}")
+    errs = run_step_and_compare(shape, "bf16", 1e9, seed=31, edit_theta=edit, check=keep, check_update=False)
+    theta = edit(inputs.params(ref.param_count(dims), seed=31).copy(), dims)
+    x = inputs.features(dims.T, dims.B, dims.D, seed=32)
+    lab = inputs.labels(dims.T, dims.B, dims.K, seed=33)
+    want = ref.learner_gradient(theta, dims, x, lab)
+    model = bm.learner_gradient(theta, shape, x, lab)
+    blocks, _ = ref.param_layout(dims)
+    e_model = _blockwise(model["grad"], want["grad"], blocks)
+    e_gpu_model = _blockwise(got["grad"], model["grad"], blocks)
+    bad = {}
+    for k, e in e_model.items():
+        bound = max(BF16_TOL, 1.25 * e)
+        say(f"[parity] {k}: gpu {errs[k]:.2e} model {e:.2e} gpu-model {e_gpu_model[k]:.2e} bound {bound:.2e}")
+        if not (errs[k] <= bound and (e_gpu_model[k] <= BF16_TOL or e_gpu_model[k] < e)):
+            bad[k] = (errs[k], e, e_gpu_model[k])
+    assert not bad, bad
+    assert errs["loss"] <= BF16_TOL and errs["y_top"] <= BF16_TOL, errs
+
+
+def _peaked_head(gamma, seed=60):
+    """Head-alone inputs at the paper's head size whose softmax is peaked as
+    in a trained model: W_s scaled by gamma, each frame labelled with the
+    class of its largest exact logit (the loss is then far below ln K)."""
+    shape = dict(L=1, D=8, H=512, P=256, K=32000, T=21, B=16)
+    dims = ref.Dims(**shape)
+    n = ref.param_count(dims)
+    blocks, _ = ref.param_layout(dims)
+    theta = inputs.params(n, seed=seed).copy()
+    off, shp = blocks["W_s"]
+    theta[off:off + int(np.prod(shp))] *= np.float32(gamma)
+    y = inputs.hidden_states(dims.T, dims.B, 2 * dims.H, seed=seed + 1)
+    p = ref.unflatten(theta, dims)
+    logits = (y.reshape(-1, 2 * dims.H).astype(np.float64) @ p["W_l"].T + p["b_l"]) @ p["W_s"].T + p["b_s"]
+    lab = logits.argmax(axis=1).reshape(dims.T, dims.B).astype(np.int32)
+    return shape, dims, theta, y, lab
+
+
+def _head_on_gpu(shape, theta, y, lab):
+    from paper_1907_05701_amd.step import LearnerStep
+    dims = ref.Dims(**shape)
+    st = LearnerStep(**shape, precision="bf16")
+    st.load(theta, np.zeros((dims.T, dims.B, dims.D), np.float32), lab)
+    st.y_top.copy_(torch.from_numpy(y).to(st.act_dtype))
+    st.head()
+    torch.cuda.synchronize()
+    blocks, _ = ref.param_layout(dims)
+    g = st.grad.cpu().numpy()
+    out = {k: g[blocks[k][0]:blocks[k][0] + int(np.prod(blocks[k][1]))].reshape(blocks[k][1])
+           for k in ("W_l", "b_l", "W_s", "b_s")}
+    return float(st.loss.cpu()[0]), out, st.dy_top.cpu().numpy()
+
+
+def test_peaked_softmax_head_bf16(gpu_lib):
+    """The bf16 head where the model is confident (W_s scaled by 8, labels at
+    each frame's largest logit: loss about 0.64 against ln K = 10.4): the
+    logits are kept in float32, so the loss and every head gradient meet the
+    2e-2 bar (with bf16 logits the float64 model of the path gives 3.3e-2)."""
+    shape, dims, theta, y, lab = _peaked_head(8.0)
+    loss_ref, _, dy_ref, g_ref = ref.head_forward_backward(theta, dims, y, lab)
+    assert loss_ref < 0.1 * np.log(dims.K)
+    loss, g, dy = _head_on_gpu(shape, theta, y, lab)
+    errs = {"loss": abs(loss - loss_ref) / loss_ref, "dy_top": rel(dy, dy_ref)}
+    errs.update({k: rel(g[k], g_ref[k]) for k in g})
+    say(f"[peaked] loss gpu={loss:.6f} ref={loss_ref:.6f}; " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    bad = {k: v for k, v in errs.items() if not v <= BF16_TOL}
+    assert not bad, bad
+
+
+def test_very_peaked_softmax_head_bf16(gpu_lib):
+    """W_s scaled by 16 (loss about 0.28, logits up to about 80): here the
+    bf16 operands themselves (weights, z, y) move the head gradients by
+    about 3.7e-2 in the float64 model of the path, so each block is held to
+    max(2e-2, 1.25 x that model's error), and the GPU must be closer to the
+    model than the model is to the oracle."""
+    bm = _bf16_model()
+    shape, dims, theta, y, lab = _peaked_head(16.0)
+    loss_ref, _, dy_ref, g_ref = ref.head_forward_backward(theta, dims, y, lab)
+    loss_m, g_m, dy_m = bm.head_gradient(theta, shape, y, lab)
+    loss, g, dy = _head_on_gpu(shape, theta, y, lab)
+    pairs = {"loss": ((loss, loss_m), loss_ref), "dy_top": ((dy, dy_m), dy_ref)}
+    pairs.update({k: ((g[k], g_m[k]), g_ref[k]) for k in g})
+    bad = {}
+    for k, ((gpu, mod), exact) in pairs.items():
+        if k == "loss":
+            e_gpu, e_mod, e_gm = abs(gpu - exact) / exact, abs(mod - exact) / exact, abs(gpu - mod) / abs(mod)
+        else:
+            e_gpu, e_mod, e_gm = rel(gpu, exact), rel(mod, exact), rel(gpu, mod)
+        bound = max(BF16_TOL, 1.25 * e_mod)
+        say(f"[very peaked] {k}: gpu {e_gpu:.2e} model {e_mod:.2e} gpu-model {e_gm:.2e} bound {bound:.2e}")
+        if not (e_gpu <= bound and (e_gm <= BF16_TOL or e_gm < e_mod)):
+            bad[k] = (e_gpu, e_mod, e_gm)
+    assert not bad, bad
 
 
 def test_long_sequence_bf16(gpu_lib):
@@ -465,3 +573,67 @@ def test_graph_replays_with_persistent_forward(gpu_lib, monkeypatch):
         np.testing.assert_array_equal(replayed.theta.cpu().numpy(), eager.theta.cpu().numpy())
         np.testing.assert_array_equal(replayed.y_top.float().cpu().numpy(), eager.y_top.float().cpu().numpy())
         say(f"[graph+persistent] replay {i} matches, loss {float(eager.loss.cpu()[0]):.6f}")
+
+
+def test_recurrence_status_is_sticky_until_queried(gpu_lib):
+    """The give-up flag (the int32 at act_ws_bytes - 256) set from the host
+    survives the next forward and backward calls, so the query after them
+    fails; the query clears it, and the next query succeeds."""
+    from paper_1907_05701_amd import binding as bd
+    from paper_1907_05701_amd.step import LearnerStep
+    shape = dict(L=2, D=40, H=512, P=32, K=100, T=5, B=16)
+    n = ref.param_count(ref.Dims(**shape))
+    st = LearnerStep(**shape, precision="bf16")
+    theta = inputs.params(n)
+    st.load(theta, inputs.features(5, 16, 40), inputs.labels(5, 16, 100), theta)
+    st.step(0.05)
+    st.check_recurrence()
+    flag = st.act_ws[st.act_ws.numel() - 256:st.act_ws.numel() - 252].view(torch.int32)
+    flag.fill_(1)
+    st.step(0.05)
+    st.step(0.05)
+    torch.cuda.synchronize()
+    with pytest.raises(bd.BlstmError) as ei:
+        st.check_recurrence()
+    assert "gave up" in str(ei.value)
+    assert int(flag.cpu()[0]) == 0
+    st.check_recurrence()
+    st.step(0.05)
+    st.check_recurrence()
+
+
+def test_graph_replays_at_benchmark_shape(gpu_lib):
+    """The benchmark's configuration: the full model at B = 128 captured
+    into one HIP graph (the persistent kernels recorded as plain launches)
+    and replayed three times, with eager work and synchronisation between
+    the replays; each replay must equal the same number of eager steps bit
+    for bit, and the sticky recurrence flag must show no give-up over all
+    replays."""
+    from paper_1907_05701_amd.step import LearnerStep
+    shape = dict(L=6, D=260, H=512, P=256, K=32000, T=21, B=128)
+    dims = ref.Dims(**shape)
+    n = ref.param_count(dims)
+    theta = inputs.params(n)
+    x = inputs.features(dims.T, dims.B, dims.D)
+    lab = inputs.labels(dims.T, dims.B, dims.K, dist="zipf")
+    peer = inputs.peer(theta)
+    eager = LearnerStep(**shape, precision="bf16")
+    eager.load(theta, x, lab, peer)
+    replayed = LearnerStep(**shape, precision="bf16")
+    replayed.load(theta, x, lab, peer)
+    graph = replayed.capture(0.05, steps=2)
+    torch.cuda.synchronize()
+    replayed.load(theta, x, lab, peer)
+    for i in range(3):
+        eager.step(0.05)
+        eager.step(0.05)
+        graph.replay()
+        torch.cuda.synchronize()
+        _ = (eager.theta * 2.0).sum().item()
+        for name in ("theta", "loss", "grad", "y_top"):
+            a = getattr(replayed, name).float().cpu().numpy()
+            b = getattr(eager, name).float().cpu().numpy()
+            np.testing.assert_array_equal(a, b, err_msg=f"replay {i}: {name}")
+        say(f"[graph bench shape] replay {i} matches, loss {float(eager.loss.cpu()[0]):.6f}")
+    replayed.check_recurrence()
+    eager.check_recurrence()

@@ -1,5 +1,6 @@
-"""GPU: the training loop with the learning-rate recipe lowers the loss on
-a fixed synthetic data set (random labels, memorised)."""
+"""GPU: the training loop with the learning-rate recipe (Section 3) follows
+an oracle loop step for step, and lowers the loss on a fixed synthetic data
+set (random labels, memorised)."""
 
 import numpy as np
 import pytest
@@ -33,3 +34,48 @@ def test_loss_decreases_over_epochs(gpu_lib, precision):
     assert np.isfinite(losses).all()
     assert losses[-1] < 0.1 * losses[0], losses
     assert losses[-1] < losses[-2] < losses[-3], losses
+
+
+def test_training_loop_follows_the_oracle_loop(gpu_lib):
+    """The training loop against an oracle loop on the same batches: per
+    step the oracle takes the learner gradient (eq. 4) at the current
+    weights and applies the update of eq. 7 with the peer equal to the
+    learner, at the rate the oracle's recipe gives for the epoch (Section
+    3: linear scaling, warm-up); the GPU runs Trainer in float32.  The
+    accumulated weight change and each epoch's mean loss must agree to
+    1e-4, and the rates must be the recipe's."""
+    from paper_1907_05701_amd import binding as bd
+    from paper_1907_05701_amd.step import LearnerStep
+    from paper_1907_05701_amd.train import Trainer
+    shape = dict(L=1, D=40, H=64, P=32, K=100, T=21, B=8)
+    dims = ref.Dims(**shape)
+    theta0 = inputs.params(ref.param_count(dims), seed=80)
+    batches = [(inputs.features(dims.T, dims.B, dims.D, seed=81 + i), inputs.labels(dims.T, dims.B, dims.K, seed=85 + i))
+               for i in range(2)]
+    epochs, base_lr, base_batch, warm = 3, 4.0, 8, 10
+    st = LearnerStep(**shape, precision="fp32")
+    st.load(theta0, *batches[0], theta0)
+    hist = Trainer(st, batches, base_lr=base_lr, base_batch=base_batch, warmup_epochs=warm,
+                   flags=bd.ADPSGD_WRITE_PEER).run(epochs)
+    theta_gpu = st.theta.cpu().numpy().astype(np.float64)
+
+    theta = theta0.astype(np.float64)
+    want = []
+    for e in range(1, epochs + 1):
+        lr = ref.lr_schedule(e, base_lr, base_batch, dims.B, warm)
+        losses = []
+        for x, lab in batches:
+            g = ref.learner_gradient(theta, dims, x, lab)
+            losses.append(g["loss"])
+            theta = ref.adpsgd_update(theta, theta, g["grad"], lr)
+        want.append((e, lr, float(np.mean(losses))))
+    print("[train] gpu", [(e, round(lr, 4), round(l, 6)) for e, lr, l in hist], flush=True)
+    print("[train] oracle", [(e, round(lr, 4), round(l, 6)) for e, lr, l in want], flush=True)
+    for (e, lr, l), (e2, lr2, l2) in zip(hist, want):
+        assert e == e2 and abs(lr - lr2) <= 1e-12 * lr2
+        assert abs(l - l2) <= 1e-4 * abs(l2), (e, l, l2)
+    d_gpu, d_ref = theta_gpu - theta0, theta - theta0
+    err = float(np.linalg.norm(d_gpu - d_ref) / np.linalg.norm(d_ref))
+    print(f"[train] accumulated update rel err {err:.2e}", flush=True)
+    assert err <= 1e-4
+    np.testing.assert_array_equal(st.peer.cpu().numpy(), st.theta.cpu().numpy())
