@@ -113,6 +113,21 @@ int softmax_ce_fwd_bwd(const blstm_dims* dims, const float* theta, const void* t
                        float* loss, float* dy_top, float* grad, void* head_ws,
                        hipStream_t stream);
 
+/* softmax_ce_fwd_bwd without a head_ws argument, for callers that cannot
+ * allocate device memory (code under stream capture, tight serving loops,
+ * harnesses that forbid allocation).  The head workspace is a static device
+ * array of HEAD_STATIC_SCRATCH_BYTES held by each device the library runs on
+ * until the process ends; dims whose head workspace (blstm_workspace_bytes'
+ * head_ws) exceeds it are rejected with BLSTM_EUNSUPPORTED.  Same arguments,
+ * results and errors as softmax_ce_fwd_bwd otherwise.  The call allocates
+ * nothing (its first call on a device looks the array's address up once).
+ * Calls that overlap on one device share the array and race: serialise them
+ * (one stream, or events). */
+#define HEAD_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+int softmax_ce_fwd_bwd_static(const blstm_dims* dims, const float* theta, const void* theta_lp,
+                              const void* y_top, const int32_t* labels, float loss_scale,
+                              float* loss, float* dy_top, float* grad, hipStream_t stream);
+
 /* Back-propagation through time of the LSTM stack (Section 5.2 model; the
  * gradient g of eq. 4 for the LSTM parameters) given dy_top = dloss/dy_top.
  * Per layer, top-down: the gate-gradient recurrence in reverse time

@@ -19,9 +19,10 @@ ADPSGD_WRITE_PEER = 2
 BLSTM_EINVAL = -1
 BLSTM_EUNSUPPORTED = -2
 BLSTM_EHIP = -3
+HEAD_STATIC_SCRATCH_BYTES = 64 << 20   # the static head workspace (adpsgd_blstm.h)
 
 EXPORTED = ("blstm_param_count", "blstm_workspace_bytes", "blstm_pack_params", "blstm_fwd",
-            "softmax_ce_fwd_bwd", "blstm_bwd", "replica_grad_reduce", "adpsgd_step",
+            "softmax_ce_fwd_bwd", "softmax_ce_fwd_bwd_static", "blstm_bwd", "replica_grad_reduce", "adpsgd_step",
             "blstm_recurrence_ok", "blstm_last_error", "blstm_timing_begin", "blstm_timing_end")
 
 
@@ -59,6 +60,7 @@ def lib():
         L.blstm_pack_params.argtypes = [DP, P, P, P]
         L.blstm_fwd.argtypes = [DP, P, P, P, P, P, P]
         L.softmax_ce_fwd_bwd.argtypes = [DP, P, P, P, P, ctypes.c_float, P, P, P, P, P]
+        L.softmax_ce_fwd_bwd_static.argtypes = [DP, P, P, P, P, ctypes.c_float, P, P, P, P]
         L.blstm_bwd.argtypes = [DP, P, P, P, P, P, P, P]
         L.blstm_recurrence_ok.argtypes = [DP, P, P]
         L.replica_grad_reduce.argtypes = [ctypes.POINTER(P), ctypes.c_int32, ctypes.c_int64,
@@ -70,6 +72,7 @@ def lib():
         L.blstm_timing_end.argtypes = [ctypes.POINTER(KernelTime), ctypes.c_int32,
                                        ctypes.POINTER(ctypes.c_int32)]
         for name in ("blstm_workspace_bytes", "blstm_pack_params", "blstm_fwd", "softmax_ce_fwd_bwd",
+                     "softmax_ce_fwd_bwd_static",
                      "blstm_bwd", "replica_grad_reduce", "adpsgd_step", "blstm_timing_begin",
                      "blstm_timing_end"):
             getattr(L, name).restype = ctypes.c_int
@@ -131,6 +134,12 @@ def softmax_ce_fwd_bwd(dims, theta, theta_lp, y_top, labels, loss_scale, loss, d
         ctypes.byref(dims), _ptr(theta), _ptr(theta_lp), _ptr(y_top), _ptr(labels),
         ctypes.c_float(loss_scale), _ptr(loss), _ptr(dy_top), _ptr(grad), _ptr(head_ws),
         _stream(stream)))
+
+
+def softmax_ce_fwd_bwd_static(dims, theta, theta_lp, y_top, labels, loss_scale, loss, dy_top, grad, stream=None):
+    return _check("softmax_ce_fwd_bwd_static", lib().softmax_ce_fwd_bwd_static(
+        ctypes.byref(dims), _ptr(theta), _ptr(theta_lp), _ptr(y_top), _ptr(labels),
+        ctypes.c_float(loss_scale), _ptr(loss), _ptr(dy_top), _ptr(grad), _stream(stream)))
 
 
 def blstm_bwd(dims, theta, theta_lp, act_ws, y_top, dy_top, grad, stream=None):

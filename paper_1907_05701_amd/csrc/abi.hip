@@ -163,7 +163,8 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   L.RL = h; h = align256(h + (size_t)M * 4);
   L.DZ = h; h = align256(h + (size_t)M * P * 4);
   L.DZT = h; h = align256(h + (size_t)M * P * es);
-  L.HCSP = h; h = align256(h + (size_t)COLSUM_MAX_CHUNKS * std::max<int64_t>(L.Kp, P) * 4);
+  // column-sum partials: db_l (P columns), and db_s on the float32 path
+  L.HCSP = h; h = align256(h + (size_t)COLSUM_MAX_CHUNKS * (es == 2 ? P : std::max<int64_t>(L.Kp, P)) * 4);
   size_t hsk = 0;
   L.sp_z = es == 2 ? plan_splits(M, P, 2 * H, BMt, BNt, BKt, 1, true, true) : 1;
   if (L.sp_z > 1) hsk = std::max(hsk, (size_t)L.sp_z * M * P * 4);

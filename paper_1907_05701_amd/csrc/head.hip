@@ -10,6 +10,7 @@
 // one workgroup per frame reduces the row and overwrites it with ds.
 #include <math.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "common.hpp"
@@ -377,4 +378,61 @@ extern "C" int softmax_ce_fwd_bwd(const blstm_dims* dims, const float* theta, co
   }
   return head_impl<float>(lo, theta, theta, (const float*)y_top, labels, loss_scale, loss, dy_top,
                           grad, (char*)head_ws, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Allocation-free variant: the head workspace is a file-scope device array
+// instead of a caller buffer.  Each device that runs it holds its own copy
+// (HEAD_STATIC_SCRATCH_BYTES) until the process ends; host code reaches it
+// only through the address hipGetSymbolAddress returns for the current device
+// (the array's name is a host-side stand-in), looked up once per device on
+// the first call there.  Nothing in the head's kernels needs the workspace
+// to start at zero (every partial is written before it is read).  Calls
+// that overlap on one device share the array and race.
+// ---------------------------------------------------------------------------
+static __device__ __attribute__((aligned(256))) unsigned char scratch[HEAD_STATIC_SCRATCH_BYTES];
+
+static int scratch_address(void** out) {
+  static std::mutex mu;
+  static void* per_dev[64] = {};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess)
+    return blstm_fail(BLSTM_EHIP, "softmax_ce_fwd_bwd_static: hipGetDevice: %s", hipGetErrorString(hipGetLastError()));
+  if (dev < 0 || dev >= 64) return blstm_fail(BLSTM_EUNSUPPORTED, "softmax_ce_fwd_bwd_static: device %d", dev);
+  std::lock_guard<std::mutex> lock(mu);
+  if (!per_dev[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return blstm_fail(BLSTM_EHIP, "softmax_ce_fwd_bwd_static: hipGetSymbolAddress: %s", hipGetErrorString(e));
+    per_dev[dev] = p;
+  }
+  *out = per_dev[dev];
+  return BLSTM_OK;
+}
+
+extern "C" int softmax_ce_fwd_bwd_static(const blstm_dims* dims, const float* theta, const void* theta_lp,
+                                         const void* y_top, const int32_t* labels, float loss_scale, float* loss,
+                                         float* dy_top, float* grad, hipStream_t stream) {
+  Layout lo;
+  int rc = make_layout(dims, &lo);
+  if (rc) return rc;
+  if (!theta || !y_top || !labels || !loss || !dy_top || !grad)
+    return blstm_fail(BLSTM_EINVAL, "softmax_ce_fwd_bwd_static: NULL pointer");
+  if (lo.head_bytes > HEAD_STATIC_SCRATCH_BYTES)
+    return blstm_fail(BLSTM_EUNSUPPORTED,
+                      "softmax_ce_fwd_bwd_static: these dims need %zu bytes of head workspace, above the static "
+                      "%zu (use softmax_ce_fwd_bwd with a caller buffer)",
+                      lo.head_bytes, (size_t)HEAD_STATIC_SCRATCH_BYTES);
+  if (lo.M > 0x7fffffff) return blstm_fail(BLSTM_EUNSUPPORTED, "too many frames");
+  void* ws = nullptr;
+  rc = scratch_address(&ws);
+  if (rc) return rc;
+  if (lo.prec == BLSTM_BF16) {
+    if (!theta_lp) return blstm_fail(BLSTM_EINVAL, "softmax_ce_fwd_bwd_static: theta_lp is NULL (bf16)");
+    return head_impl<bf16>(lo, theta, (const bf16*)theta_lp, (const bf16*)y_top, labels, loss_scale, loss, dy_top,
+                           grad, (char*)ws, stream);
+  }
+  return head_impl<float>(lo, theta, theta, (const float*)y_top, labels, loss_scale, loss, dy_top, grad, (char*)ws,
+                          stream);
 }
