@@ -7,8 +7,7 @@ struct PersistArgs {
   bf16* Y;            // layer output [M][2H] (forward: read h_prev, write h)
   const bf16* W;      // bf16 parameter copy (flat layout)
   int64_t whh0, whh1; // element offsets of W_hh for the two directions
-  const bf16* WT;     // backward with more than one 16-row block per workgroup: W_hh^T of
-                      // this layer, [2][H][4H] (directions)
+  const bf16* WT;     // unused by the persistent kernels (W_hh^T of the layer, [2][H][4H])
   const bf16* Gx;     // forward: input projection [M][8H]
   float* C;           // cell states [M][2H] (forward writes, backward reads)
   bf16* G;            // gate pre-activations [M][2][H][4] (direction, unit, gate i/f/g/o; forward writes, backward reads)
@@ -25,24 +24,27 @@ struct PersistArgs {
   uint32_t seq;       // the launch's position among the call's launches (filled in by persist_layer)
 };
 
-// At most this many batch slices of 16*MB rows per launch (MB <= 8), so one
-// launch covers at most PERSIST_MAX_SLICES*128 rows.
+// At most this many batch slices of 16*MB rows per launch (MB <= PERSIST_MAX_MB),
+// so one launch covers at most PERSIST_MAX_ROWS rows.
 #define PERSIST_MAX_SLICES 32
-#define PERSIST_MAX_ROWS (PERSIST_MAX_SLICES * 16 * 8)
-// Exchange buffer: 2 slots x 2 directions x row quads x (H/32 members) x H
+#define PERSIST_MAX_MB 1   // two row blocks per workgroup spill registers next to the W_hh slice
+#define PERSIST_MAX_ROWS (PERSIST_MAX_SLICES * 16 * PERSIST_MAX_MB)
+// Exchange buffer: 2 slots x 2 directions x row quads x (H/64 members) x H
 // units words of 8 bytes (the backward's partial sums, four rows per word;
-// the forward uses H/4 words per row).
+// the forward uses H/4 words per row, never more).
 static inline size_t persist_xch_bytes(int B, int H) {
   const size_t rows = B < PERSIST_MAX_ROWS ? B : PERSIST_MAX_ROWS;
-  const size_t members = H / 32 > 0 ? H / 32 : 1;
-  return (size_t)2 * 2 * ((rows + 3) / 4) * members * H * 8;
+  const size_t members = H / 64 > 0 ? H / 64 : 1;
+  const size_t bwd = (size_t)2 * 2 * ((rows + 3) / 4) * members * H * 8;
+  const size_t fwd = (size_t)2 * 2 * rows * (H / 4 > 0 ? H / 4 : 1) * 8;
+  return bwd > fwd ? bwd : fwd;
 }
 
-// True if the persistent kernels can hold a W_hh slice for this H in LDS
-// (and T fits the 8-bit step numbers).
+// True if the persistent kernels handle this H (a multiple of 64, at most
+// 512: a member's 256 W_hh rows fit in its registers); any T.
 bool persist_supported(int H, int T);
-// Whether the persistent BPTT of a layer reads W_hh^T (PersistArgs::WT): only
-// when its workgroups take more than one 16-row block (W_hh slice in LDS).
+// Whether the persistent BPTT of a layer reads W_hh^T (PersistArgs::WT):
+// never (its W_hh rows are read as they lie).
 bool persist_bwd_needs_wt(int H, int B);
 // Status block (PERSIST_STATUS_BYTES at the end of the activation
 // workspace): an int flag set by any exchange wait that gives up, and a tag

@@ -41,7 +41,7 @@ import numpy as np
 ALL_POINTS = ("x", "w", "gx", "hrec", "y", "pre", "z", "s", "ds", "dz", "da", "part")
 # the points where the library's bf16 path rounds (its logits are float32)
 PATH_POINTS = tuple(p for p in ALL_POINTS if p != "s")
-MEMBER_UNITS = 32   # hidden units whose gate rows one recurrent workgroup owns
+MEMBER_UNITS = 64   # hidden units whose gate rows one recurrent workgroup owns
 
 
 def bf(v):

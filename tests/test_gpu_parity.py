@@ -325,12 +325,13 @@ def test_long_sequence_bf16(gpu_lib):
                          check_update=False)
 
 
-@pytest.mark.parametrize("B", [200, 300, 1100], ids=["mb2", "mb4", "mb8_two_chunks"])
+@pytest.mark.parametrize("B", [200, 300, 1100], ids=["ragged_slices", "two_chunks", "five_chunks"])
 def test_recurrence_batch_regimes_bf16(gpu_lib, B):
-    """Batches large enough that each recurrent workgroup covers 2, 4 or 8
-    row blocks, and (B=1100) that the batch is processed in two chunks.  Two
-    layers, so that exchange words left by the previous layer's launches
-    (forward bottom-up, backward top-down) are met and must not match."""
+    """Batches whose last 16-row slice is ragged (B=200: 13 slices), that
+    need two launches per layer (B=300: 256 + 44 rows) and five (B=1100).
+    Two layers, so that exchange words left by the previous layer's
+    launches (forward bottom-up, backward top-down) are met and must not
+    match."""
     run_step_and_compare(dict(L=2, D=40, H=512, P=32, K=50, T=3, B=B), "bf16", BF16_TOL, seed=11,
                          check_update=False)
 
