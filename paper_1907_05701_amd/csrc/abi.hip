@@ -113,7 +113,9 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   // da^T [8H][M] and per-step bias partials, two of each (alternating layers)
   L.dat_bytes = align256(L.write_dat ? (size_t)M * 8 * H * es : 0);
   L.DAT = a; a += 2 * L.dat_bytes;
-  L.dbp_bytes = align256((size_t)d->T * cdiv(d->B, 16) * 8 * H * 4);
+  // per-step 16-row partials (per-step BPTT) or per-workgroup partials over
+  // all steps (persistent BPTT, 8-row workgroups)
+  L.dbp_bytes = align256((size_t)std::max<int64_t>((int64_t)d->T * cdiv(d->B, 16), cdiv(d->B, 8)) * 8 * H * 4);
   L.DBP = a; a += 2 * L.dbp_bytes;
   L.CSP = a; a = align256(a + (size_t)COLSUM_MAX_CHUNKS * 8 * H * 4);
   // split-K plans and partial buffers of the backward GEMMs

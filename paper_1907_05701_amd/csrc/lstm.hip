@@ -637,7 +637,8 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
           g[ng++] = F32Job{opnd(DA, 8 * H, 8 * H, M), Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0, part_dx};
         // db_ih = db_hh = sum over frames of da, from the BPTT kernel's
         // per-row-block partials, in the same reduction launch
-        const ColSumJob cs{DBPl, (done ? 1 : Tn) * (int)cdiv(B, 16), 2, 4 * H, 8 * H, 4 * H,
+        const int dbp_rows = done ? (int)cdiv(B, persist_rows_per_workgroup(H, B)) : Tn * (int)cdiv(B, 16);
+        const ColSumJob cs{DBPl, dbp_rows, 2, 4 * H, 8 * H, 4 * H,
                            grad + lo.bih[l][0], grad + lo.bhh[l][0], lo.bih[l][1] - lo.bih[l][0]};
         const bool with_db = step_fused && colsum_job_ok(cs);
         if (gemm_f32_group<true, false>("gemm_bwd_group", ss, ng, g, with_db ? &cs : nullptr)) {
@@ -668,7 +669,8 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     // db_ih = db_hh = sum over frames of da (unless the reduction above did it)
     if (!db_done) {
       if (step_fused)
-        colsum_parts("colsum_db", ss, DBPl, (done ? 1 : Tn) * (int)cdiv(B, 16), 8 * H, 4 * H,
+        colsum_parts("colsum_db", ss, DBPl,
+                     done ? (int)cdiv(B, persist_rows_per_workgroup(H, B)) : Tn * (int)cdiv(B, 16), 8 * H, 4 * H,
                      lo.bih[l][1] - lo.bih[l][0], grad + lo.bih[l][0], grad + lo.bhh[l][0]);
       else
         colsum<T>("colsum_db", s, DA, M, 8 * H, 8 * H, csp, 4 * H, lo.bih[l][1] - lo.bih[l][0],

@@ -88,24 +88,37 @@ __device__ __forceinline__ uint32_t lane_xor2(uint32_t v) {
 // bit 14 clear and the 8-bit significand of the bf16 of x), magnitudes from
 // 2^65 and non-finite values saturated to 2^64; tiny values become bf16
 // subnormals.  Decoding multiplies by 2^64 (exact).
-__device__ __forceinline__ uint32_t p15_encode(float x) {
-  uint32_t b = __builtin_bit_cast(uint16_t, (bf16)(x * 0x1p-64f));
-  if (b & 0x4000u) b = (b & 0x8000u) | 0x3F80u;
-  return b;
+// two bf16 values in one dword, `lo` in the low half
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (bf16)lo) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)hi) << 16);
 }
-__device__ __forceinline__ float p15_decode(uint32_t c) {
-  return __builtin_bit_cast(float, (c & 0xBFFFu) << 16) * 0x1p64f;
+// the 15-bit form of four partial sums in one word (tag bits clear)
+__device__ __forceinline__ uint64_t p15x4_encode(f32x4 v) {
+  uint32_t lo = pack_bf16x2(v[0] * 0x1p-64f, v[1] * 0x1p-64f);
+  uint32_t hi = pack_bf16x2(v[2] * 0x1p-64f, v[3] * 0x1p-64f);
+  if ((lo | hi) & 0x40004000u) {   // some |x| >= 2^65 or non-finite: saturate those halves
+    auto fix = [](uint32_t p) {
+      uint32_t r = p;
+      if (p & 0x4000u) r = (r & 0xFFFF0000u) | (p & 0x8000u) | 0x3F80u;
+      if (p & 0x40000000u) r = (r & 0xFFFFu) | (p & 0x80000000u) | 0x3F800000u;
+      return r;
+    };
+    lo = fix(lo);
+    hi = fix(hi);
+  }
+  return ((uint64_t)hi << 32) | lo;
+}
+// the four partial sums of a word (tag bits ignored)
+__device__ __forceinline__ f32x4 p15x4_decode(uint64_t w) {
+  const uint32_t lo = (uint32_t)w & 0xBFFFBFFFu, hi = (uint32_t)(w >> 32) & 0xBFFFBFFFu;
+  return f32x4{__builtin_bit_cast(float, lo << 16), __builtin_bit_cast(float, lo & 0xFFFF0000u),
+               __builtin_bit_cast(float, hi << 16), __builtin_bit_cast(float, hi & 0xFFFF0000u)} * 0x1p64f;
 }
 __device__ __forceinline__ uint64_t h4_tag(uint32_t seq, int n) {
   const uint32_t t = 1u | (((uint32_t)n >> 1 & 1u) << 1) | ((seq & 3u) << 2);
   return ((uint64_t)(t & 1u) << 14) | ((uint64_t)(t >> 1 & 1u) << 30) | ((uint64_t)(t >> 2 & 1u) << 46) |
          ((uint64_t)(t >> 3 & 1u) << 62);
-}
-
-// two bf16 values in one dword, `lo` in the low half
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return (uint32_t)__builtin_bit_cast(uint16_t, (bf16)lo) |
-         ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)hi) << 16);
 }
 
 // Polls the N words base[j * stride] (want: the expected tag bits; a word
@@ -132,16 +145,29 @@ __device__ __forceinline__ void poll_words(uint64_t (&wv)[N], const uint64_t* ba
   }
 }
 
+// lanes 32-63 of x replaced by lanes 0-31 of y (v_permlane32_swap_b32;
+// lanes 0-31 of x are kept)
+__device__ __forceinline__ float upper_from_lower(float x, float y) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x), __builtin_bit_cast(unsigned, y),
+                                                  false, false);
+  return __builtin_bit_cast(float, r[0]);
+}
+
 // ---------------------------------------------------------------------------
 // Forward.
+//
+// RV rows of the batch per workgroup (8 or 16) on 16-row MFMA tiles.  With
+// RV = 8 the tiles' rows 8-15 are zeros, and after the k halves meet the
+// owner lanes swap the valid rows of lanes 0-31 into lanes 32-63, so that
+// every lane applies the cell to 2 rows instead of 4 (half the VALU work of
+// the step, which bounds it once the W_hh slice is in registers).
 // ---------------------------------------------------------------------------
-template <int MB>
+template <int RV>
 __global__ __launch_bounds__(NTH) void lstm_fwd_persist(const PersistArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds_raw[];
-  constexpr int R = 16 * MB;
-  // MB == 1: the k half 0 waves own the row block; MB > 1: half kh owns the
-  // row blocks m with m % 2 == kh
-  constexpr int MO = MB == 1 ? 1 : MB / 2;
+  static_assert(RV == 8 || RV == 16, "rows per workgroup");
+  constexpr int R = 16;          // MFMA tile rows
+  constexpr int NR = RV / 4;     // rows per owner lane
   const int H = a.H, B = a.B, Tn = a.Tn;
   const int NG = 2 * a.NS;
   const int g = blockIdx.x % NG, mem = blockIdx.x / NG;
@@ -150,8 +176,7 @@ __global__ __launch_bounds__(NTH) void lstm_fwd_persist(const PersistArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int ub = w & 3, kh = w >> 2;
   const int KH = H / 64;   // 32-deep k-steps per k half
-  const bool owner = MB > 1 || kh == 0;
-  auto mblk = [&](int o) { return MB == 1 ? 0 : 2 * o + kh; };
+  const bool owner = kh == 0;
 
   // W_hh fragments (B operand): gate q of unit u0 + ub*16 + lane%16, k-step
   // kh*KH + i, k = 8*(lane/16) .. +8 within it.  Staged by direct-to-LDS
@@ -190,204 +215,189 @@ __global__ __launch_bounds__(NTH) void lstm_fwd_persist(const PersistArgs a) {
     }
   }
 
-  // LDS during the steps: gathered h [H/8][R + 1][8] (MFMA A layout), the
-  // k-half partial sums, and (MB == 1) a step's c [16][64] (float), h
-  // [16][64] and gate pre-activations [16][64][4] (bf16) for 16-byte stores
+  // LDS during the steps: gathered h [H/8][R + 1][8] (MFMA A layout; rows
+  // RV..15 stay zero), the k-half partial sums, and step buffers (by step
+  // parity) of c [RV][64] (float), h [RV][64] and gate pre-activations
+  // [RV][64][4] (bf16), staged for 16-byte stores
+  const int rend = a.b0 + a.rows;
+  const int rowbase = a.b0 + s * RV;
   bf16* hl = (bf16*)lds_raw;
   f32x4* red = (f32x4*)(lds_raw + (size_t)(H / 8) * (R + 1) * 16);
-  float* sC = (float*)(red + 4 * MB * 4 * 64);
-  bf16* sY = (bf16*)(sC + 16 * PU);
-  bf16* sG = sY + 16 * PU;
+  char* stage0 = (char*)(red + 4 * 4 * 64);
+  constexpr int STEP_STAGE = RV * PU * (4 + 2 + 8);
+  auto stC = [&](int par) { return (float*)(stage0 + par * STEP_STAGE); };
+  auto stY = [&](int par) { return (bf16*)(stage0 + par * STEP_STAGE + RV * PU * 4); };
+  auto stG = [&](int par) { return (bf16*)(stage0 + par * STEP_STAGE + RV * PU * 6); };
+  // c, h and the gates of step tt in 16-byte pieces (the NT threads from
+  // first): per row, the 64 units x 4 gates are 512 contiguous bytes (32
+  // pieces), c 256 bytes (16) and h 128 bytes (8)
+  auto store_step = [&](int tt, int par, int first, int nt) {
+    const float* sC = stC(par);
+    const bf16* sY = stY(par);
+    const bf16* sG = stG(par);
+    for (int pc = tid - first; pc < RV * 56; pc += nt) {
+      if (pc < RV * 32) {
+        const int rl = pc >> 5, c = pc & 31;
+        if (rowbase + rl < rend)
+          *(uint4*)(a.G + ((int64_t)tt * B + rowbase + rl) * 8 * H + (int64_t)d * 4 * H + (int64_t)u0 * 4 + c * 8) =
+              *(const uint4*)&sG[rl * PU * 4 + c * 8];
+      } else if (pc < RV * 48) {
+        const int rl = (pc - RV * 32) >> 4, c = (pc - RV * 32) & 15;
+        if (rowbase + rl < rend)
+          *(float4*)(a.C + ((int64_t)tt * B + rowbase + rl) * 2 * H + (int64_t)d * H + u0 + c * 4) =
+              *(const float4*)&sC[rl * PU + c * 4];
+      } else {
+        const int rl = (pc - RV * 48) >> 3, c = (pc - RV * 48) & 7;
+        if (rowbase + rl < rend)
+          *(uint4*)(a.Y + ((int64_t)tt * B + rowbase + rl) * 2 * H + (int64_t)d * H + u0 + c * 8) =
+              *(const uint4*)&sY[rl * PU + c * 8];
+      }
+    }
+  };
+  if constexpr (RV < R) {
+    for (int i = tid; i < (H / 8) * (R - RV); i += NTH)
+      *(uint4*)&hl[((i / (R - RV)) * (R + 1) + RV + i % (R - RV)) * 8] = make_uint4(0u, 0u, 0u, 0u);
+  }
 
-  const int rend = a.b0 + a.rows;
-  const int rowbase = a.b0 + s * R;
   const int unit = u0 + ub * 16 + (lane & 15);
   const int wpr = H / 4;   // exchange words per row
   const int64_t slot_stride = (int64_t)2 * a.rows * wpr;
+  // the slice rows of an owner lane's NR cell rows
+  auto lrow = [&](int r) { return RV == R ? (lane >> 4) * 4 + r : ((lane >> 4) & 1) * 4 + (lane >> 5) * 2 + r; };
 
-  float creg[MO][4];
+  float creg[NR];
 #pragma unroll
-  for (int o = 0; o < MO; ++o)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) creg[o][r] = 0.f;
+  for (int r = 0; r < NR; ++r) creg[r] = 0.f;
 
   // input projection of a step (independent of h), loaded one step ahead so
   // that its latency hides behind the previous step's exchange
-  bf16 gx[MO][4][4], gxn[MO][4][4];
+  bf16 gx[NR][4], gxn[NR][4];
   auto load_gx = [&](int tt) {
 #pragma unroll
-    for (int o = 0; o < MO; ++o)
+    for (int r = 0; r < NR; ++r) {
+      const int row = rowbase + lrow(r);
+      const bf16* p = a.Gx + ((int64_t)tt * B + (row < rend ? row : a.b0)) * 8 * H + (int64_t)d * 4 * H + unit;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = rowbase + mblk(o) * 16 + (lane >> 4) * 4 + r;
-        const bf16* p = a.Gx + ((int64_t)tt * B + (row < rend ? row : a.b0)) * 8 * H + (int64_t)d * 4 * H + unit;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) gxn[o][r][q] = p[q * H];
-      }
+      for (int q = 0; q < 4; ++q) gxn[r][q] = p[q * H];
+    }
   };
   if (owner) load_gx(d ? Tn - 1 : 0);
 
-  constexpr int WPT = (R * 128 + NTH - 1) / NTH;   // gathered words per thread (at H = 512)
+  constexpr int NGT = NTH;   // gathering threads (all: measured faster than the owner waves alone)
+  constexpr int WPT = (RV * 128 + NGT - 1) / NGT;     // gathered words per thread (at H = 512)
   for (int tau = 0; tau < Tn; ++tau) {
     const int t = d ? Tn - 1 - tau : tau;
     if (owner) {
 #pragma unroll
-      for (int o = 0; o < MO; ++o)
+      for (int r = 0; r < NR; ++r)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) gx[o][r][q] = gxn[o][r][q];
+        for (int q = 0; q < 4; ++q) gx[r][q] = gxn[r][q];
     }
 
-    f32x4 acc[MB][4];
+    f32x4 acc[4];
 #pragma unroll
-    for (int m = 0; m < MB; ++m)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) acc[m][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < 4; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
     if (tau > 0) {
-      // h of the previous step (R rows x H/4 words of this slice, contiguous
-      // in the exchange buffer), polled by all threads in whole cache lines
-      // and staged in LDS in the MFMA A layout
-      const int nwords = R * wpr;
-      const uint64_t* src = a.X + ((tau - 1) & 1) * slot_stride + ((int64_t)d * a.rows + (rowbase - a.b0)) * wpr;
-      const uint64_t want = h4_tag(a.seq, tau);
-      uint64_t wv[WPT];
+      // h of the previous step (RV rows x H/4 words of this slice, contiguous
+      // in the exchange buffer), polled by the gathering threads in whole
+      // cache lines and staged in LDS in the MFMA A layout
+      if (tid < NGT) {
+        const int nwords = RV * wpr;
+        const uint64_t* src = a.X + ((tau - 1) & 1) * slot_stride + ((int64_t)d * a.rows + (rowbase - a.b0)) * wpr;
+        const uint64_t want = h4_tag(a.seq, tau);
+        uint64_t wv[WPT];
 #pragma unroll
-      for (int j = 0; j < WPT; ++j) {
-        const int idx = tid + NTH * j;
-        const bool ok = idx < nwords && rowbase + idx / wpr < rend;
-        wv[j] = ok ? ll_load(src + idx) : want;
-      }
-      poll_words<WPT>(wv, src + tid, NTH, want, a.status);
+        for (int j = 0; j < WPT; ++j) {
+          const int idx = tid + NGT * j;
+          const bool ok = idx < nwords && rowbase + idx / wpr < rend;
+          wv[j] = ok ? ll_load(src + idx) : want;
+        }
+        poll_words<WPT>(wv, src + tid, NGT, want, a.status);
 #pragma unroll
-      for (int j = 0; j < WPT; ++j) {
-        const int idx = tid + NTH * j;
-        if (idx >= nwords) break;
-        const int row = idx / wpr, wc = idx % wpr;   // units 4 wc .. 4 wc + 3
-        const bool ok = rowbase + row < rend;
-        *(uint64_t*)&hl[((wc >> 1) * (R + 1) + row) * 8 + 4 * (wc & 1)] = ok ? (wv[j] & ~H4_TAG_BITS) : 0ull;
+        for (int j = 0; j < WPT; ++j) {
+          const int idx = tid + NGT * j;
+          if (idx >= nwords) break;
+          const int row = idx / wpr, wc = idx % wpr;   // units 4 wc .. 4 wc + 3
+          const bool ok = rowbase + row < rend;
+          *(uint64_t*)&hl[((wc >> 1) * (R + 1) + row) * 8 + 4 * (wc & 1)] = ok ? (wv[j] & ~H4_TAG_BITS) : 0ull;
+        }
       }
       __syncthreads();
 #pragma unroll
       for (int i = 0; i < KH_MAX; ++i) {
         if (i >= KH) break;
         const int kg = (kh * KH + i) * 4 + (lane >> 4);
+        const bf16x8 af = *(const bf16x8*)&hl[(kg * (R + 1) + (lane & 15)) * 8];
 #pragma unroll
-        for (int m = 0; m < MB; ++m) {
-          const bf16x8 af = *(const bf16x8*)&hl[(kg * (R + 1) + m * 16 + (lane & 15)) * 8];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) acc[m][q] = Mfma<bf16>::mma(af, bw[i][q], acc[m][q]);
-        }
+        for (int q = 0; q < 4; ++q) acc[q] = Mfma<bf16>::mma(af, bw[i][q], acc[q]);
       }
     }
-    // the two k halves of each row block meet at its owner
+    // the two k halves meet at the owner (k half 0)
+    if (!owner) {
 #pragma unroll
-    for (int m = 0; m < MB; ++m) {
-      const bool mine = MB == 1 ? kh == 0 : (m & 1) == kh;
-      if (!mine) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) red[((ub * MB + m) * 4 + q) * 64 + lane] = acc[m][q];
-      }
+      for (int q = 0; q < 4; ++q) red[(ub * 4 + q) * 64 + lane] = acc[q];
     }
     __syncthreads();
     if (owner) {
       // cell math of all owned rows, then h published (the other members
       // wait for it), then the saved activations (only read after the launch)
       uint64_t* xo = a.X + (tau & 1) * slot_stride;
-      float hv[MO][4], gv[MO][4][4];
 #pragma unroll
-      for (int o = 0; o < MO; ++o) {
-        const int m = mblk(o);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) acc[m][q] += red[((ub * MB + m) * 4 + q) * 64 + lane];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-#pragma unroll
-          for (int q = 0; q < 4; ++q) gv[o][r][q] = acc[m][q][r] + (float)gx[o][r][q];
-          const float ig = sigmoidf_(gv[o][r][0]), fg = sigmoidf_(gv[o][r][1]);
-          const float gg = tanhf_(gv[o][r][2]), og = sigmoidf_(gv[o][r][3]);
-          const float c = fg * creg[o][r] + ig * gg;
-          creg[o][r] = c;
-          hv[o][r] = og * tanhf_(c);
+      for (int q = 0; q < 4; ++q) {
+        acc[q] += red[(ub * 4 + q) * 64 + lane];
+        if constexpr (RV < R) {
+          // rows 2, 3 (lanes 0-15) and 6, 7 (lanes 16-31) into lanes 32-63
+          acc[q][0] = upper_from_lower(acc[q][0], acc[q][2]);
+          acc[q][1] = upper_from_lower(acc[q][1], acc[q][3]);
         }
+      }
+      float hv[NR], gv[NR][4];
+#pragma unroll
+      for (int r = 0; r < NR; ++r) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) gv[r][q] = acc[q][r] + (float)gx[r][q];
+        const float ig = sigmoidf_(gv[r][0]), fg = sigmoidf_(gv[r][1]);
+        const float gg = tanhf_(gv[r][2]), og = sigmoidf_(gv[r][3]);
+        const float c = fg * creg[r] + ig * gg;
+        creg[r] = c;
+        hv[r] = og * tanhf_(c);
       }
       // every row's h before the first publish (the empty asm pins the
       // values here, so the compiler cannot sink their math past a publish)
 #pragma unroll
-      for (int o = 0; o < MO; ++o)
+      for (int r = 0; r < NR; ++r) __asm__ volatile("" : "+v"(hv[r]));
 #pragma unroll
-        for (int r = 0; r < 4; ++r) __asm__ volatile("" : "+v"(hv[o][r]));
+      for (int r = 0; r < NR; ++r) {
+        const int row = rowbase + lrow(r);
+        const float h_next_unit = lane_xor1(hv[r]);   // lanes of one row, units u and u^1
+        // lane 4i stores units 4i .. 4i+3 (the pairs of lanes 4i and 4i+2)
+        const uint32_t p2 = pack_bf16x2(hv[r], h_next_unit);
+        const uint32_t p4 = lane_xor2(p2);
+        if (row < rend && (lane & 3) == 0)
+          ll_store64(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 4,
+                     ((((uint64_t)p4 << 32) | p2) & ~H4_TAG_BITS) | h4_tag(a.seq, tau + 1));
+      }
+      // into LDS; the whole workgroup writes them out after the barrier
+      const int ul = ub * 16 + (lane & 15);
+      float* sC = stC(tau & 1);
+      bf16* sY = stY(tau & 1);
+      bf16* sG = stG(tau & 1);
 #pragma unroll
-      for (int o = 0; o < MO; ++o)
+      for (int r = 0; r < NR; ++r) {
+        const int rl = lrow(r);
+        sC[rl * PU + ul] = creg[r];
+        sY[rl * PU + ul] = (bf16)hv[r];
+        bf16x4 g4;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = rowbase + mblk(o) * 16 + (lane >> 4) * 4 + r;
-          const float h_next_unit = lane_xor1(hv[o][r]);   // lanes of one row, units u and u^1
-          // lane 4i stores units 4i .. 4i+3 (the pairs of lanes 4i and 4i+2)
-          const uint32_t p2 = pack_bf16x2(hv[o][r], h_next_unit);
-          const uint32_t p4 = lane_xor2(p2);
-          if (row < rend && (lane & 3) == 0)
-            ll_store64(xo + ((int64_t)d * a.rows + (row - a.b0)) * wpr + unit / 4,
-                       ((((uint64_t)p4 << 32) | p2) & ~H4_TAG_BITS) | h4_tag(a.seq, tau + 1));
-        }
-      if constexpr (MB == 1) {
-        // into LDS; the whole workgroup writes them out after the barrier
-        const int ul = ub * 16 + (lane & 15);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int rl = (lane >> 4) * 4 + r;
-          sC[rl * PU + ul] = creg[0][r];
-          sY[rl * PU + ul] = (bf16)hv[0][r];
-          bf16x4 g4;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) g4[q] = (bf16)gv[0][r][q];
-          *(bf16x4*)&sG[(rl * PU + ul) * 4] = g4;
-        }
-      } else {
-#pragma unroll
-        for (int o = 0; o < MO; ++o)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int row = rowbase + mblk(o) * 16 + (lane >> 4) * 4 + r;
-            if (row >= rend) continue;
-            const int64_t fr = (int64_t)t * B + row;
-            a.C[fr * 2 * H + (int64_t)d * H + unit] = creg[o][r];
-            a.Y[fr * 2 * H + (int64_t)d * H + unit] = (bf16)hv[o][r];
-            bf16x4 g4;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) g4[q] = (bf16)gv[o][r][q];
-            *(bf16x4*)(a.G + fr * 8 * H + (int64_t)d * 4 * H + (int64_t)unit * 4) = g4;
-          }
+        for (int q = 0; q < 4; ++q) g4[q] = (bf16)gv[r][q];
+        *(bf16x4*)&sG[(rl * PU + ul) * 4] = g4;
       }
       if (tau + 1 < Tn) load_gx(d ? Tn - 2 - tau : tau + 1);
     }
-    __syncthreads();   // h, the partial sums and the staged values are reused by the next step
-    if constexpr (MB == 1) {
-      // c, h and the gates of the step in 16-byte pieces: a row's 64 units
-      // x 4 gates are 512 contiguous bytes (one piece per thread), its c 256
-      // bytes (threads 0-255) and its h 128 bytes (threads 256-383).  The
-      // next step's gather barrier comes before the LDS is rewritten.
-      {
-        const int rl = tid >> 5, c = tid & 31;
-        const int row = rowbase + rl;
-        if (row < rend)
-          *(uint4*)(a.G + ((int64_t)t * B + row) * 8 * H + (int64_t)d * 4 * H + (int64_t)u0 * 4 + c * 8) =
-              *(const uint4*)&sG[rl * PU * 4 + c * 8];
-      }
-      if (tid < 256) {
-        const int rl = tid >> 4, c = tid & 15;
-        const int row = rowbase + rl;
-        if (row < rend)
-          *(float4*)(a.C + ((int64_t)t * B + row) * 2 * H + (int64_t)d * H + u0 + c * 4) =
-              *(const float4*)&sC[rl * PU + c * 4];
-      } else if (tid < 384) {
-        const int rl = (tid - 256) >> 3, c = (tid - 256) & 7;
-        const int row = rowbase + rl;
-        if (row < rend)
-          *(uint4*)(a.Y + ((int64_t)t * B + row) * 2 * H + (int64_t)d * H + u0 + c * 8) =
-              *(const uint4*)&sY[rl * PU + c * 8];
-      }
-    }
+    // the step's saved activations by the whole workgroup (the next step's
+    // gather barrier comes before the owners rewrite this buffer)
+    __syncthreads();
+    store_step(t, tau & 1, 0, NTH);
   }
 }
 
@@ -402,14 +412,19 @@ __global__ __launch_bounds__(NTH) void lstm_fwd_persist(const PersistArgs a) {
 // all members, summed in member order.  An exchange word holds one unit's
 // partials for four adjacent rows; words are ordered (row quad, member,
 // unit), so a member publishes whole cache lines and a reader takes 512
-// contiguous bytes of each member.
+// contiguous bytes of each member.  RV rows per workgroup (8 or 16) on
+// 16-row MFMA tiles (with RV = 8 the da block's rows 8-15 stay zero).
 // ---------------------------------------------------------------------------
-template <int MB>
+template <int RV>
 __global__ __launch_bounds__(NTH) void lstm_bwd_persist(const PersistArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds_raw[];
-  constexpr int R = 16 * MB;            // rows of this member's slice
-  constexpr int ITEMS = 2 * MB;         // (row, unit) cell items per thread
-  constexpr bool SPLIT = MB == 1;       // two threads per gathered (row quad, unit): member halves
+  static_assert(RV == 8 || RV == 16, "rows per workgroup");
+  constexpr int R = 16;                 // MFMA tile rows
+  constexpr int ITEMS = RV / 8;         // (row, unit) cell items per thread
+  // waves 0-3 gather (so their polls wait on no store of the step), waves
+  // 4-7 write da out (DA, DAT, bias partials)
+  constexpr int NG_T = NTH / 2;           // gathering threads
+  constexpr int TPI = NG_T / (16 * RV);   // threads per gathered (row quad, unit): member parts
   const int H = a.H, B = a.B, Tn = a.Tn;
   const int NM = H / PU, NG = 2 * a.NS;
   const int g = blockIdx.x % NG, mem = blockIdx.x / NG;
@@ -466,12 +481,17 @@ __global__ __launch_bounds__(NTH) void lstm_bwd_persist(const PersistArgs a) {
   }
 
   // LDS during the steps: own da as the A operand [32 k groups][R + 1][8]
-  // (k = own row), gathered dh_rec [2][R][64] (member halves when SPLIT)
+  // (k = own row; rows RV..15 stay zero), gathered dh_rec [TPI][RV][64]
+  // (member parts)
   bf16* al = (bf16*)lds_raw;
   float* dhl = (float*)(al + (size_t)32 * (R + 1) * 8);
+  if constexpr (RV < R) {
+    for (int i = tid; i < 32 * (R - RV); i += NTH)
+      *(uint4*)&al[((i / (R - RV)) * (R + 1) + RV + i % (R - RV)) * 8] = make_uint4(0u, 0u, 0u, 0u);
+  }
 
   const int rend = a.b0 + a.rows;
-  const int rowbase = a.b0 + s * R;
+  const int rowbase = a.b0 + s * RV;
   const int rquads = (a.rows + 3) / 4;             // row quads of this launch
   const int64_t slot_stride = (int64_t)2 * rquads * NM * H;
   // cell items: unit cu = tid % 64, rows tid/64 + 8*i
@@ -479,54 +499,74 @@ __global__ __launch_bounds__(NTH) void lstm_bwd_persist(const PersistArgs a) {
   float dcreg[ITEMS];
 #pragma unroll
   for (int i = 0; i < ITEMS; ++i) dcreg[i] = 0.f;
-  // da^T and bias partials: thread t takes own gate row t/2 and 8 of the 16
-  // rows of each 16-row block; the bias partial of a block is summed over the
-  // steps in order and written once
-  const int dkk = tid >> 1, dh8 = (tid & 1) * 8;
+  // da^T and bias partials (waves 4-7): thread t takes own gate row t - 256
+  // and the RV rows; the bias partial of the slice is summed over the steps
+  // in order and written once
+  const int dkk = tid & 255;
   const int64_t dgrow = (int64_t)d * 4 * H + (int64_t)((dkk >> 4) & 3) * H + u0 + (dkk >> 6) * 16 + (dkk & 15);
-  float dbacc[MB];
-#pragma unroll
-  for (int m = 0; m < MB; ++m) dbacc[m] = 0.f;
+  const uint32_t odat = (uint32_t)(dgrow * a.M + rowbase);   // DAT element of frame 0
+  float dbacc = 0.f;
 
   // everything the cell derivative needs besides dh_rec: dy, the gate
   // pre-activations and c at t, c at the step's predecessor in forward time
   // (which is the next step's t).  Fetched one step ahead, right after the
   // previous step's gather, so that no gather waits for them; c at t is the
-  // previous step's predecessor value.
+  // previous step's predecessor value.  Per-item element offsets are fixed
+  // (32-bit, row and unit); a step adds its frame base to the pointers.
   float dyn[ITEMS], cpn[ITEMS], cc[ITEMS];
   bf16x4 gtn[ITEMS];
+  uint32_t oc[ITEMS], og[ITEMS];   // item offsets into [B][2H] (C, DY) and [B][8H] (G) frames
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    int row = rowbase + (tid >> 6) + 8 * i;
+    row = row < rend ? row : a.b0;
+    oc[i] = (uint32_t)(row * 2 * H + d * H + u0 + cu);
+    og[i] = (uint32_t)(row * 8 * H + d * 4 * H + (u0 + cu) * 4);
+  }
+  const int64_t fc = (int64_t)B * 2 * H, fg = (int64_t)B * 8 * H;   // elements per frame
+  // DA pieces of this thread (waves 4-7; 8 own gate rows of one row per 16-byte piece)
+  constexpr int NDA = 32 * RV / (NTH / 2);
+  uint32_t oda[NDA];
+#pragma unroll
+  for (int c0 = 0; c0 < NDA; ++c0) {
+    const int c = c0 * (NTH / 2) + (tid & 255), kk = (c & 31) * 8, r = c >> 5;
+    oda[c0] = (uint32_t)((rowbase + r) * 8 * H + d * 4 * H + ((kk >> 4) & 3) * H + u0 + (kk >> 6) * 16 + (kk & 15));
+  }
   auto fetch = [&](int tau_) {
     const int t_ = d ? tau_ : Tn - 1 - tau_;
     const int tp_ = d ? t_ + 1 : t_ - 1;
     const bool hp = tp_ >= 0 && tp_ < Tn;
+    const float* dyt = a.DY + t_ * fc;
+    const float* cpt = a.C + (hp ? tp_ : 0) * fc;
+    const bf16* gt = a.G + t_ * fg;
 #pragma unroll
     for (int i = 0; i < ITEMS; ++i) {
-      int row = rowbase + (tid >> 6) + 8 * i;
-      row = row < rend ? row : a.b0;
-      const int64_t fr = (int64_t)t_ * B + row;
-      const int unit = u0 + cu;
-      dyn[i] = a.DY[fr * 2 * H + (int64_t)d * H + unit];
-      cpn[i] = hp ? a.C[((int64_t)tp_ * B + row) * 2 * H + (int64_t)d * H + unit] : 0.f;
-      // the unit's four gates are adjacent: one 8-byte load
-      gtn[i] = *(const bf16x4*)(a.G + fr * 8 * H + (int64_t)d * 4 * H + (int64_t)unit * 4);
+      dyn[i] = dyt[oc[i]];
+      cpn[i] = hp ? cpt[oc[i]] : 0.f;
+      gtn[i] = *(const bf16x4*)(gt + og[i]);   // the unit's four gates: one 8-byte load
     }
   };
   {
-    const int t0 = d ? 0 : Tn - 1;
+    const float* ct = a.C + (d ? 0 : Tn - 1) * fc;
 #pragma unroll
-    for (int i = 0; i < ITEMS; ++i) {
-      int row = rowbase + (tid >> 6) + 8 * i;
-      row = row < rend ? row : a.b0;
-      cc[i] = a.C[((int64_t)t0 * B + row) * 2 * H + (int64_t)d * H + u0 + cu];
-    }
+    for (int i = 0; i < ITEMS; ++i) cc[i] = ct[oc[i]];
   }
   fetch(0);
 
-  // gathered (row quad, unit) items: MB == 1: 256 items, two threads each
-  // (member halves [0, hm) and [hm, NM)); MB > 1: 256 MB items, MB / 2 per thread
-  constexpr int GI = SPLIT ? 1 : MB / 2;    // items per thread
-  constexpr int GM = SPLIT ? 4 : 8;         // members per thread at most (NM <= 8)
-  const int hm = (NM + 1) / 2;
+  // gathered (row quad, unit) items: 16 RV of them, TPI threads of waves 0-3
+  // each (member parts of MP members, summed in part order by the cell)
+  const int MP = (NM + TPI - 1) / TPI;
+  const int part = (tid & 255) / (16 * RV), item = tid % (16 * RV);
+  const int gqd = item >> 6;   // row quad within the slice
+  const int m0 = part * MP, mcount = max(0, min(NM, m0 + MP) - m0);
+  constexpr int GM = (8 + TPI - 1) / TPI;   // members per part at most (NM <= 8)
+  const uint32_t ogath = (uint32_t)((((int64_t)d * rquads + (rowbase - a.b0) / 4 + gqd) * NM + m0) * H + u0 + (item & 63));
+  // word offsets (within a slot) of the published words per unit block
+  uint32_t opub[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    opub[j] = (uint32_t)((((int64_t)d * rquads + (rowbase - a.b0) / 4 + (lane >> 4)) * NM + mem) * H +
+                         (w + 8 * j) * 16 + (lane & 15));
 
   for (int tau = 0; tau < Tn; ++tau) {
     const int t = d ? tau : Tn - 1 - tau;
@@ -543,18 +583,12 @@ __global__ __launch_bounds__(NTH) void lstm_bwd_persist(const PersistArgs a) {
     }
 
     if (tau > 0) {
-      const uint64_t* xs = a.X + ((tau - 1) & 1) * slot_stride;
-      const uint64_t want = h4_tag(a.seq, tau);
-#pragma unroll
-      for (int gi = 0; gi < GI; ++gi) {
-        const int item = SPLIT ? (tid & 255) : tid + NTH * gi;
-        const int qd = item >> 6, u = item & 63;   // row quad within the slice, own unit
-        const int mh = SPLIT ? tid >> 8 : 0;
-        const int m0 = SPLIT ? mh * hm : 0, mcount = SPLIT ? (mh ? NM - hm : hm) : NM;
-        float sum[4] = {0.f, 0.f, 0.f, 0.f};
-        if (rowbase + 4 * qd < rend) {
-          const uint64_t* src = xs + ((int64_t)d * rquads + (rowbase - a.b0) / 4 + qd) * NM * H + u0 + u;
-          const uint64_t* base = src + (int64_t)m0 * H;
+      if (tid < NG_T) {
+        const uint64_t* xs = a.X + ((tau - 1) & 1) * slot_stride;
+        const uint64_t want = h4_tag(a.seq, tau);
+        f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (rowbase + 4 * gqd < rend) {
+          const uint64_t* base = xs + ogath;
           uint64_t wv[GM];
 #pragma unroll
           for (int k = 0; k < GM; ++k) wv[k] = k < mcount ? ll_load(base + (int64_t)k * H) : want;
@@ -562,15 +596,14 @@ __global__ __launch_bounds__(NTH) void lstm_bwd_persist(const PersistArgs a) {
 #pragma unroll
           for (int k = 0; k < GM; ++k) {
             if (k >= mcount) break;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) sum[r] += p15_decode((uint32_t)(wv[k] >> (16 * r)) & 0xffffu);
+            sum += p15x4_decode(wv[k]);
           }
         }
 #pragma unroll
-        for (int r = 0; r < 4; ++r) dhl[mh * R * PU + (4 * qd + r) * PU + u] = sum[r];
+        for (int r = 0; r < 4; ++r) dhl[(part * RV + 4 * gqd + r) * PU + (item & 63)] = sum[r];
       }
     } else {
-      for (int i = tid; i < (SPLIT ? 2 : 1) * R * PU; i += NTH) dhl[i] = 0.f;
+      for (int i = tid; i < TPI * RV * PU; i += NTH) dhl[i] = 0.f;
     }
     __syncthreads();
 #pragma unroll
@@ -586,16 +619,19 @@ __global__ __launch_bounds__(NTH) void lstm_bwd_persist(const PersistArgs a) {
     for (int i = 0; i < ITEMS; ++i) {
       const int r = (tid >> 6) + 8 * i;
       const int row = rowbase + r;
-      const float ig = ga[i][0], fg = ga[i][1], gg = ga[i][2], og = ga[i][3];
-      const float dh = (SPLIT ? dhl[r * PU + cu] + dhl[R * PU + r * PU + cu] : dhl[r * PU + cu]) + dy[i];
+      const float ig = ga[i][0], fg_ = ga[i][1], gg = ga[i][2], og_ = ga[i][3];
+      float dhr = 0.f;
+#pragma unroll
+      for (int pp = 0; pp < TPI; ++pp) dhr += dhl[(pp * RV + r) * PU + cu];
+      const float dh = dhr + dy[i];
       const float tc = tanhf_(cc[i]);
-      const float dc = dh * og * (1.f - tc * tc) + dcreg[i];
-      dcreg[i] = dc * fg;
+      const float dc = dh * og_ * (1.f - tc * tc) + dcreg[i];
+      dcreg[i] = dc * fg_;
       float da[4];
       da[0] = dc * gg * ig * (1.f - ig);
-      da[1] = dc * cp[i] * fg * (1.f - fg);
+      da[1] = dc * cp[i] * fg_ * (1.f - fg_);
       da[2] = dc * ig * (1.f - gg * gg);
-      da[3] = dh * tc * og * (1.f - og);
+      da[3] = dh * tc * og_ * (1.f - og_);
       const bool ok = row < rend;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -608,81 +644,64 @@ __global__ __launch_bounds__(NTH) void lstm_bwd_persist(const PersistArgs a) {
     }
     __syncthreads();
 
-    // P = da_own [R x 256] * W_own [256 x H]; unit blocks w + 8j of this
+    // P = da_own [16 x 256] * W_own [256 x H]; unit blocks w + 8j of this
     // wave.  On the critical path, so before the global copies of da.
     if (tau + 1 < Tn) {
       uint64_t* xo = a.X + (tau & 1) * slot_stride;
-      f32x4 acc[MB][4];
+      f32x4 acc[4];
 #pragma unroll
-      for (int m = 0; m < MB; ++m)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      // one k-step's A fragments at a time (the scheduling barrier keeps the
-      // compiler from loading all of them ahead, which the registers holding
-      // W_hh leave no room for)
+      for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // the A fragments one k-step ahead of the products (two in registers:
+      // the registers holding W_hh leave no room for all eight)
+      const bf16* ab = &al[((lane >> 4) * (R + 1) + (lane & 15)) * 8];
+      bf16x8 af = *(const bf16x8*)ab, an;
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
+        if (ks + 1 < 8) an = *(const bf16x8*)(ab + (ks + 1) * 4 * (R + 1) * 8);
+        // (unit blocks past H hold zero fragments; their sums are not published)
 #pragma unroll
-        for (int m = 0; m < MB; ++m) {
-          const bf16x8 af = *(const bf16x8*)&al[((ks * 4 + (lane >> 4)) * (R + 1) + m * 16 + (lane & 15)) * 8];
-          // (unit blocks past H hold zero fragments; their sums are not published)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[m][j] = Mfma<bf16>::mma(af, bw[ks][j], acc[m][j]);
-        }
-        __builtin_amdgcn_sched_barrier(0);
+        for (int j = 0; j < 4; ++j) acc[j] = Mfma<bf16>::mma(af, bw[ks][j], acc[j]);
+        af = an;
       }
       // publish: word (row quad, member, unit), the lane's four rows
       const uint64_t tg = h4_tag(a.seq, tau + 1);
+      const int rl = (lane >> 4) * 4;
 #pragma unroll
-      for (int m = 0; m < MB; ++m)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int rl = m * 16 + (lane >> 4) * 4;
-          const int nb = w + 8 * j;
-          const int unit = nb * 16 + (lane & 15);
-          const uint64_t v = (uint64_t)p15_encode(acc[m][j][0]) | ((uint64_t)p15_encode(acc[m][j][1]) << 16) |
-                             ((uint64_t)p15_encode(acc[m][j][2]) << 32) | ((uint64_t)p15_encode(acc[m][j][3]) << 48);
-          if (rowbase + rl < rend && nb < NB)
-            ll_store64(xo + (((int64_t)d * rquads + (rowbase - a.b0 + rl) / 4) * NM + mem) * H + unit, v | tg);
-        }
+      for (int j = 0; j < 4; ++j) {
+        const uint64_t v = p15x4_encode(acc[j]);
+        if (rl < RV && rowbase + rl < rend && w + 8 * j < NB) ll_store64(xo + opub[j], v | tg);
+      }
     }
 
-    // da in frame-major rows (DA, for dX): 16 bytes of LDS and of DA per
-    // piece, 8 own gate rows of one row
-    for (int c = tid; c < 32 * R; c += NTH) {
-      const int kg = c & 31, r = c >> 5;
-      const int row = rowbase + r;
-      if (row < rend) {
-        const int kk = kg * 8;
-        const int64_t col = (int64_t)d * 4 * H + (int64_t)((kk >> 4) & 3) * H + u0 + (kk >> 6) * 16 + (kk & 15);
-        *(uint4*)(a.DA + ((int64_t)t * B + row) * 8 * H + col) = *(const uint4*)&al[(kg * (R + 1) + r) * 8];
-      }
-    }
-    // the own da block (R rows x 256 gate rows, in LDS) also goes out
-    // frame-contiguous (DAT) and as bias-gradient partial sums per 16-row
-    // block (DBP): thread t takes gate row t/2 and 8 of the 16 rows of a block
-    if (a.DAT || a.DBP) {
+    // waves 4-7: da in frame-major rows (DA, for dX), 16 bytes of LDS and
+    // of DA per piece (8 own gate rows of one row); frame-contiguous (DAT,
+    // the RV frames of one own gate row); and the bias partial sums (DBP)
+    if (tid >= NTH / 2) {
+      bf16* dat = a.DA + (int64_t)t * fg;
 #pragma unroll
-      for (int m = 0; m < MB; ++m) {
-        bf16 v[8];
+      for (int c0 = 0; c0 < NDA; ++c0) {
+        const int c = c0 * (NTH / 2) + (tid & 255), kg = c & 31, r = c >> 5;
+        if (rowbase + r < rend) *(uint4*)(dat + oda[c0]) = *(const uint4*)&al[(kg * (R + 1) + r) * 8];
+      }
+      if (a.DAT || a.DBP) {
+        bf16 v[RV];
         float sum = 0.f;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          v[j] = al[((dkk >> 3) * (R + 1) + m * 16 + dh8 + j) * 8 + (dkk & 7)];
+        for (int j = 0; j < RV; ++j) {
+          v[j] = al[((dkk >> 3) * (R + 1) + j) * 8 + (dkk & 7)];
           sum += (float)v[j];
         }
-        const int row = rowbase + m * 16 + dh8;
-        if (a.DAT && row < rend) *(uint4*)(a.DAT + dgrow * a.M + (int64_t)t * B + row) = *(const uint4*)v;
-        sum += __shfl_xor(sum, 1);
-        dbacc[m] += sum;   // steps in order
+        if (a.DAT) {
+          bf16* p = a.DAT + (int64_t)t * B + odat;
+#pragma unroll
+          for (int j = 0; j < RV; j += 8)
+            if (rowbase + j < rend) *(uint4*)(p + j) = *(const uint4*)&v[j];
+        }
+        dbacc += sum;   // steps in order
       }
     }
   }
-  if (a.DBP && (tid & 1) == 0) {
-#pragma unroll
-    for (int m = 0; m < MB; ++m)
-      if (rowbase + m * 16 < rend) a.DBP[(int64_t)((rowbase + m * 16) / 16) * 8 * H + dgrow] = dbacc[m];
-  }
+  if (a.DBP && tid >= NTH / 2 && rowbase < rend) a.DBP[(int64_t)(rowbase / RV) * 8 * H + dgrow] = dbacc;
 }
 
 // The recurrence status block (at the end of the activation workspace): an
@@ -717,11 +736,9 @@ __global__ void status_reset_kernel(int* status) {
 // ---------------------------------------------------------------------------
 // Host side.
 // ---------------------------------------------------------------------------
-size_t persist_lds_bytes(int H, bool backward, int MB) {
-  const size_t R = 16 * (size_t)MB;
-  const size_t run = backward ? (size_t)32 * (R + 1) * 16 + 2 * R * PU * 4
-                              : (size_t)(H / 8) * (R + 1) * 16 + (size_t)4 * MB * 4 * 64 * 16 +
-                                    (MB == 1 ? (size_t)16 * PU * (4 + 2 + 8) : 0);
+size_t persist_lds_bytes(int H, bool backward, int RV) {
+  const size_t run = backward ? (size_t)32 * 17 * 16 + (size_t)(NTH / (16 * RV)) * RV * PU * 4
+                              : (size_t)(H / 8) * 17 * 16 + (size_t)4 * 4 * 64 * 16 + (size_t)2 * RV * PU * (4 + 2 + 8);
   return std::max(run, (size_t)STAGE_BYTES);
 }
 
@@ -755,12 +772,12 @@ static bool force_cooperative() {
   return e && e[0] == '1';
 }
 
-template <int MB, bool BWD>
+template <int RV, bool BWD>
 static hipError_t launch_one(PersistArgs a, hipStream_t s) {
   const void* fn;
-  if constexpr (BWD) fn = (const void*)lstm_bwd_persist<MB>;
-  else fn = (const void*)lstm_fwd_persist<MB>;
-  const size_t lds = persist_lds_bytes(a.H, BWD, MB);
+  if constexpr (BWD) fn = (const void*)lstm_bwd_persist<RV>;
+  else fn = (const void*)lstm_fwd_persist<RV>;
+  const size_t lds = persist_lds_bytes(a.H, BWD, RV);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   const dim3 grid(2 * a.NS * (a.H / PU)), block(NTH);
@@ -804,25 +821,30 @@ static hipError_t launch_one(PersistArgs a, hipStream_t s) {
   return e;
 }
 
-// Rows per workgroup (16*MB, MB <= PERSIST_MAX_MB) and rows per launch: as
-// few row blocks per workgroup as fill the chip (one workgroup per CU);
-// more rows by chunking.  False if no launch fits.
-static bool persist_plan(int H, int B, int* MBo, int* chunko) {
+// Rows per workgroup and rows per launch: 8 rows (half of each MFMA tile
+// idle, half the cell work and exchange per workgroup) when the batch fits
+// the chip that way (one workgroup per CU), else 16; more rows by chunking.
+// False if no launch fits.
+static bool persist_plan(int H, int B, int* RVo, int* chunko) {
   const int NM = H / PU;
   const int max_ns = std::min(persist_max_wg() / (2 * NM), PERSIST_MAX_SLICES);
   if (max_ns < 1) return false;
-  int MB = 1;
-  while (MB < PERSIST_MAX_MB && (B + 16 * MB - 1) / (16 * MB) > max_ns) MB *= 2;
-  *MBo = MB;
-  *chunko = std::min(B, max_ns * 16 * MB);
+  const int RV = (B + 7) / 8 <= max_ns ? 8 : 16;
+  *RVo = RV;
+  *chunko = std::min(B, max_ns * RV);
   return true;
+}
+
+int persist_rows_per_workgroup(int H, int B) {
+  int RV, chunk;
+  return persist_plan(H, B, &RV, &chunk) ? RV : 16;
 }
 
 bool persist_bwd_needs_wt(int, int) { return false; }
 
 hipError_t persist_clear(bool backward, const PersistArgs& a, hipStream_t s) {
-  int MB, chunk;
-  if (!persist_plan(a.H, a.B, &MB, &chunk)) return hipErrorInvalidValue;
+  int RV, chunk;
+  if (!persist_plan(a.H, a.B, &RV, &chunk)) return hipErrorInvalidValue;
   // both exchange slots start without any valid tag; the forward's clear
   // also initialises the status block of a fresh workspace
   const int64_t words = backward ? (int64_t)2 * 2 * ((chunk + 3) / 4) * (a.H / PU) * a.H
@@ -844,18 +866,18 @@ hipError_t persist_status_reset(int* status, hipStream_t s) {
 }
 
 hipError_t persist_layer(bool backward, PersistArgs a, hipStream_t s) {
-  int MB, chunk;
-  if (!persist_plan(a.H, a.B, &MB, &chunk)) return hipErrorInvalidValue;
+  int RV, chunk;
+  if (!persist_plan(a.H, a.B, &RV, &chunk)) return hipErrorInvalidValue;
   for (int b0 = 0; b0 < a.B; b0 += chunk) {
     PersistArgs c = a;
     c.b0 = b0;
     c.rows = std::min(chunk, a.B - b0);
-    c.NS = (c.rows + 16 * MB - 1) / (16 * MB);
+    c.NS = (c.rows + RV - 1) / RV;
     // the launch's position in the call (the caller's tag numbers the layers
     // in the order the call runs them)
     c.seq = a.tag * (uint32_t)cdiv(a.B, chunk) + (uint32_t)(b0 / chunk);
-    static_assert(PERSIST_MAX_MB == 1, "one 16-row block per workgroup: the only instantiated kernels");
-    const hipError_t e = backward ? launch_one<1, true>(c, s) : launch_one<1, false>(c, s);
+    const hipError_t e = RV == 8 ? (backward ? launch_one<8, true>(c, s) : launch_one<8, false>(c, s))
+                                 : (backward ? launch_one<16, true>(c, s) : launch_one<16, false>(c, s));
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -15,7 +15,8 @@ struct PersistArgs {
   const float* DY;    // backward: gradient reaching the layer output [M][2H]
   uint64_t* X;        // step-exchange words (see lstm_persist.hip), PERSIST_XCH_BYTES
   bf16* DAT;          // backward, optional: da also frame-contiguous [8H][M] (needs B % 8 == 0)
-  float* DBP;         // backward, optional: sums of da over 16-row blocks and all steps [cdiv(B,16)][8H]
+  float* DBP;         // backward, optional: sums of da over each workgroup's rows and all steps
+                      // [cdiv(B, rows per workgroup)][8H] (see persist_rows_per_workgroup)
   int64_t M;          // frames, T*B (DAT row length)
   int* status;        // recurrence status block (sticky flag, see persist_status_reset)
   uint32_t tag;       // caller: the layer's position in the order the call runs the layers
@@ -24,11 +25,10 @@ struct PersistArgs {
   uint32_t seq;       // the launch's position among the call's launches (filled in by persist_layer)
 };
 
-// At most this many batch slices of 16*MB rows per launch (MB <= PERSIST_MAX_MB),
-// so one launch covers at most PERSIST_MAX_ROWS rows.
+// At most this many batch slices of 8 or 16 rows per launch, so one launch
+// covers at most PERSIST_MAX_ROWS rows.
 #define PERSIST_MAX_SLICES 32
-#define PERSIST_MAX_MB 1   // two row blocks per workgroup spill registers next to the W_hh slice
-#define PERSIST_MAX_ROWS (PERSIST_MAX_SLICES * 16 * PERSIST_MAX_MB)
+#define PERSIST_MAX_ROWS (PERSIST_MAX_SLICES * 16)
 // Exchange buffer: 2 slots x 2 directions x row quads x (H/64 members) x H
 // units words of 8 bytes (the backward's partial sums, four rows per word;
 // the forward uses H/4 words per row, never more).
@@ -43,6 +43,9 @@ static inline size_t persist_xch_bytes(int B, int H) {
 // True if the persistent kernels handle this H (a multiple of 64, at most
 // 512: a member's 256 W_hh rows fit in its registers); any T.
 bool persist_supported(int H, int T);
+// Batch rows per persistent workgroup (8 or 16) for this H and B: the row
+// block of the BPTT's bias partial sums (PersistArgs::DBP).
+int persist_rows_per_workgroup(int H, int B);
 // Whether the persistent BPTT of a layer reads W_hh^T (PersistArgs::WT):
 // never (its W_hh rows are read as they lie).
 bool persist_bwd_needs_wt(int H, int B);
