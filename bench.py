@@ -43,6 +43,10 @@ def kernel_work(name, c, n_params):
         # the recurrent products h_prev W_hh^T (forward) or da W_hh (BPTT);
         # the first step of each direction has no previous state
         return "mfma", L * (T - 1) * 2 * 2 * B * 4 * H * H, "flop", None
+    if name == "gemm_bwd_group":
+        # per layer in one grouped launch: dW_ih, dW_hh and (above layer 0) dX
+        return "mfma", (sum(2 * 2 * 4 * H * d * M for d in Dl) + L * 2 * 2 * 4 * H * H * (T - 1) * B
+                        + (L - 1) * 2 * M * 2 * H * 8 * H), "flop", L
     if name == "gemm_dwih":
         return "mfma", sum(2 * 2 * 4 * H * d * M for d in Dl), "flop", L
     if name == "gemm_dwhh":
@@ -108,17 +112,20 @@ def peak_for(bound, precision):
     return (PEAK_BF16_TFLOPS if precision == "bf16" else PEAK_FP32_TFLOPS), "TFLOP/s"
 
 
-def cpu_baseline(cfg, budget_s=12.0):
+def cpu_baseline(cfg, budget_s=12.0, one_thread_s=6.0):
     """The float64 oracle on the host cores, on a bounded slice of the same
     workload: the full layer dimensions with B=16 sequences, whole steps
-    (gradient + update) repeated until the time budget is spent."""
+    (gradient + update) repeated until the time budget is spent; then the
+    same on one BLAS thread.  Frames/s of the slice (the oracle's cost is
+    linear in B, so the slice's rate is the workload's)."""
     import numpy as np
     from oracle import blstm_ref as ref
     from paper_1907_05701_amd import inputs
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
+        threadpool_limits = None
         threads = os.cpu_count()
     Bs = min(16, cfg["B"])
     dims = ref.Dims(L=cfg["L"], D=cfg["D"], H=cfg["H"], P=cfg["P"], K=cfg["K"], T=cfg["T"], B=Bs)
@@ -127,18 +134,104 @@ def cpu_baseline(cfg, budget_s=12.0):
     peer = inputs.peer(theta)
     x = inputs.features(dims.T, Bs, dims.D)
     lab = inputs.labels(dims.T, Bs, dims.K, dist=cfg["label_dist"])
-    steps, t0 = 0, time.perf_counter()
-    while True:
-        g = ref.learner_gradient(theta, dims, x, lab)
-        ref.adpsgd_update(theta, peer, g["grad"], cfg["lr"])
-        steps += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or steps >= 50:
-            break
-    return {"value": round(steps * dims.T * Bs / el, 2), "unit": "frames/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"{steps} float64 oracle step(s) (gradient + update) at the workload's layer "
-                      f"dimensions with B={Bs} of {cfg['B']} sequences, {el:.1f} s"}
+
+    def rate(budget):
+        steps, t0 = 0, time.perf_counter()
+        while True:
+            g = ref.learner_gradient(theta, dims, x, lab)
+            ref.adpsgd_update(theta, peer, g["grad"], cfg["lr"])
+            steps += 1
+            el = time.perf_counter() - t0
+            if el >= budget or steps >= 50:
+                return steps, el
+
+    steps, el = rate(budget_s)
+    out = {"value": round(steps * dims.T * Bs / el, 2), "unit": "frames/s", "cores": int(threads),
+           "kind": "oracle", "nproc": os.cpu_count(), "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
+           "sample": f"{steps} float64 oracle step(s) (gradient + update) at the workload's layer "
+                     f"dimensions with B={Bs} of {cfg['B']} sequences, {el:.1f} s on {threads} BLAS threads"}
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            s1, e1 = rate(one_thread_s)
+        out["one_thread_value"] = round(s1 * dims.T * Bs / e1, 2)
+        out["one_thread_sample"] = f"{s1} step(s), {e1:.1f} s on 1 BLAS thread"
+    return out
+
+
+CLASSES = {
+    "gate_projection": ("gemm_gx",),
+    "backward_products": ("gemm_bwd_group", "gemm_dwih", "gemm_dwhh", "gemm_dx"),
+    "head_products": ("gemm_z", "gemm_logits", "gemm_logits_ds", "gemm_dws", "gemm_dz", "gemm_dwl", "gemm_dy"),
+    "recurrence_fwd": ("lstm_rec_fwd_persist", "lstm_rec_fwd"),
+    "recurrence_bwd": ("lstm_rec_bwd_persist", "lstm_rec_bwd"),
+}
+
+
+def class_rates(st, cfg, lr, steps):
+    """Per-class MFMA rates of `steps` eager learner steps: each class's
+    algorithmic FLOPs over its kernels' summed event time, against the bf16
+    peak; and the recurrences' time per time step."""
+    from paper_1907_05701_amd import binding as bd
+    import torch
+    bd.blstm_timing_begin("")
+    for _ in range(steps):
+        st.step(lr)
+    per = bd.blstm_timing_end(cap=128)
+    torch.cuda.synchronize()
+    ms = {k: v[1] / steps for k, v in per.items()}
+    mfma = {}
+    for cls, names in CLASSES.items():
+        t = sum(ms.get(k, 0.0) for k in names)
+        flop = 0
+        for k in names:
+            if k not in ms:
+                continue
+            w = kernel_work(k, cfg, st.n)
+            if w is not None and not (k == "gemm_logits_ds"):   # the logits count once (recomputed for ds)
+                flop += w[1]
+        if t > 0:
+            tf = flop / (t * 1e-3) / 1e12
+            mfma[cls] = {"ms_per_step": round(t, 4), "gflop_per_step": round(flop / 1e9, 2),
+                         "tflops": round(tf, 1), "frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 4)}
+    L, T = cfg["L"], cfg["T"]
+    rec = {}
+    for key, cls in (("fwd", "recurrence_fwd"), ("bwd", "recurrence_bwd")):
+        if cls in mfma:
+            rec[key] = round(mfma[cls]["ms_per_step"] * 1e3 / (L * T), 3)
+    return {"mfma": mfma, "recurrence_step_us": rec,
+            "kernel_ms": {k: round(v, 4) for k, v in sorted(ms.items(), key=lambda kv: -kv[1])}}
+
+
+def update_rate(cfg, n, iters):
+    """The fused update alone at the paper's parameter count with 8 resident
+    replica gradients (the update-only workload), timed with HIP events on
+    the launching stream: HBM GB/s of its algorithmic bytes."""
+    import torch
+    from paper_1907_05701_amd import binding as bd
+    from paper_1907_05701_amd import inputs
+    R = 8
+    dev = torch.device("cuda:0")
+    theta0 = inputs.params(n)
+    th = torch.from_numpy(theta0).to(dev)
+    pe = torch.from_numpy(inputs.peer(theta0)).to(dev)
+    gs = [torch.from_numpy(g).to(dev) for g in inputs.replica_grads(n, R)]
+    s = torch.cuda.current_stream()
+    for _ in range(3):
+        bd.adpsgd_step(th, pe, gs, 1.0 / R, cfg["lr"], 0, None)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(s)
+    for _ in range(iters):
+        bd.adpsgd_step(th, pe, gs, 1.0 / R, cfg["lr"], 0, None)
+    e1.record(s)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / iters
+    nbytes = update_bytes(n, R, False, False)
+    gbs = nbytes / us / 1e3
+    del gs, th, pe
+    torch.cuda.empty_cache()
+    return {"n": n, "R": R, "bytes_per_param": nbytes // n, "us": round(us, 2), "GB/s": round(gbs, 1),
+            "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4)}
 
 
 def update_bytes(n, R, write_peer, shadow):
@@ -264,6 +357,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="full_b128")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-update-measure", action="store_true",
+                    help="skip the fused-update (8 replicas) measurement of the main workload")
     ap.add_argument("--breakdown", action="store_true", help="per-kernel times to stderr")
     ap.add_argument("--mode", choices=("graph", "eager"), default="graph",
                     help="replay the timed steps as one HIP graph, or launch them one by one")
@@ -349,6 +444,11 @@ def main():
     st.check_recurrence()   # raises if a persistent launch's exchange wait gave up
     loss = float(st.loss.cpu()[0])
 
+    # per-class achieved rates over a few eager steps with every kernel timed
+    # by HIP events on its stream (each run of per-step launches is one pair)
+    classes = class_rates(st, cfg, lr, steps=min(args.steps, 5))
+    update = update_rate(cfg, st.n, iters=20) if not args.no_update_measure else None
+
     ms_per_step = elapsed * 1e3 / args.steps
     value = frames * args.steps / elapsed
     bound, amount, unit, _ = kernel_work(dominant, cfg, st.n)
@@ -368,7 +468,10 @@ def main():
            "dtype": cfg["precision"], "data": "synthetic",
            "config": {"workload": args.workload, **shape, "frames_per_step": frames, "mode": args.mode,
                       "params": st.n, "label_dist": cfg["label_dist"]},
-           "loss_last_step": loss, "roofline": roofline}
+           "loss_last_step": loss, "roofline": roofline, "mfma_by_class": classes["mfma"],
+           "recurrence_step_us": classes["recurrence_step_us"], "kernel_ms_per_step": classes["kernel_ms"]}
+    if update is not None:
+        out["update_r8"] = update
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg)
     print(json.dumps(out), flush=True)
