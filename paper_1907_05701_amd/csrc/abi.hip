@@ -161,7 +161,9 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   L.S = h; h = align256(h + (size_t)M * L.Kp * es);
   L.LST = h; h = align256(h + (es == 2 ? (size_t)M * cdiv(d->K, 64) * 8 : 0));
   L.LSE = h; h = align256(h + (es == 2 ? (size_t)M * 4 : 0));
-  L.LDB = h; h = align256(h + (es == 2 ? (size_t)cdiv(M, 32) * L.Kp * 4 : 0));   // db_s partials per 32+ frames
+  L.LDB = h; h = align256(h + (es == 2 ? (size_t)cdiv(M, 32) * L.Kp * 4 : 0));   // db_s partials per frame tile (32 frames or more)
+  // bf16: db_l shares of the 128-class strips (W_s^T db_s, per strip)
+  L.DBLP = h; h = align256(h + (es == 2 ? (size_t)cdiv(d->K, 128) * d->P * 4 : 0));
   L.RL = h; h = align256(h + (size_t)M * 4);
   L.DZ = h; h = align256(h + (size_t)M * P * 4);
   L.DZT = h; h = align256(h + (size_t)M * P * es);

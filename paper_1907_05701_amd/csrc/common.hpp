@@ -85,7 +85,7 @@ struct Layout {
   bool write_dat;     // bf16 with B % 8 == 0: BPTT also writes da^T [8H][M] for the weight gradients
   size_t act_bytes;
   // head_ws byte offsets
-  size_t Z, S, LST, LSE, LDB, RL, DZ, DZT, HCSP, HSKP;
+  size_t Z, S, LST, LSE, LDB, RL, DZ, DZT, HCSP, HSKP, DBLP;
   size_t head_bytes;
   size_t ytop_bytes;
   // split-K factors of the weight/input-gradient GEMMs (1 = direct store)

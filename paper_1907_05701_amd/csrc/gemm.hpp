@@ -168,6 +168,14 @@ struct TileLoader {
   }
 };
 
+// Epilogues that combine the waves of a workgroup declare
+// `static constexpr bool workgroup = true` and take apply_wg<BM, WM, WN>(...,
+// lds, tm, tn) instead of apply: every thread of the workgroup calls it once,
+// and the kernel's LDS is theirs after a barrier.
+template <class E, class = void> struct EpiIsWorkgroup : std::false_type {};
+template <class E>
+struct EpiIsWorkgroup<E, std::void_t<decltype(E::workgroup)>> : std::integral_constant<bool, E::workgroup> {};
+
 template <typename T, int BM, int BN, int BK, int WM, int WN, bool AKC, bool BKC, int VA, int VB,
           class Epi, int STAGES = 1>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const Opnd A, const Opnd B, int64_t M,
@@ -286,7 +294,11 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(const Opnd A, const 
       __syncthreads();
     }
   }
-  epi.template apply<FM, FN>(z, sp, m0 + wm * (BM / WM), n0 + wn * (BN / WN), acc, lane);
+  if constexpr (EpiIsWorkgroup<Epi>::value)
+    epi.template apply_wg<BM, WM, WN, FM, FN>(m0 + wm * (BM / WM), n0 + wn * (BN / WN), acc, lane, (char*)&lds[0][0],
+                                              (int)blockIdx.x);
+  else
+    epi.template apply<FM, FN>(z, sp, m0 + wm * (BM / WM), n0 + wn * (BN / WN), acc, lane);
 }
 
 // Plain store epilogue: out[z][sp][m][n] = acc + bias[z][n] + bias2[z][n].

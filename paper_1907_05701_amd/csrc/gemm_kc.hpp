@@ -252,7 +252,10 @@ __device__ __forceinline__ void kc_gemm_tile(const KcArgs& p, const Epi& epi, in
     if (it + STAGES - 1 < ntiles) issue(it + STAGES - 1);
     compute(it);
   }
-  epi.template apply<FM, FN>(z, sp, m0 + wm * (BM / WM), n0 + wn * (BN / WN), acc, lane);
+  if constexpr (EpiIsWorkgroup<Epi>::value)
+    epi.template apply_wg<BM, WM, WN, FM, FN>(m0 + wm * (BM / WM), n0 + wn * (BN / WN), acc, lane, kc_lds, tn);
+  else
+    epi.template apply<FM, FN>(z, sp, m0 + wm * (BM / WM), n0 + wn * (BN / WN), acc, lane);
 }
 
 template <int BM, int BN, int WM, int WN, int STAGES, int BK, bool AKC, bool BKC, class Epi>

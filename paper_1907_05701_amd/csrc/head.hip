@@ -10,6 +10,8 @@
 // one workgroup per frame reduces the row and overwrites it with ds.
 #include <math.h>
 
+#include <cmath>
+
 #include <mutex>
 #include <type_traits>
 
@@ -92,8 +94,16 @@ __global__ __launch_bounds__(256) void softmax_ce_rows_kernel(float* __restrict_
 // lane) and the frame loss lse - s[label].  The logits are thus exact
 // float32 values (bf16 storage of a logit of 20 would carry an error of up
 // to 0.06 into the loss and softmax) and 344 MB of float32 logits are neither
-// written nor read back.
+// written nor read back.  The bias gradients come from the second
+// product's column-sum partials: db_s directly, and db_l = W_s^T db_s (the
+// sum over frames of dz = ds W_s), so no pass reads ds or dz back for them.
+//
+// Exponentials on the hardware base-2 exponential: exp(x) = 2^(x log2 e),
+// with the subtraction of the maximum (or log-sum-exp) and, for a positive
+// loss scale, log2(scale) folded into one fused multiply-add per element.
 // ---------------------------------------------------------------------------
+#define LOG2E_F 1.4426950408889634f
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ void lse_pair(float& m, float& s, float m2, float s2) {
   const float mx = fmaxf(m, m2);
   s = (m == -INFINITY ? 0.f : s * __expf(m - mx)) + (m2 == -INFINITY ? 0.f : s2 * __expf(m2 - mx));
@@ -117,18 +127,19 @@ __device__ __forceinline__ float row16_sum(float v) {
 struct EpiLogitStats {
   const float* bias;   // b_s [K]
   float2* stats;       // [M][nstrip] (maximum, sum of exp(s - maximum))
-  int64_t K, M;        // classes (product rows), frames (product columns)
+  int K, M;            // classes (product rows), frames (product columns)
   int nstrip, srows;
   template <int FM, int FN>
-  __device__ __forceinline__ void apply(int, int, int64_t mw, int64_t nw, f32x4 (&acc)[FM][FN], int lane) const {
-    if (mw >= K) return;
-    const int strip = (int)(mw / srows);
+  __device__ __forceinline__ void apply(int, int, int64_t mw64, int64_t nw64, f32x4 (&acc)[FM][FN], int lane) const {
+    if (mw64 >= K) return;
+    const int mw = (int)mw64, nw = (int)nw64;
+    const int strip = mw / srows;
     float bv[FM][4];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t k = mw + i * 16 + (lane >> 4) * 4 + r;
+        const int k = mw + i * 16 + (lane >> 4) * 4 + r;
         bv[i][r] = k < K ? bias[k] : -INFINITY;
       }
 #pragma unroll
@@ -137,19 +148,23 @@ struct EpiLogitStats {
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, acc[i][j][r] + bv[i][r]);
+        for (int r = 0; r < 4; ++r) {
+          acc[i][j][r] += bv[i][r];   // the logit (the accumulators are not used after this)
+          mx = fmaxf(mx, acc[i][j][r]);
+        }
       float sm = 0.f;
       if (mx != -INFINITY) {
+        const float nm = -mx * LOG2E_F;
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) sm += __expf(acc[i][j][r] + bv[i][r] - mx);
+          for (int r = 0; r < 4; ++r) sm += exp2_hw(fmaf(acc[i][j][r], LOG2E_F, nm));
       }
       // the four lane groups hold the other classes of the same frame
       lse_pair(mx, sm, __shfl_xor(mx, 16), __shfl_xor(sm, 16));
       lse_pair(mx, sm, __shfl_xor(mx, 32), __shfl_xor(sm, 32));
-      const int64_t f = nw + j * 16 + (lane & 15);
-      if ((lane >> 4) == 0 && f < M) stats[f * nstrip + strip] = make_float2(mx, sm);
+      const int f = nw + j * 16 + (lane & 15);
+      if ((lane >> 4) == 0 && f < M) stats[(int64_t)f * nstrip + strip] = make_float2(mx, sm);
     }
   }
 };
@@ -177,33 +192,42 @@ __global__ __launch_bounds__(256) void logit_lse_kernel(const float2* __restrict
 }
 
 // Second product: ds (bf16, [M][Kp], zero in the padding classes), the
-// frame loss at the label's class, and the column sums of ds over the wave's
-// frames (db_s partials, one row per block of `fcols` frames, summed in a
+// frame loss at the label's class, and the column sums of ds over the
+// workgroup's frames (db_s partials, one row per frame tile, summed in a
 // fixed order).  Lane group g = lane / 16 holds classes 4g .. 4g+3 of each
 // 16-class fragment; for a fragment pair (i, i+1) the groups g and g ^ 1
 // swap halves so that each lane stores 8 consecutive classes (16 bytes):
 // even groups classes 8(g/2) .. +7 of fragment i, odd groups those of i+1.
+// Per element: one subtraction, one fused multiply-add, the exponential and
+// the column-sum add; classes past K carry a bias of -inf and frames past M
+// a log-sum-exp of +inf, so both give exact zeros without a test.  The label
+// (at most one class of a frame) is handled in a branch that a lane takes
+// only for the fragment holding it.
 struct EpiSoftmaxDs {
-  const float* bias;
-  const float* lse;
-  const int32_t* labels;
-  bf16* ds;
-  float* rowloss;
-  float* dbp;          // [cdiv(M, fcols)][K] column-sum partials
+  static constexpr bool workgroup = true;
+  const float* bias;      // b_s [K]
+  const float* lse;       // [M]
+  const int32_t* labels;  // [M]
+  bf16* ds;               // [M][Kp]
+  float* rowloss;         // [M]: lse - s[label] (frames with an out-of-range label hold NaN already)
+  float* dbp;             // [frame tiles][K] column-sum partials (one row per workgroup's frames)
   float scale;
-  int64_t K, Kp, M;
-  int fcols;
-  template <int FM, int FN>
-  __device__ __forceinline__ void apply(int, int, int64_t mw, int64_t nw, f32x4 (&acc)[FM][FN], int lane) const {
+  float l2s;              // log2(scale) folded into the exponent (scale > 0 and normal), else NaN
+  int K, Kp, M;
+  template <int BM, int WM, int WN, int FM, int FN>
+  __device__ __forceinline__ void apply_wg(int64_t mw64, int64_t nw64, f32x4 (&acc)[FM][FN], int lane, char* lds,
+                                           int tn) const {
     static_assert(FM % 2 == 0, "fragment pairs");
+    const int mw = (int)mw64, nw = (int)nw64;
     const int g = lane >> 4;
-    float bv[FM][4];
+    const bool fold = l2s == l2s;
+    float bl[FM][4];   // bias * log2(e), -inf past K
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t k = mw + i * 16 + g * 4 + r;
-        bv[i][r] = k < K ? bias[k] : 0.f;
+        const int k = mw + i * 16 + g * 4 + r;
+        bl[i][r] = k < K ? bias[k] * LOG2E_F : -INFINITY;
       }
     float csum[FM][4];
 #pragma unroll
@@ -212,54 +236,172 @@ struct EpiSoftmaxDs {
       for (int r = 0; r < 4; ++r) csum[i][r] = 0.f;
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
-      const int64_t f = nw + j * 16 + (lane & 15);
+      const int f = nw + j * 16 + (lane & 15);
       const bool fok = f < M;
-      const float L = fok ? lse[f] : 0.f;
-      const int lab = fok ? labels[f] : -1;
+      const float L = fok ? lse[f] : INFINITY;
+      int lab = fok ? labels[f] : -1;
+      lab = lab < K ? lab : -1;
+      const float Lc = fold ? fmaf(L, LOG2E_F, -l2s) : L * LOG2E_F;
       uint2 pk[FM];
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          v[r] = exp2_hw(fmaf(acc[i][j][r], LOG2E_F, bl[i][r] - Lc));
+          if (!fold) v[r] *= scale;
+        }
+        const int kb = mw + i * 16 + g * 4;
+        if ((unsigned)(lab - kb) < 4u) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (lab - kb == r) {
+              rowloss[f] = L - (acc[i][j][r] + bias[lab]);
+              v[r] -= scale;
+            }
+        }
         bf16 e[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int64_t k = mw + i * 16 + g * 4 + r;
-          const float sv = acc[i][j][r] + bv[i][r];
-          const float v = (fok && k < K) ? __expf(sv - L) * scale - (k == lab ? scale : 0.f) : 0.f;
-          csum[i][r] += v;
-          e[r] = (bf16)v;
-          if (fok && k == lab) rowloss[f] = L - sv;
+          csum[i][r] += v[r];
+          e[r] = (bf16)v[r];
         }
         pk[i] = *(const uint2*)e;
       }
+      bf16* drow = ds + (int64_t)f * Kp;
 #pragma unroll
       for (int i = 0; i < FM; i += 2) {
         const uint2 send = (g & 1) ? pk[i] : pk[i + 1];
         const uint2 got = make_uint2((uint32_t)__shfl_xor((int)send.x, 16), (uint32_t)__shfl_xor((int)send.y, 16));
         const uint4 v = (g & 1) ? make_uint4(got.x, got.y, pk[i + 1].x, pk[i + 1].y)
                                 : make_uint4(pk[i].x, pk[i].y, got.x, got.y);
-        const int64_t k0 = mw + (i + (g & 1)) * 16 + (g >> 1) * 8;
-        if (fok && k0 < Kp) *(uint4*)(ds + f * Kp + k0) = v;
+        const int k0 = mw + (i + (g & 1)) * 16 + (g >> 1) * 8;
+        if (fok && k0 < Kp) *(uint4*)(drow + k0) = v;
       }
     }
     // column sums over the wave's frames: across the 16 lanes of a group
     // with DPP adds (lane ^ 1, lane ^ 2 within quads, then the half-row and
-    // row mirrors), a fixed order that leaves the sum in every lane
+    // row mirrors), a fixed order that leaves the sum in every lane; then
+    // over the workgroup's frame waves in order through LDS (free once
+    // every wave has left the product loop), one partial row per workgroup
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) csum[i][r] = row16_sum(csum[i][r]);
-    if ((lane & 15) == 0 && nw < M) {
-      float* row = dbp + (nw / fcols) * K;
+    const int wid = threadIdx.x >> 6, wm = wid % WM, wn = wid / WM;
+    float* red = (float*)lds;   // [WN][BM]
+    __syncthreads();
+    if ((lane & 15) == 0) {
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t k = mw + i * 16 + g * 4 + r;
-          if (k < K) row[k] = csum[i][r];
-        }
+        for (int r = 0; r < 4; ++r) red[wn * BM + wm * (BM / WM) + i * 16 + g * 4 + r] = csum[i][r];
+    }
+    __syncthreads();
+    const int m0 = mw - wm * (BM / WM);
+    for (int c = threadIdx.x; c < BM; c += WM * WN * 64) {
+      float sum = 0.f;
+#pragma unroll
+      for (int q = 0; q < WN; ++q) sum += red[q * BM + c];
+      if (m0 + c < K) dbp[(int64_t)tn * K + m0 + c] = sum;
     }
   }
+
 };
+
+// Bias gradients and loss from the second product's outputs, one workgroup
+// of 1024 threads per strip of 128 classes plus one for the loss:
+//   db_s[k] = sum of the column-sum partial rows of class k (four row
+//     quarters, each in row order, then added in quarter order);
+//   share[strip][p] = sum over the strip's classes k of db_s[k] W_s[k][p]
+//     (four quarters of 32 classes, each in class order, then in quarter
+//     order; the bf16 W_s that the dz product multiplies); db_l = W_s^T db_s
+//     is the sum over frames of dz = ds W_s;
+//   loss = scale * sum of the frame losses (1024 strided partial sums,
+//     then a fixed tree).
+// head_bias_final_kernel sums the shares in strip order (64 contiguous
+// ranges, then in range order).  Every loop over memory is unrolled so that
+// a thread has its loads in flight together.
+#define HB_STRIP 128
+__global__ __launch_bounds__(1024) void head_bias_kernel(const float* __restrict__ dbp, int nrows, int K, int P,
+                                                         const bf16* __restrict__ ws, float* __restrict__ share,
+                                                         float* __restrict__ grad_bs, const float* __restrict__ rowloss,
+                                                         int M, float scale, float* __restrict__ loss) {
+  __shared__ float part[4][256];
+  __shared__ float sdb[HB_STRIP];
+  const int tid = threadIdx.x;
+  const int nstrip = (K + HB_STRIP - 1) / HB_STRIP;
+  if ((int)blockIdx.x == nstrip) {
+    float* sh = &part[0][0];
+    float sum = 0.f;
+    for (int f = tid; f < M; f += 1024) sum += rowloss[f];
+    sh[tid] = sum;
+    __syncthreads();
+    for (int w = 512; w > 0; w >>= 1) {
+      if (tid < w) sh[tid] += sh[tid + w];
+      __syncthreads();
+    }
+    if (tid == 0) *loss = scale * sh[0];
+    return;
+  }
+  const int k0 = blockIdx.x * HB_STRIP, kn = min(HB_STRIP, K - k0);
+  {
+    const int c = tid & (HB_STRIP - 1), q = tid / HB_STRIP;   // q < 8: row eighths
+    const int per = (nrows + 7) / 8, r0 = q * per, r1 = min(nrows, r0 + per);
+    float sum = 0.f;
+    if (c < kn) {
+#pragma unroll 8
+      for (int r = r0; r < r1; ++r) sum += dbp[(int64_t)r * K + k0 + c];
+    }
+    part[q >> 1][(q & 1) * HB_STRIP + c] = sum;
+  }
+  __syncthreads();
+  if (tid < HB_STRIP) {
+    float sum = 0.f;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) sum += part[q >> 1][(q & 1) * HB_STRIP + tid];
+    sdb[tid] = sum;
+    if (tid < kn) grad_bs[k0 + tid] = sum;
+  }
+  __syncthreads();
+  const int q = tid >> 8, pl = tid & 255;
+  const int c0 = q * (HB_STRIP / 4), c1 = min(kn, c0 + HB_STRIP / 4);
+  for (int p0 = 0; p0 < P; p0 += 256) {
+    const int p = p0 + pl;
+    float acc = 0.f;
+    if (p < P) {
+#pragma unroll 16
+      for (int c = c0; c < c1; ++c) acc += sdb[c] * (float)ws[(int64_t)(k0 + c) * P + p];
+    }
+    part[q][pl] = acc;
+    __syncthreads();
+    if (q == 0 && p < P) share[(int64_t)blockIdx.x * P + p] = ((part[0][pl] + part[1][pl]) + part[2][pl]) + part[3][pl];
+    __syncthreads();
+  }
+}
+
+// db_l[p] for 16 columns per workgroup: thread (g, column) sums the shares
+// of strip range g (64 contiguous ranges) in order; the ranges are added in
+// order.
+__global__ __launch_bounds__(1024) void head_bias_final_kernel(const float* __restrict__ share, int nstrip, int P,
+                                                               float* __restrict__ grad_bl) {
+  __shared__ float sh[64][16];
+  const int pl = threadIdx.x & 15, g = threadIdx.x >> 4;
+  const int p = blockIdx.x * 16 + pl;
+  const int per = (nstrip + 63) / 64, t0 = g * per, t1 = min(nstrip, t0 + per);
+  float sum = 0.f;
+  if (p < P) {
+#pragma unroll 8
+    for (int t = t0; t < t1; ++t) sum += share[(int64_t)t * P + p];
+  }
+  sh[g][pl] = sum;
+  __syncthreads();
+  if (threadIdx.x < 16 && p < P) {
+    float tot = 0.f;
+    for (int i = 0; i < 64; ++i) tot += sh[i][pl];
+    grad_bl[p] = tot;
+  }
+}
 
 // loss = scale * sum of per-frame losses, in a fixed order.
 __global__ __launch_bounds__(256) void loss_sum_kernel(const float* __restrict__ rowloss, int64_t M,
@@ -313,22 +455,28 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
     const Opnd Aw = opnd(W + lo.Ws, P, P, K), Bz = opnd(Z, P, P, M);
     const bool kc = kc_eligible(Aw, Bz, P, true, true);
     const int srows = (kc && kc_tall(K, M, 1, 1)) ? KcTileTall::BM / KcTileTall::WM : KcTile::BM / KcTile::WM;
-    const int fcols = kc ? KcTile::BN / KcTile::WN : GemmCfgK32::BN / GemmCfgK32::WN;
+    // frames per workgroup tile of the second product (one db_s partial row each)
+    const int ftile = kc ? KcTile::BN : GemmCfgK32::BN;
     static_assert(KcTile::BM / KcTile::WM == GemmCfgK32::BM / GemmCfgK32::WM, "strip rows of the fallback tiles");
-    static_assert(KcTile::BN / KcTile::WN == KcTileTall::BN / KcTileTall::WN, "frame columns of the kc tiles");
+    static_assert(KcTile::BN == KcTileTall::BN, "frame columns of the kc tiles");
     const int nstrip = (int)cdiv(K, srows);
     float2* stats = (float2*)(hws + lo.LST);
     float* lse = (float*)(hws + lo.LSE);
     float* dbp = (float*)(hws + lo.LDB);
-    EpiLogitStats e1{theta + lo.bs, stats, K, M, nstrip, srows};
+    EpiLogitStats e1{theta + lo.bs, stats, K, (int)M, nstrip, srows};
     gemm_launch<T, true, true, V, V>("gemm_logits", s, Aw, Bz, K, M, P, 1, 1, e1);
     BLSTM_LAUNCH("logit_lse", logit_lse_kernel, dim3((unsigned)cdiv(M, 4)), dim3(256), 0, s, stats, nstrip, M, labels,
                  K, lse, RL);
-    EpiSoftmaxDs e2{theta + lo.bs, lse, labels, (bf16*)DS, RL, dbp, scale, K, Kp, M, fcols};
+    const float l2s = (scale > 0.f && std::isnormal(scale)) ? std::log2(scale) : NAN;
+    EpiSoftmaxDs e2{theta + lo.bs, lse, labels, (bf16*)DS, RL, dbp, scale, l2s, K, Kp, (int)M};
     gemm_launch<T, true, true, V, V>("gemm_logits_ds", s, Aw, Bz, K, M, P, 1, 1, e2);
-    BLSTM_LAUNCH("loss_sum", loss_sum_kernel, dim3(1), dim3(256), 0, s, RL, M, scale, loss);
-    // db_s = sum of the per-frame-block partials, in order
-    colsum_parts("colsum_dbs", s, dbp, (int)cdiv(M, fcols), K, K, 0, grad + lo.bs, nullptr);
+    // db_s, db_l and the loss
+    const int nbs = (int)cdiv(K, HB_STRIP);
+    float* share = (float*)(hws + lo.DBLP);
+    BLSTM_LAUNCH("head_bias", head_bias_kernel, dim3((unsigned)nbs + 1), dim3(1024), 0, s, dbp, (int)cdiv(M, ftile),
+                 K, P, (const bf16*)(W + lo.Ws), share, grad + lo.bs, RL, (int)M, scale, loss);
+    BLSTM_LAUNCH("head_bias_final", head_bias_final_kernel, dim3((unsigned)cdiv(P, 16)), dim3(1024), 0, s, share,
+                 nbs, P, grad + lo.bl);
   } else {
     // s = z W_s^T + b_s, then loss and ds in place
     float* S = (float*)(hws + lo.S);
@@ -350,8 +498,8 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
   // transposing W_s each step first)
   gemm_f32<T, true, false, V, V>("gemm_dz", s, opnd(DS, Kp, Kp, M), opnd(W + lo.Ws, P, P, K), M, P,
                                  K, 1, lo.sp_dz, DZ, P, 0, part, DZT, P);
-  // db_l = sum over frames of dz
-  colsum<float>("colsum_dbl", s, DZ, M, P, P, csp, P, 0, grad + lo.bl, nullptr);
+  // db_l = sum over frames of dz (bf16: already summed with db_s)
+  if constexpr (!lp) colsum<float>("colsum_dbl", s, DZ, M, P, P, csp, P, 0, grad + lo.bl, nullptr);
   // dW_l = dz^T y
   gemm_f32<T, false, false, V, V>("gemm_dwl", s, opnd(DZT, P, P, M), opnd(ytop, H2, H2, M), P, H2, M,
                                   1, lo.sp_dWl, grad + lo.Wl, H2, 0, part);
