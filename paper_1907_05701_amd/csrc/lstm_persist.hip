@@ -829,7 +829,11 @@ static bool persist_plan(int H, int B, int* RVo, int* chunko) {
   const int NM = H / PU;
   const int max_ns = std::min(persist_max_wg() / (2 * NM), PERSIST_MAX_SLICES);
   if (max_ns < 1) return false;
-  const int RV = (B + 7) / 8 <= max_ns ? 8 : 16;
+  int RV = (B + 7) / 8 <= max_ns ? 8 : 16;
+  // ADPSGD_BLSTM_ROWS_PER_WG=16 keeps 16 rows per workgroup at any batch
+  // (half the workgroups at B <= 128, for measurements)
+  if (const char* e = getenv("ADPSGD_BLSTM_ROWS_PER_WG"))
+    if (atoi(e) == 16) RV = 16;
   *RVo = RV;
   *chunko = std::min(B, max_ns * RV);
   return true;
