@@ -12,7 +12,9 @@
  *
  * Conventions shared by every call:
  *   - All pointers named theta/grad/x/y/dy/... are DEVICE pointers allocated by
- *     the caller; the library never allocates device memory.  State carried
+ *     the caller; no call allocates device memory (the allocation-free head
+ *     entry point works in a static device array of the library, held from
+ *     the library's load on each device that runs it).  State carried
  *     between calls lives in the caller's act_ws (saved activations, the
  *     recurrence status flag).  Host-side, the library keeps a per-device
  *     side stream with its events (created on first use by an eager
