@@ -85,35 +85,33 @@ __device__ __forceinline__ uint32_t lane_xor2(uint32_t v) {
 // BPTT words: four partial sums (rows 4i
 // .. 4i+3 of one unit) in a 15-bit form that frees the same bits: the bf16
 // of x * 2^-64 (so bf16 exponents 65 .. 190, i.e. 2^-62 <= |x| < 2^65, keep
-// bit 14 clear and the 8-bit significand of the bf16 of x), magnitudes from
-// 2^65 and non-finite values saturated to 2^64; tiny values become bf16
-// subnormals.  Decoding multiplies by 2^64 (exact).
+// bit 14 clear and the 8-bit significand of the bf16 of x), with x * 2^-64
+// clamped to +-(2 - 2^-7), the largest bf16 below 2: larger magnitudes and
+// infinities saturate there, and a NaN becomes -(2 - 2^-7) (v_med3_f32
+// returns the minimum of the non-NaN inputs when one is a quiet NaN); tiny
+// values become bf16 subnormals.  Readers add the scaled values and
+// multiply the sum by 2^64 (exact, as is every step of it: the scaled
+// values stay below 2 in magnitude and bf16 subnormals add exactly).
 // two bf16 values in one dword, `lo` in the low half
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return (uint32_t)__builtin_bit_cast(uint16_t, (bf16)lo) |
-         ((uint32_t)__builtin_bit_cast(uint16_t, (bf16)hi) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{lo, hi}), bf16x2_t));   // one v_cvt_pk_bf16_f32
 }
 // the 15-bit form of four partial sums in one word (tag bits clear)
 __device__ __forceinline__ uint64_t p15x4_encode(f32x4 v) {
-  uint32_t lo = pack_bf16x2(v[0] * 0x1p-64f, v[1] * 0x1p-64f);
-  uint32_t hi = pack_bf16x2(v[2] * 0x1p-64f, v[3] * 0x1p-64f);
-  if ((lo | hi) & 0x40004000u) {   // some |x| >= 2^65 or non-finite: saturate those halves
-    auto fix = [](uint32_t p) {
-      uint32_t r = p;
-      if (p & 0x4000u) r = (r & 0xFFFF0000u) | (p & 0x8000u) | 0x3F80u;
-      if (p & 0x40000000u) r = (r & 0xFFFFu) | (p & 0x80000000u) | 0x3F800000u;
-      return r;
-    };
-    lo = fix(lo);
-    hi = fix(hi);
-  }
+  constexpr float M = 1.9921875f;   // bf16 0x3FFF
+  float c[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) c[q] = __builtin_amdgcn_fmed3f(v[q] * 0x1p-64f, -M, M);
+  const uint32_t lo = pack_bf16x2(c[0], c[1]), hi = pack_bf16x2(c[2], c[3]);
   return ((uint64_t)hi << 32) | lo;
 }
-// the four partial sums of a word (tag bits ignored)
-__device__ __forceinline__ f32x4 p15x4_decode(uint64_t w) {
+// the four scaled partial sums of a word (x * 2^-64; tag bits ignored)
+__device__ __forceinline__ f32x4 p15x4_decode_scaled(uint64_t w) {
   const uint32_t lo = (uint32_t)w & 0xBFFFBFFFu, hi = (uint32_t)(w >> 32) & 0xBFFFBFFFu;
   return f32x4{__builtin_bit_cast(float, lo << 16), __builtin_bit_cast(float, lo & 0xFFFF0000u),
-               __builtin_bit_cast(float, hi << 16), __builtin_bit_cast(float, hi & 0xFFFF0000u)} * 0x1p64f;
+               __builtin_bit_cast(float, hi << 16), __builtin_bit_cast(float, hi & 0xFFFF0000u)};
 }
 __device__ __forceinline__ uint64_t h4_tag(uint32_t seq, int n) {
   const uint32_t t = 1u | (((uint32_t)n >> 1 & 1u) << 1) | ((seq & 3u) << 2);
@@ -596,8 +594,9 @@ __global__ __launch_bounds__(NTH) void lstm_bwd_persist(const PersistArgs a) {
 #pragma unroll
           for (int k = 0; k < GM; ++k) {
             if (k >= mcount) break;
-            sum += p15x4_decode(wv[k]);
+            sum += p15x4_decode_scaled(wv[k]);
           }
+          sum *= 0x1p64f;
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r) dhl[(part * RV + 4 * gqd + r) * PU + (item & 63)] = sum[r];

@@ -325,6 +325,31 @@ def test_long_sequence_bf16(gpu_lib):
                          check_update=False)
 
 
+def test_non_finite_gradients_keep_the_exchange_going(gpu_lib):
+    """dy_top with a NaN row, a row of +-1e30 and a row of +-inf: the BPTT's
+    exchanged partial sums saturate instead of carrying a non-finite value
+    into the tag bits, so no member waits in vain (the recurrence status
+    stays clear) and the non-finite rows reach the gradient as non-finite
+    values while the exchange of every other row goes on."""
+    from paper_1907_05701_amd.step import LearnerStep
+    shape = dict(L=2, D=24, H=128, P=16, K=30, T=5, B=8)
+    say(f"[non-finite] shape={shape}")
+    dims = ref.Dims(**shape)
+    theta = inputs.params(ref.param_count(dims), seed=5)
+    st = LearnerStep(**shape, precision="bf16")
+    st.load(theta, inputs.features(5, 8, 24, seed=6), inputs.labels(5, 8, 30, seed=7))
+    st.forward()
+    st.check_recurrence()
+    dy = torch.from_numpy(np.random.default_rng(8).standard_normal((5, 8, 256)).astype(np.float32))
+    dy[:, 0, :] = float("nan")
+    dy[:, 1, ::2], dy[:, 1, 1::2] = 1e30, -1e30
+    dy[:, 2, ::2], dy[:, 2, 1::2] = float("inf"), float("-inf")
+    st.backward(dy_top=dy.to(st.device))
+    torch.cuda.synchronize()
+    st.check_recurrence()
+    assert not torch.isfinite(st.grad).all().item()
+
+
 @pytest.mark.parametrize("B", [200, 300, 1100], ids=["ragged_slices", "two_chunks", "five_chunks"])
 def test_recurrence_batch_regimes_bf16(gpu_lib, B):
     """Batches whose last 16-row slice is ragged (B=200: 13 slices), that
