@@ -99,10 +99,19 @@ __global__ __launch_bounds__(64) void splitk_reduce4_kernel(const float* __restr
   const int z = blockIdx.z;
   if (n >= N) return;
   const float* p = part + ((int64_t)z * splits * M + m) * N + n;
-  float4 acc = *(const float4*)p;
-  for (int k = 1; k < splits; ++k) {
-    const float4 v = *(const float4*)(p + (int64_t)k * M * N);
-    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  // the first eight summands loaded together, then added in order
+  constexpr int U = 8;
+  float4 v[U];
+#pragma unroll
+  for (int k = 0; k < U; ++k)
+    if (k < splits) v[k] = *(const float4*)(p + (int64_t)k * M * N);
+  float4 acc = v[0];
+#pragma unroll
+  for (int k = 1; k < U; ++k)
+    if (k < splits) { acc.x += v[k].x; acc.y += v[k].y; acc.z += v[k].z; acc.w += v[k].w; }
+  for (int k = U; k < splits; ++k) {
+    const float4 w = *(const float4*)(p + (int64_t)k * M * N);
+    acc.x += w.x; acc.y += w.y; acc.z += w.z; acc.w += w.w;
   }
   if (bias) { acc.x += bias[n]; acc.y += bias[n + 1]; acc.z += bias[n + 2]; acc.w += bias[n + 3]; }
   if (dst) *(float4*)(dst + z * dst_zstride + m * ld + n) = acc;
@@ -186,10 +195,20 @@ static __global__ __launch_bounds__(256) void splitk_reduce_group_kernel(const R
   const uint32_t z = e / r.per, rem = e - z * r.per;
   const uint32_t m = rem / r.N4, n = (rem - m * r.N4) * 4;
   const float* p = r.part + (int64_t)z * r.zin + (int64_t)m * r.N4 * 4 + n;
-  float4 acc = *(const float4*)p;
-  for (int k = 1; k < r.splits; ++k) {
-    const float4 v = *(const float4*)(p + (int64_t)k * r.kstride);
-    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  // the first eight summands loaded together (one memory round trip), then
+  // added in order; any further ones one by one after them
+  constexpr int U = 8;
+  float4 v[U];
+#pragma unroll
+  for (int k = 0; k < U; ++k)
+    if (k < r.splits) v[k] = *(const float4*)(p + (int64_t)k * r.kstride);
+  float4 acc = v[0];
+#pragma unroll
+  for (int k = 1; k < U; ++k)
+    if (k < r.splits) { acc.x += v[k].x; acc.y += v[k].y; acc.z += v[k].z; acc.w += v[k].w; }
+  for (int k = U; k < r.splits; ++k) {
+    const float4 w = *(const float4*)(p + (int64_t)k * r.kstride);
+    acc.x += w.x; acc.y += w.y; acc.z += w.z; acc.w += w.w;
   }
   const int64_t o = (int64_t)z * r.dst_zstride + (int64_t)m * r.ld + n;
   *(float4*)(r.dst + o) = acc;
