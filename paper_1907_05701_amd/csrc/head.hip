@@ -178,9 +178,17 @@ __global__ __launch_bounds__(256) void logit_lse_kernel(const float2* __restrict
   const int lane = threadIdx.x & 63;
   if (m >= M) return;
   float mx = -INFINITY, sm = 0.f;
-  for (int i = lane; i < nstrip; i += 64) {
-    const float2 p = stats[m * nstrip + i];
-    lse_pair(mx, sm, p.x, p.y);
+  // the lane's strips lane, lane + 64, ... combined in that order; eight
+  // loads in flight at a time
+  constexpr int U = 8;
+  for (int i0 = lane; i0 < nstrip; i0 += 64 * U) {
+    float2 p[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (i0 + 64 * u < nstrip) p[u] = stats[m * nstrip + i0 + 64 * u];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (i0 + 64 * u < nstrip) lse_pair(mx, sm, p[u].x, p[u].y);
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) lse_pair(mx, sm, __shfl_xor(mx, off), __shfl_xor(sm, off));
