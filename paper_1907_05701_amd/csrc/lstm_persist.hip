@@ -2,12 +2,15 @@
 // of one layer, for both directions at once, and each workgroup keeps its
 // slice of W_hh in registers for the whole chunk.
 //
-// Work split.  The batch is cut into slices of R = 16*MB rows; a group of
-// NM = H/64 workgroups ("members") owns one (direction, slice) pair, and
-// member m owns hidden units [64m, 64m + 64), i.e. 256 gate rows of W_hh
-// (256 KB at H = 512: 128 VGPRs in each of the workgroup's 8 waves).  Eight
-// members per group instead of sixteen halves the chip-wide exchange volume
-// of every step; at the paper's B = 128 a launch takes 128 workgroups.
+// Work split.  The batch is cut into slices of RV rows (8 when all the
+// batch's 8-row slices fit one launch at one workgroup per CU, else 16,
+// with launches of up to 16 slices), each on 16-row MFMA tiles;
+// a group of NM = H/64 workgroups ("members") owns one (direction, slice)
+// pair, and member m owns hidden units [64m, 64m + 64), i.e. 256 gate rows
+// of W_hh (256 KB at H = 512: 128 VGPRs in each of the workgroup's 8
+// waves).  Eight members per group instead of sixteen halves the chip-wide
+// exchange volume of every step; at the paper's B = 128 a launch takes 256
+// workgroups (2 directions x 16 slices of 8 rows x 8 members).
 //   forward : wave (ub, kh) = (w % 4, w / 4) multiplies h_prev (all H units
 //             of the slice, gathered from the members' published h) by the
 //             four gates of the 16 units of block ub over the k half kh; the
@@ -16,7 +19,7 @@
 //             gate pre-activations for the backward.
 //   backward: the gate derivatives of the member's 64 units (dc stays in
 //             registers), then wave w multiplies the member's own da block
-//             [R x 256 own gate rows] by its W_hh rows for the unit blocks
+//             [16 x 256 own gate rows] by its W_hh rows for the unit blocks
 //             w, w+8, w+16, w+24: partial dh_rec for all H units, published;
 //             each member sums the NM partials of its own units in member
 //             order.
