@@ -29,6 +29,8 @@
 // slot freed by the previous tile and multiplies the current one.
 #pragma once
 
+#include <atomic>
+
 #include "gemm.hpp"
 #include "dma.hpp"
 
@@ -320,16 +322,23 @@ static inline KcArgs kc_args(const Opnd& A, const Opnd& B, int64_t M, int64_t N,
   return p;
 }
 
+// Raises a kernel's dynamic LDS limit once per device (raised: that
+// kernel's own mask of devices done so far).
+static inline void kc_raise_lds_limit(const void* fn, size_t bytes, std::atomic<uint64_t>& raised) {
+  int dev = 0;
+  const bool known = hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64;
+  if (known && (raised.load(std::memory_order_relaxed) >> dev & 1u)) return;
+  (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (known) raised.fetch_or((uint64_t)1 << dev, std::memory_order_relaxed);
+}
+
 template <class C, bool AKC, bool BKC, class Epi>
 static inline void gemm_kc_launch(const char* name, hipStream_t s, const Opnd& A, const Opnd& B, int64_t M,
                                   int64_t N, int64_t K, int batches, int splits, const Epi& epi) {
   const KcArgs p = kc_args<C, AKC, BKC>(A, B, M, N, K, batches, splits);
   auto fn = gemm_kc_kernel<C::BM, C::BN, C::WM, C::WN, C::STAGES, C::BK, AKC, BKC, Epi>;
-  static bool attr_set = false;   // raising the LDS limit is per function, once
-  if (!attr_set) {
-    (void)hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::lds_bytes);
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> lds_raised{0};
+  kc_raise_lds_limit((const void*)fn, C::lds_bytes, lds_raised);
   BLSTM_LAUNCH(name, fn, dim3((unsigned)p.total), dim3(C::WM * C::WN * 64),
                C::lds_bytes, s, p, epi);
 }
@@ -405,11 +414,8 @@ static inline bool gemm_kc_group_launch(const char* name, hipStream_t s, int n, 
   }
   g.start[n] = start;
   auto fn = gemm_kc_group_kernel<C::BM, C::BN, C::WM, C::WN, C::STAGES, C::BK, AKC, BKC, Epi>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    (void)hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::lds_bytes);
-    attr_set = true;
-  }
+  static std::atomic<uint64_t> lds_raised{0};
+  kc_raise_lds_limit((const void*)fn, C::lds_bytes, lds_raised);
   BLSTM_LAUNCH(name, fn, dim3((unsigned)start), dim3(C::WM * C::WN * 64), C::lds_bytes, s, g);
   return true;
 }
