@@ -299,7 +299,7 @@ static inline bool kc_operand_ok(const Opnd& o, int64_t K, bool kc) {
 
 static inline int kc_seg_shift(const Opnd& o) { return o.seg > 0 ? __builtin_ctzll((unsigned long long)o.seg) : 0; }
 
-static int kc_group_rows = 4;   // measured best at the learner-step shapes
+static constexpr int kc_group_rows = 4;   // measured best at the learner-step shapes
 
 template <class C, bool AKC, bool BKC>
 static inline KcArgs kc_args(const Opnd& A, const Opnd& B, int64_t M, int64_t N, int64_t K, int batches, int splits) {
