@@ -385,6 +385,20 @@ def test_non_finite_gradients_keep_the_exchange_going(gpu_lib):
     assert not torch.isfinite(st.grad).all().item()
 
 
+@pytest.mark.parametrize("H", [192, 320, 448], ids=["3_members", "5_members", "7_members"])
+def test_recurrence_member_counts_bf16(gpu_lib, H):
+    """Groups of 3, 5 and 7 members (H = 64 x members): the BPTT's gathering
+    threads split the members into two parts of unequal size, and the
+    forward's gathered words per row (H / 4) are not a power of two."""
+    from paper_1907_05701_amd import binding as bd
+    bd.blstm_timing_begin("lstm_rec")
+    run_step_and_compare(dict(L=2, D=40, H=H, P=32, K=50, T=5, B=24), "bf16", BF16_TOL, seed=13,
+                         check_update=False)
+    got = bd.blstm_timing_end()
+    if os.environ.get("ADPSGD_BLSTM_NO_PERSIST") != "1":   # the persistent kernels ran, one launch per layer
+        assert got["lstm_rec_fwd_persist"][0] == 2 and got["lstm_rec_bwd_persist"][0] == 2, got
+
+
 @pytest.mark.parametrize("B", [200, 300, 1100], ids=["ragged_slices", "two_chunks", "five_chunks"])
 def test_recurrence_batch_regimes_bf16(gpu_lib, B):
     """Batches whose last 16-row slice is ragged (B=200: 13 slices), that
