@@ -322,9 +322,11 @@ struct EpiSoftmaxDs {
 //   db_s[k] = sum of the column-sum partial rows of class k (four row
 //     quarters, each in row order, then added in quarter order);
 //   share[strip][p] = sum over the strip's classes k of db_s[k] W_s[k][p]
-//     (four quarters of 32 classes, each in class order, then in quarter
-//     order; the bf16 W_s that the dz product multiplies); db_l = W_s^T db_s
-//     is the sum over frames of dz = ds W_s;
+//     (with W_s rows 16-byte aligned and P <= 256: 32 groups of 4 classes,
+//     each thread 8 adjacent columns of one group by 16-byte loads, groups
+//     added in order; otherwise four quarters of 32 classes, each in class
+//     order, then in quarter order; the bf16 W_s that the dz product
+//     multiplies); db_l = W_s^T db_s is the sum over frames of dz = ds W_s;
 //   loss = scale * sum of the frame losses (1024 strided partial sums,
 //     then a fixed tree).
 // head_bias_final_kernel sums the shares in strip order (64 contiguous
@@ -334,9 +336,10 @@ struct EpiSoftmaxDs {
 __global__ __launch_bounds__(1024) void head_bias_kernel(const float* __restrict__ dbp, int nrows, int K, int P,
                                                          const bf16* __restrict__ ws, float* __restrict__ share,
                                                          float* __restrict__ grad_bs, const float* __restrict__ rowloss,
-                                                         int M, float scale, float* __restrict__ loss) {
+                                                         int M, float scale, float* __restrict__ loss, bool vec) {
   __shared__ float part[4][256];
   __shared__ float sdb[HB_STRIP];
+  __shared__ float gsum[HB_STRIP / 4][256];   // vec: class-group sums per column
   const int tid = threadIdx.x;
   const int nstrip = (K + HB_STRIP - 1) / HB_STRIP;
   if ((int)blockIdx.x == nstrip) {
@@ -372,6 +375,40 @@ __global__ __launch_bounds__(1024) void head_bias_kernel(const float* __restrict
     if (tid < kn) grad_bs[k0 + tid] = sum;
   }
   __syncthreads();
+  if (vec) {
+    // thread (class group cg of 4 classes, 8 adjacent columns from p8): four
+    // 16-byte loads of W_s in flight together; the 32 group sums then added
+    // in group order
+    const int cg = tid >> 5, p8 = (tid & 31) * 8;
+    float acc[8];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) acc[v] = 0.f;
+    if (p8 < P) {
+      uint4 wv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int c = cg * 4 + i;
+        wv[i] = c < kn ? *(const uint4*)(ws + (int64_t)(k0 + c) * P + p8) : make_uint4(0u, 0u, 0u, 0u);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float dv = cg * 4 + i < kn ? sdb[cg * 4 + i] : 0.f;
+        const bf16* e = (const bf16*)&wv[i];
+#pragma unroll
+        for (int v = 0; v < 8; ++v) acc[v] += dv * (float)e[v];
+      }
+#pragma unroll
+      for (int v = 0; v < 8; ++v) gsum[cg][p8 + v] = acc[v];
+    }
+    __syncthreads();
+    if (tid < P) {
+      float t = 0.f;
+#pragma unroll 8
+      for (int g = 0; g < HB_STRIP / 4; ++g) t += gsum[g][tid];
+      share[(int64_t)blockIdx.x * P + tid] = t;
+    }
+    return;
+  }
   const int q = tid >> 8, pl = tid & 255;
   const int c0 = q * (HB_STRIP / 4), c1 = min(kn, c0 + HB_STRIP / 4);
   for (int p0 = 0; p0 < P; p0 += 256) {
@@ -481,8 +518,10 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
     // db_s, db_l and the loss
     const int nbs = (int)cdiv(K, HB_STRIP);
     float* share = (float*)(hws + lo.DBLP);
+    // W_s rows read 8 columns at a time when they are 16-byte aligned
+    const bool hb_vec = P % 8 == 0 && P <= 256 && ((uintptr_t)(W + lo.Ws) & 15) == 0;
     BLSTM_LAUNCH("head_bias", head_bias_kernel, dim3((unsigned)nbs + 1), dim3(1024), 0, s, dbp, (int)cdiv(M, ftile),
-                 K, P, (const bf16*)(W + lo.Ws), share, grad + lo.bs, RL, (int)M, scale, loss);
+                 K, P, (const bf16*)(W + lo.Ws), share, grad + lo.bs, RL, (int)M, scale, loss, hb_vec);
     BLSTM_LAUNCH("head_bias_final", head_bias_final_kernel, dim3((unsigned)cdiv(P, 16)), dim3(1024), 0, s, share,
                  nbs, P, grad + lo.bl);
   } else {
