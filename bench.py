@@ -44,9 +44,13 @@ def kernel_work(name, c, n_params):
         # the first step of each direction has no previous state
         return "mfma", L * (T - 1) * 2 * 2 * B * 4 * H * H, "flop", None
     if name == "gemm_bwd_group":
-        # per layer in one grouped launch: dW_ih, dW_hh and (above layer 0) dX
-        return "mfma", (sum(2 * 2 * 4 * H * d * M for d in Dl) + L * 2 * 2 * 4 * H * H * (T - 1) * B
-                        + (L - 1) * 2 * M * 2 * H * 8 * H), "flop", L
+        # per layer above layer 0, right after its BPTT: dX (the weight
+        # gradients of every layer follow the last BPTT, in gemm_dw_group)
+        return "mfma", (L - 1) * 2 * M * 2 * H * 8 * H, "flop", L - 1
+    if name == "gemm_dw_group":
+        # dW_ih and dW_hh of every layer, up to 8 products per launch
+        return "mfma", (sum(2 * 2 * 4 * H * d * M for d in Dl) + L * 2 * 2 * 4 * H * H * (T - 1) * B), "flop", \
+            -(-2 * L // 8)
     if name == "gemm_dwih":
         return "mfma", sum(2 * 2 * 4 * H * d * M for d in Dl), "flop", L
     if name == "gemm_dwhh":
@@ -160,7 +164,7 @@ def cpu_baseline(cfg, budget_s=12.0, one_thread_s=6.0):
 
 CLASSES = {
     "gate_projection": ("gemm_gx",),
-    "backward_products": ("gemm_bwd_group", "gemm_dwih", "gemm_dwhh", "gemm_dx"),
+    "backward_products": ("gemm_bwd_group", "gemm_dw_group", "gemm_dwih", "gemm_dwhh", "gemm_dx"),
     "head_products": ("gemm_z", "gemm_logits", "gemm_logits_ds", "gemm_dws", "gemm_dz", "gemm_dwl", "gemm_dy"),
     "recurrence_fwd": ("lstm_rec_fwd_persist", "lstm_rec_fwd"),
     "recurrence_bwd": ("lstm_rec_bwd_persist", "lstm_rec_bwd"),

@@ -110,9 +110,10 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   // bf16 with B % 8 == 0: the BPTT kernels also write da frame-contiguous
   // (da^T), the A operand of the weight gradients
   L.write_dat = es == 2 && d->B % 8 == 0;
-  // da^T [8H][M] and per-step bias partials, two of each (alternating layers)
+  // da^T [8H][M], one per layer (the weight gradients of every layer run
+  // after the last BPTT; the side-stream path alternates two of them)
   L.dat_bytes = align256(L.write_dat ? (size_t)M * 8 * H * es : 0);
-  L.DAT = a; a += 2 * L.dat_bytes;
+  L.DAT = a; a += (size_t)std::max(2, d->L) * L.dat_bytes;
   // per-step 16-row partials (per-step BPTT) or per-workgroup partials over
   // all steps (persistent BPTT, 8-row workgroups)
   L.dbp_bytes = align256((size_t)std::max<int64_t>((int64_t)d->T * cdiv(d->B, 16), cdiv(d->B, 8)) * 8 * H * 4);

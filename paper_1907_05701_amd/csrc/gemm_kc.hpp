@@ -268,7 +268,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kc_kernel(const KcArgs p, c
 // Several independent products in one launch (fills the chip when each alone
 // would not): product i owns workgroups [start[i], start[i+1]); every start is
 // a multiple of 8 so that the XCD-aware tile order of each product holds.
-#define KC_MAX_GROUP 4
+#define KC_MAX_GROUP 8
 template <class Epi>
 struct KcGroup {
   KcArgs p[KC_MAX_GROUP];

@@ -561,10 +561,18 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     side = side_stream();
   hipStream_t ss = side ? side->st : s;
   float* part_side = side ? (float*)(ws + lo.SKP2) : part;
+  // bf16 with da^T and no side stream: each layer's weight-gradient products
+  // wait for one grouped launch after the last BPTT (their da^T kept per
+  // layer), so a layer's own launch after its BPTT holds only dX, the
+  // product the next BPTT needs; the deferred products all have about the
+  // same k length and fill whole rounds of the chip together
+  const bool defer = lp && lo.write_dat && !side;
+  F32Job deferred[2 * MAX_LAYERS];
+  int nd = 0;
   const float* dY = dytop;
   for (int l = lo.L - 1; l >= 0; --l) {
     const int par = side ? (l & 1) : 0;
-    T* DATl = (T*)(ws + lo.DAT + par * lo.dat_bytes);
+    T* DATl = (T*)(ws + lo.DAT + (defer ? l : par) * lo.dat_bytes);
     float* DBPl = (float*)(ws + lo.DBP + par * lo.dbp_bytes);
     if (side && l + 2 < lo.L) (void)hipStreamWaitEvent(s, side->dw_done[l + 2], 0);
     const T* Xl = l == 0 ? (const T*)(ws + lo.X0) : (const T*)(ws + lo.Y[l - 1]);
@@ -632,8 +640,17 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
                       lo.sp_dWih[l], grad + lo.Wih[l][0], Dl, lo.Wih[l][1] - lo.Wih[l][0], part_ih};
         g[1] = F32Job{opnd(DAT + B, M, (int)Kr, 4 * H, 4 * H * M - B), opnd(Yl, 2 * H, H, Kr, (int64_t)B * 2 * H + H),
                       4 * H, H, Kr, 2, lo.sp_dWhh[l], grad + lo.Whh[l][0], H, lo.Whh[l][1] - lo.Whh[l][0], part_hh};
+        // the whole k range per tile (the deferred launch has tiles enough;
+        // the side-stream path does the same, so that both sum alike)
+        g[0].splits = g[1].splits = 1;
         int ng = 2;
-        if (!side && l > 0)
+        if (defer) {
+          deferred[nd++] = g[0];
+          deferred[nd++] = g[1];
+          ng = 0;
+        }
+        const bool dx_here = !side && l > 0;
+        if (dx_here)
           g[ng++] = F32Job{opnd(DA, 8 * H, 8 * H, M), Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0, part_dx};
         // db_ih = db_hh = sum over frames of da, from the BPTT kernel's
         // per-row-block partials, in the same reduction launch
@@ -641,15 +658,19 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
         const ColSumJob cs{DBPl, dbp_rows, 2, 4 * H, 8 * H, 4 * H,
                            grad + lo.bih[l][0], grad + lo.bhh[l][0], lo.bih[l][1] - lo.bih[l][0]};
         const bool with_db = step_fused && colsum_job_ok(cs);
-        if (gemm_f32_group<true, false>("gemm_bwd_group", ss, ng, g, with_db ? &cs : nullptr)) {
+        if (ng == 0) {
+          // (layer 0, weight gradients deferred: the bias sums alone, by the
+          // same reduction)
+          db_done = with_db && colsum_job_launch("splitk_reduce_group", ss, cs);
+        } else if (gemm_f32_group<true, false>("gemm_bwd_group", ss, ng, g, with_db ? &cs : nullptr)) {
           db_done = with_db;
         } else {
-          static const char* const nm[3] = {"gemm_dwih", "gemm_dwhh", "gemm_dx"};
           for (int i = 0; i < ng; ++i)
-            gemm_f32<T, true, false, V, V>(nm[i], ss, g[i].A, g[i].B, g[i].M, g[i].N, g[i].K, g[i].batches,
-                                           g[i].splits, g[i].dst, g[i].ld, g[i].dst_zstride, g[i].part);
+            gemm_f32<T, true, false, V, V>(i == ng - 1 && dx_here ? "gemm_dx" : (i == 0 ? "gemm_dwih" : "gemm_dwhh"),
+                                           ss, g[i].A, g[i].B, g[i].M, g[i].N, g[i].K, g[i].batches, g[i].splits,
+                                           g[i].dst, g[i].ld, g[i].dst_zstride, g[i].part);
         }
-        dx_done = dx_done || ng == 3;
+        dx_done = dx_done || dx_here;
         dw_done = true;
       }
     }
@@ -683,6 +704,18 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       gemm_f32<T, true, false, V, V>("gemm_dx", s, A, Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0, part_dx);
     }
     if (l > 0) dY = dst_dx;
+  }
+  // the deferred weight gradients, KC_MAX_GROUP products per launch (top
+  // layers first, so the smaller layer-0 dW_ih rides in the last one)
+  for (int i0 = 0; i0 < nd; i0 += KC_MAX_GROUP) {
+    const int n = std::min(KC_MAX_GROUP, nd - i0);
+    if (!gemm_f32_group<true, false>("gemm_dw_group", s, n, deferred + i0)) {
+      for (int i = i0; i < i0 + n; ++i) {
+        const F32Job& j = deferred[i];
+        gemm_f32<T, true, false, V, V>((i & 1) ? "gemm_dwhh" : "gemm_dwih", s, j.A, j.B, j.M, j.N, j.K, j.batches,
+                                       1, j.dst, j.ld, j.dst_zstride, part);
+      }
+    }
   }
   if (side) (void)hipStreamWaitEvent(s, side->dw_done[0], 0);   // join before returning
   return blstm_check_launch("blstm_bwd");

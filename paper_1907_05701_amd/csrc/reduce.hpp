@@ -221,6 +221,30 @@ static inline bool colsum_job_ok(const ColSumJob& c) {
          (int64_t)c.batches * c.N / 4 < ((int64_t)1 << 31);
 }
 
+// The reduction job of a column sum (rows summed in row order).
+static inline ReduceJob colsum_reduce_job(const ColSumJob& cs, int start) {
+  ReduceJob r;
+  r.part = cs.part; r.dst = cs.dst; r.dst2 = cs.dst2;
+  r.N4 = (uint32_t)(cs.N / 4); r.per = r.N4; r.count = (uint32_t)((int64_t)cs.batches * cs.N / 4);
+  r.ld = 0; r.dst_zstride = cs.dst_zstride;
+  r.kstride = cs.kstride; r.zin = cs.zin;
+  r.splits = cs.rows; r.start = start;
+  return r;
+}
+
+// A column sum alone, through the same reduction kernel (so the same
+// summation order as when it rides on a grouped launch); false if the job
+// does not qualify.
+static inline bool colsum_job_launch(const char* name, hipStream_t s, const ColSumJob& cs) {
+  if (!colsum_job_ok(cs)) return false;
+  ReduceGroup rg;
+  rg.n = 1;
+  rg.j[0] = colsum_reduce_job(cs, 0);
+  BLSTM_LAUNCH(name, splitk_reduce_group_kernel, dim3((unsigned)cdiv((int64_t)rg.j[0].count, 256)), dim3(256), 0, s,
+               rg);
+  return true;
+}
+
 // bf16 products only (the direct-to-LDS kernel); false and nothing launched
 // if a product cannot take that path or its reduction needs unaligned rows.
 // cs (optional): column sums added to the reduction launch.
@@ -254,14 +278,8 @@ static inline bool gemm_f32_group(const char* name, hipStream_t s, int n, const 
     rblocks += (int)cdiv(count, 256);
   }
   if (cs) {
-    const int64_t count = (int64_t)cs->batches * cs->N / 4;
-    ReduceJob& r = rg.j[rg.n++];
-    r.part = cs->part; r.dst = cs->dst; r.dst2 = cs->dst2;
-    r.N4 = (uint32_t)(cs->N / 4); r.per = r.N4; r.count = (uint32_t)count;
-    r.ld = 0; r.dst_zstride = cs->dst_zstride;
-    r.kstride = cs->kstride; r.zin = cs->zin;
-    r.splits = cs->rows; r.start = rblocks;
-    rblocks += (int)cdiv(count, 256);
+    rg.j[rg.n] = colsum_reduce_job(*cs, rblocks);
+    rblocks += (int)cdiv((int64_t)rg.j[rg.n++].count, 256);
   }
   if (!gemm_kc_group_launch<AKC, BKC>(name, s, n, it, e)) return false;
   if (rg.n) BLSTM_LAUNCH("splitk_reduce_group", splitk_reduce_group_kernel, dim3((unsigned)rblocks), dim3(256), 0, s, rg);
