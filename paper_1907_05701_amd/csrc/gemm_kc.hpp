@@ -261,7 +261,7 @@ __device__ __forceinline__ void kc_gemm_tile(const KcArgs& p, const Epi& epi, in
 }
 
 template <int BM, int BN, int WM, int WN, int STAGES, int BK, bool AKC, bool BKC, class Epi>
-__global__ __launch_bounds__(WM * WN * 64) void gemm_kc_kernel(const KcArgs p, const Epi epi) {
+__global__ __launch_bounds__(WM * WN * 64, WM * WN / 2) void gemm_kc_kernel(const KcArgs p, const Epi epi) {
   kc_gemm_tile<BM, BN, WM, WN, STAGES, BK, AKC, BKC, Epi>(p, epi, blockIdx.x);
 }
 
@@ -278,7 +278,7 @@ struct KcGroup {
 };
 
 template <int BM, int BN, int WM, int WN, int STAGES, int BK, bool AKC, bool BKC, class Epi>
-__global__ __launch_bounds__(WM * WN * 64) void gemm_kc_group_kernel(const KcGroup<Epi> g) {
+__global__ __launch_bounds__(WM * WN * 64, WM * WN / 2) void gemm_kc_group_kernel(const KcGroup<Epi> g) {
   int i = 0;
   while (i + 1 < g.n && (int)blockIdx.x >= g.start[i + 1]) ++i;
   kc_gemm_tile<BM, BN, WM, WN, STAGES, BK, AKC, BKC, Epi>(g.p[i], g.e[i], (int)blockIdx.x - g.start[i]);

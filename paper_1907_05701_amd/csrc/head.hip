@@ -206,8 +206,9 @@ __global__ __launch_bounds__(256) void logit_lse_kernel(const float2* __restrict
 // 16-class fragment; for a fragment pair (i, i+1) the groups g and g ^ 1
 // swap halves so that each lane stores 8 consecutive classes (16 bytes):
 // even groups classes 8(g/2) .. +7 of fragment i, odd groups those of i+1.
-// Per element: one subtraction, one fused multiply-add, the exponential and
-// the column-sum add; classes past K carry a bias of -inf and frames past M
+// Per element: one subtraction, one fused multiply-add, the exponential, a
+// multiplication by the loss scale (by one when it is folded into the
+// exponent) and the column-sum add; classes past K carry a bias of -inf and frames past M
 // a log-sum-exp of +inf, so both give exact zeros without a test.  The label
 // (at most one class of a frame) is handled in a branch that a lane takes
 // only for the fragment holding it.
@@ -229,26 +230,49 @@ struct EpiSoftmaxDs {
     const int mw = (int)mw64, nw = (int)nw64;
     const int g = lane >> 4;
     const bool fold = l2s == l2s;
-    float bl[FM][4];   // bias * log2(e), -inf past K
+    const float mul = fold ? 1.0f : scale;   // v * 1 is v
+    // bias * log2(e), -inf past K; every load is issued before the first
+    // use (a load under the k < K test would be waited for one at a time)
+    float bl[FM][4];
+    const float* bp = bias + mw + g * 4;
+    if (mw + FM * 16 <= K) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+      for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int k = mw + i * 16 + g * 4 + r;
-        bl[i][r] = k < K ? bias[k] * LOG2E_F : -INFINITY;
-      }
+        for (int r = 0; r < 4; ++r) bl[i][r] = bp[i * 16 + r];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) bl[i][r] *= LOG2E_F;
+    } else {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) bl[i][r] = bias[min(mw + i * 16 + g * 4 + r, K - 1)];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) bl[i][r] = mw + i * 16 + g * 4 + r < K ? bl[i][r] * LOG2E_F : -INFINITY;
+    }
     float csum[FM][4];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) csum[i][r] = 0.f;
+    float Lj[FN];
+    int labj[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int f = nw + j * 16 + (lane & 15);
+      Lj[j] = f < M ? lse[f] : INFINITY;
+      labj[j] = f < M ? labels[f] : -1;
+    }
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const int f = nw + j * 16 + (lane & 15);
       const bool fok = f < M;
-      const float L = fok ? lse[f] : INFINITY;
-      int lab = fok ? labels[f] : -1;
-      lab = lab < K ? lab : -1;
+      const float L = Lj[j];
+      const int lab = labj[j] < K ? labj[j] : -1;
       const float Lc = fold ? fmaf(L, LOG2E_F, -l2s) : L * LOG2E_F;
       uint2 pk[FM];
 #pragma unroll
@@ -257,7 +281,7 @@ struct EpiSoftmaxDs {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           v[r] = exp2_hw(fmaf(acc[i][j][r], LOG2E_F, bl[i][r] - Lc));
-          if (!fold) v[r] *= scale;
+          v[r] *= mul;
         }
         const int kb = mw + i * 16 + g * 4;
         if ((unsigned)(lab - kb) < 4u) {
