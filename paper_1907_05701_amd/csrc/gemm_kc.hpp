@@ -30,6 +30,7 @@
 #pragma once
 
 #include <atomic>
+#include <cstring>
 
 #include "gemm.hpp"
 #include "dma.hpp"
@@ -268,7 +269,7 @@ __global__ __launch_bounds__(WM * WN * 64, WM * WN / 2) void gemm_kc_kernel(cons
 // Several independent products in one launch (fills the chip when each alone
 // would not): product i owns workgroups [start[i], start[i+1]); every start is
 // a multiple of 8 so that the XCD-aware tile order of each product holds.
-#define KC_MAX_GROUP 8
+#define KC_MAX_GROUP 12
 template <class Epi>
 struct KcGroup {
   KcArgs p[KC_MAX_GROUP];
@@ -279,8 +280,11 @@ struct KcGroup {
 
 template <int BM, int BN, int WM, int WN, int STAGES, int BK, bool AKC, bool BKC, class Epi>
 __global__ __launch_bounds__(WM * WN * 64, WM * WN / 2) void gemm_kc_group_kernel(const KcGroup<Epi> g) {
+  // the product index: every start compared at once (the loads are
+  // independent, so they issue together)
   int i = 0;
-  while (i + 1 < g.n && (int)blockIdx.x >= g.start[i + 1]) ++i;
+#pragma unroll
+  for (int k = 1; k < KC_MAX_GROUP; ++k) i += (k < g.n && (int)blockIdx.x >= g.start[k]);
   kc_gemm_tile<BM, BN, WM, WN, STAGES, BK, AKC, BKC, Epi>(g.p[i], g.e[i], (int)blockIdx.x - g.start[i]);
 }
 
@@ -402,6 +406,7 @@ static inline bool gemm_kc_group_launch(const char* name, hipStream_t s, int n, 
   typedef KcTile C;
   if (n < 1 || n > KC_MAX_GROUP) return false;
   KcGroup<Epi> g;
+  std::memset((void*)&g, 0, sizeof g);
   g.n = n;
   int start = 0;
   for (int i = 0; i < n; ++i) {

@@ -705,8 +705,9 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
     }
     if (l > 0) dY = dst_dx;
   }
-  // the deferred weight gradients, KC_MAX_GROUP products per launch (top
-  // layers first, so the smaller layer-0 dW_ih rides in the last one)
+  // the deferred weight gradients, KC_MAX_GROUP products per launch (all of
+  // them for up to six layers: one launch, so that only its last round of
+  // the chip is a partial one)
   for (int i0 = 0; i0 < nd; i0 += KC_MAX_GROUP) {
     const int n = std::min(KC_MAX_GROUP, nd - i0);
     if (!gemm_f32_group<true, false>("gemm_dw_group", s, n, deferred + i0)) {

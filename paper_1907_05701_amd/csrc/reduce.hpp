@@ -2,6 +2,8 @@
 // (bias gradients) and the float32-output GEMM wrapper with optional split-K.
 #pragma once
 
+#include <cstring>
+
 #include "common.hpp"
 #include "gemm_kc.hpp"
 
@@ -188,7 +190,8 @@ struct ReduceGroup {
 
 static __global__ __launch_bounds__(256) void splitk_reduce_group_kernel(const ReduceGroup g) {
   int i = 0;
-  while (i + 1 < g.n && (int)blockIdx.x >= g.j[i + 1].start) ++i;
+#pragma unroll
+  for (int k = 1; k < KC_MAX_GROUP; ++k) i += (k < g.n && (int)blockIdx.x >= g.j[k].start);
   const ReduceJob& r = g.j[i];
   const uint32_t e = ((uint32_t)blockIdx.x - (uint32_t)r.start) * 256u + threadIdx.x;
   if (e >= r.count) return;
@@ -238,6 +241,7 @@ static inline ReduceJob colsum_reduce_job(const ColSumJob& cs, int start) {
 static inline bool colsum_job_launch(const char* name, hipStream_t s, const ColSumJob& cs) {
   if (!colsum_job_ok(cs)) return false;
   ReduceGroup rg;
+  std::memset((void*)&rg, 0, sizeof rg);
   rg.n = 1;
   rg.j[0] = colsum_reduce_job(cs, 0);
   BLSTM_LAUNCH(name, splitk_reduce_group_kernel, dim3((unsigned)cdiv((int64_t)rg.j[0].count, 256)), dim3(256), 0, s,
@@ -255,6 +259,7 @@ static inline bool gemm_f32_group(const char* name, hipStream_t s, int n, const 
   KcItem it[KC_MAX_GROUP];
   EpiStore<float> e[KC_MAX_GROUP];
   ReduceGroup rg;
+  std::memset((void*)&rg, 0, sizeof rg);
   rg.n = 0;
   int rblocks = 0;
   for (int i = 0; i < n; ++i) {
