@@ -29,10 +29,12 @@ PEAK_FP32_TFLOPS = 157.3      # MI355X dense fp32 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 
-def kernel_work(name, c, n_params):
+def kernel_work(name, c, n_params, fused_gx=False):
     """Algorithmic work of all launches of kernel `name` in one step:
     (bound, amount, unit, launches).  FLOPs count 2 per multiply-add of the
-    products the step needs; bytes count each tensor read or written once."""
+    products the step needs; bytes count each tensor read or written once.
+    fused_gx: the persistent forward computes the input projection itself
+    (no gemm_gx launch), so its work includes that product."""
     L, D, H, P, K, T, B = (c[k] for k in "LDHPKTB")
     M = T * B
     es = 2 if c["precision"] == "bf16" else 4
@@ -42,15 +44,18 @@ def kernel_work(name, c, n_params):
     if name in ("lstm_rec_fwd", "lstm_rec_bwd", "lstm_rec_fwd_persist", "lstm_rec_bwd_persist"):
         # the recurrent products h_prev W_hh^T (forward) or da W_hh (BPTT);
         # the first step of each direction has no previous state
-        return "mfma", L * (T - 1) * 2 * 2 * B * 4 * H * H, "flop", None
+        rec = L * (T - 1) * 2 * 2 * B * 4 * H * H
+        if fused_gx and name == "lstm_rec_fwd_persist":
+            rec += sum(2 * 2 * M * 4 * H * d for d in Dl)
+        return "mfma", rec, "flop", None
     if name == "gemm_bwd_group":
         # per layer above layer 0, right after its BPTT: dX (the weight
         # gradients of every layer follow the last BPTT, in gemm_dw_group)
         return "mfma", (L - 1) * 2 * M * 2 * H * 8 * H, "flop", L - 1
     if name == "gemm_dw_group":
-        # dW_ih and dW_hh of every layer, up to 8 products per launch
+        # dW_ih and dW_hh of every layer, up to 12 products per launch
         return "mfma", (sum(2 * 2 * 4 * H * d * M for d in Dl) + L * 2 * 2 * 4 * H * H * (T - 1) * B), "flop", \
-            -(-2 * L // 8)
+            -(-2 * L // 12)
     if name == "gemm_dwih":
         return "mfma", sum(2 * 2 * 4 * H * d * M for d in Dl), "flop", L
     if name == "gemm_dwhh":
@@ -183,6 +188,7 @@ def class_rates(st, cfg, lr, steps):
     per = bd.blstm_timing_end(cap=128)
     torch.cuda.synchronize()
     ms = {k: v[1] / steps for k, v in per.items()}
+    fused = "gemm_gx" not in ms and "lstm_rec_fwd_persist" in ms
     mfma = {}
     for cls, names in CLASSES.items():
         t = sum(ms.get(k, 0.0) for k in names)
@@ -190,7 +196,7 @@ def class_rates(st, cfg, lr, steps):
         for k in names:
             if k not in ms:
                 continue
-            w = kernel_work(k, cfg, st.n)
+            w = kernel_work(k, cfg, st.n, fused_gx=fused)
             if w is not None and not (k == "gemm_logits_ds"):   # the logits count once (recomputed for ds)
                 flop += w[1]
         if t > 0:
@@ -202,6 +208,8 @@ def class_rates(st, cfg, lr, steps):
     for key, cls in (("fwd", "recurrence_fwd"), ("bwd", "recurrence_bwd")):
         if cls in mfma:
             rec[key] = round(mfma[cls]["ms_per_step"] * 1e3 / (L * T), 3)
+    # the forward launches' time includes the input projection when fused
+    rec["fwd_includes_input_projection"] = fused
     return {"mfma": mfma, "recurrence_step_us": rec,
             "kernel_ms": {k: round(v, 4) for k, v in sorted(ms.items(), key=lambda kv: -kv[1])}}
 
@@ -413,7 +421,8 @@ def main():
         for name, (cnt, ms) in ranked:
             print(f"  {name:22s} {cnt:5d} launches {ms * 1e3:10.1f} us {100 * ms / tot:5.1f}%",
                   file=sys.stderr)
-    dominant = next(n for n, _ in ranked if kernel_work(n, cfg, st.n) is not None)
+    fused_gx = "gemm_gx" not in per and "lstm_rec_fwd_persist" in per
+    dominant = next(n for n, _ in ranked if kernel_work(n, cfg, st.n, fused_gx) is not None)
 
     # timed region: K steps, the dominant kernel bracketed by HIP events on
     # the stream it runs on.  In graph mode the K steps (with their event
@@ -455,7 +464,7 @@ def main():
 
     ms_per_step = elapsed * 1e3 / args.steps
     value = frames * args.steps / elapsed
-    bound, amount, unit, _ = kernel_work(dominant, cfg, st.n)
+    bound, amount, unit, _ = kernel_work(dominant, cfg, st.n, fused_gx)
     n_launch, total_ms = dom
     per_launch = amount * args.steps / n_launch
     avg_s = total_ms / n_launch / 1e3

@@ -404,6 +404,13 @@ static PersistArgs persist_args(const Layout& lo, const bf16* W, char* ws, int l
   return pa;
 }
 
+// Whether the persistent forward computes the input projection itself
+// (ADPSGD_BLSTM_FUSE_GX=0: a separate product launch, for comparisons).
+static bool fuse_gx() {
+  const char* e = getenv("ADPSGD_BLSTM_FUSE_GX");
+  return !(e && e[0] == '0');
+}
+
 template <typename T>
 static int fwd_impl(const Layout& lo, const float* theta, const T* W, const float* x, char* ws,
                     T* ytop, hipStream_t s) {
@@ -439,17 +446,33 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
     Opnd Bw = opnd(W + lo.Wih[l][0], Dl, Dl, 4 * H, lo.Wih[l][1] - lo.Wih[l][0]);
     const auto epi = epi_store<T>(GX, 8 * H, M, 4 * H, 4 * H, 0, theta + lo.bih[l][0],
                                   theta + lo.bhh[l][0], lo.bih[l][1] - lo.bih[l][0]);
-    if (l == 0 && WP0) {
-      // bf16 with D not a multiple of 8: W_ih padded to the input's pitch
-      Bw = opnd(WP0, Dpl, Dpl, 4 * H, (int64_t)4 * H * Dpl);
-      gemm_launch<T, true, true, V, V>("gemm_gx", s, A, Bw, M, 4 * H, Dpl, 2, 1, epi);
-    } else if (Dl % V == 0)
-      gemm_launch<T, true, true, V, V>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
-    else
-      gemm_launch<T, true, true, V, 4>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
+    // bf16 persistent path: the forward launch computes G_x itself (each
+    // workgroup its own rows and gate columns), with the same operands
+    const bf16* wih = (l == 0 && WP0) ? WP0 : (const bf16*)(W + lo.Wih[l][0]);
+    const int64_t ldw = (l == 0 && WP0) ? Dpl : Dl;
+    const int64_t wih_d = (l == 0 && WP0) ? (int64_t)4 * H * Dpl : lo.Wih[l][1] - lo.Wih[l][0];
+    const int kin = (l == 0 && WP0) ? Dpl : Dl;
+    const bool fuse = persist && std::is_same<T, bf16>::value && fuse_gx() && kin % 8 == 0 && Dpl % 8 == 0 &&
+                      ldw % 8 == 0 && wih_d % 8 == 0 && ((uintptr_t)Xl & 15) == 0 && ((uintptr_t)wih & 15) == 0;
+    auto launch_gx = [&]() {
+      if (l == 0 && WP0) {
+        // bf16 with D not a multiple of 8: W_ih padded to the input's pitch
+        Bw = opnd(WP0, Dpl, Dpl, 4 * H, (int64_t)4 * H * Dpl);
+        gemm_launch<T, true, true, V, V>("gemm_gx", s, A, Bw, M, 4 * H, Dpl, 2, 1, epi);
+      } else if (Dl % V == 0)
+        gemm_launch<T, true, true, V, V>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
+      else
+        gemm_launch<T, true, true, V, 4>("gemm_gx", s, A, Bw, M, 4 * H, Dl, 2, 1, epi);
+    };
+    if (!fuse) launch_gx();
     if (persist) {
       PersistArgs pa = persist_args(lo, (const bf16*)W, ws, l);
-      pa.Y = (bf16*)Yl; pa.Gx = (const bf16*)GX; pa.C = Cl; pa.G = (bf16*)Gl;
+      pa.Y = (bf16*)Yl; pa.Gx = (bf16*)GX; pa.C = Cl; pa.G = (bf16*)Gl;
+      if (fuse) {
+        pa.Xin = (const bf16*)Xl; pa.ldx = Dpl; pa.Kin = kin;
+        pa.Wih = wih; pa.ldw = ldw; pa.wih_d = wih_d;
+        pa.bih = theta + lo.bih[l][0]; pa.bhh = theta + lo.bhh[l][0]; pa.b_d = lo.bih[l][1] - lo.bih[l][0];
+      }
       if (!xch_cleared) {
         xch_cleared = persist_clear(false, pa, s) == hipSuccess;
         status_cleared = status_cleared || xch_cleared;
@@ -461,6 +484,7 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
       }
       if (xch_cleared && persist_layer(false, pa, s) == hipSuccess) continue;
       (void)hipGetLastError();   // cooperative launch refused: take the per-step path
+      if (fuse) launch_gx();
     }
     RecFwdArgs<T> ra;
     ra.Y = Yl; ra.Whh0 = W + lo.Whh[l][0]; ra.Whh1 = W + lo.Whh[l][1]; ra.Gx = GX; ra.C = Cl;

@@ -46,6 +46,7 @@
 #include "common.hpp"
 #include "lstm_persist.hpp"
 #include "dma.hpp"
+#include "gemm_kc.hpp"
 
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
@@ -155,6 +156,150 @@ __device__ __forceinline__ float upper_from_lower(float x, float y) {
 }
 
 // ---------------------------------------------------------------------------
+// Input projection inside the forward launch (when the caller passes the
+// layer input): before its steps, each workgroup computes
+//   G_x[t][row][d 4H + q H + u0 + ul] = x[t][row] . W_ih[d][q H + u0 + ul] + b_ih + b_hh
+// for its own RV rows at every step and its member's 256 gate columns
+// (q < 4, ul < 64), the entries its own steps read.  The work is split
+// evenly over the whole chip, with no launch of its own.  The sum runs as
+// in the separate product: 64-deep k-tiles in ascending order, each on two
+// v_mfma_f32_16x16x32_bf16 steps, the biases added to the float32 sum
+// before the rounding to bf16; so the values are bit for bit the same.
+// Rows (step, slice row) in passes of GXR; both operands staged by
+// direct-to-LDS loads in the K-contiguous tile layout of gemm_kc.hpp (in
+// the LDS that the W_hh staging and the steps use afterwards); wave w owns
+// gate columns 32w .. 32w+31.
+// ---------------------------------------------------------------------------
+#define GXR 176   // rows per pass (11 MFMA row tiles)
+// LDS of the projection: two stages of 64-deep k-tiles (x and W_ih rows of
+// 128 bytes) and one scratch KB (the destination of load instructions that
+// have no rows, so every wave issues as many loads per k-tile as every other
+// and one vmcnt bound serves them all).  Measured on MI355X: 32-deep tiles
+// in 3-5 stages, and a third W_ih stage, were slower.
+#define GX_BK 64
+#define GX_ST 2
+static constexpr size_t gx_lds_bytes = (size_t)GX_ST * (GXR + 4 * PU) * 2 * GX_BK + 1024;
+template <int RV>
+__device__ __forceinline__ void gx_prologue(const PersistArgs& a, char* lds, int d, int u0, int rowbase, int rend) {
+  constexpr int BK = GX_BK, ST = GX_ST, ROWB = 2 * BK, FM = GXR / 16, FN = 2;
+  constexpr int CPR = ROWB / 16, RPI = 64 / CPR;      // 16-byte chunks per tile row, rows per load instruction
+  constexpr int NA = GXR / RPI, NB = 4 * PU / RPI;    // load instructions per k-tile
+  constexpr int QA = (NA + 7) / 8, QB = NB / 8;       // per wave
+  constexpr int TA = GXR * ROWB, STG = (GXR + 4 * PU) * ROWB;
+  static_assert(NB % 8 == 0 && GXR % RPI == 0, "tile rows split over the waves");
+  static_assert(BK == 32 || BK == 64, "k-tile depth");
+  const int H = a.H, B = a.B, K = a.Kin;
+  const int rows = a.Tn * RV;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int fr = lane & 15, fc = lane >> 4;
+  const int lr = lane / CPR, ls = lane % CPR;   // load lanes: row within the instruction, 16-byte slot
+  char* scratch = lds + ST * STG;
+  const __amdgpu_buffer_rsrc_t rx = dma_rsrc(a.Xin);
+  const __amdgpu_buffer_rsrc_t rw = dma_rsrc(a.Wih + (d ? a.wih_d : 0));
+  const int ntiles = (K + BK - 1) / BK;
+  // W_ih rows of this lane's loads (instruction q 8 + w fills tile rows
+  // RPI ins .. RPI ins + RPI - 1; tile row br is gate br / 64 of unit
+  // u0 + br % 64)
+  int64_t wrow[QB];
+#pragma unroll
+  for (int q = 0; q < QB; ++q) {
+    const int br = (q * 8 + w) * RPI + lr;
+    wrow[q] = ((int64_t)(br >> 6) * H + u0 + (br & 63)) * a.ldw;
+  }
+  float bv[FN];
+#pragma unroll
+  for (int jn = 0; jn < FN; ++jn) {
+    const int n = 32 * w + jn * 16 + fr;
+    const int64_t gi = (d ? a.b_d : 0) + (int64_t)(n >> 6) * H + u0 + (n & 63);
+    float v = 0.f;
+    v += a.bih[gi];
+    v += a.bhh[gi];
+    bv[jn] = v;
+  }
+  for (int m0 = 0; m0 < rows; m0 += GXR) {
+    // frame rows of this lane's A loads
+    int64_t xrow[QA];
+    bool xok[QA];
+#pragma unroll
+    for (int q = 0; q < QA; ++q) {
+      const int ins = q * 8 + w;
+      const int m = m0 + ins * RPI + lr;
+      const int r = m % RV;
+      xok[q] = ins < NA && m < rows && rowbase + r < rend;
+      xrow[q] = xok[q] ? ((int64_t)(m / RV) * B + rowbase + r) * a.ldx : 0;
+    }
+    auto issue = [&](int j) {
+      char* st = lds + (j % ST) * STG;
+      const int64_t k0 = (int64_t)j * BK;
+#pragma unroll
+      for (int q = 0; q < QA; ++q) {
+        const int ins = q * 8 + w;
+        const int64_t k = k0 + kc_slot<BK>(ls, ins * RPI + lr) * 8;
+        dma16(rx, xok[q] && k < K ? (uint32_t)((xrow[q] + k) * 2) : DMA_OFF_NONE,
+              ins < NA ? st + ins * 1024 : scratch);
+      }
+#pragma unroll
+      for (int q = 0; q < QB; ++q) {
+        const int ins = q * 8 + w;
+        const int64_t k = k0 + kc_slot<BK>(ls, ins * RPI + lr) * 8;
+        dma16(rw, k < K ? (uint32_t)((wrow[q] + k) * 2) : DMA_OFF_NONE, st + TA + ins * 1024);
+      }
+    };
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int jn = 0; jn < FN; ++jn) acc[i][jn] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < ST - 1; ++j)
+      if (j < ntiles) issue(j);
+    for (int j = 0; j < ntiles; ++j) {
+      if (j + ST - 2 < ntiles)
+        kc_wait_vm<(ST - 2) * (QA + QB)>();
+      else
+        kc_wait_vm<0>();
+      __syncthreads();   // tile j in LDS; every wave is done with tile j - 1
+      if (j + ST - 1 < ntiles) issue(j + ST - 1);
+      const char* st = lds + (j % ST) * STG;
+#pragma unroll
+      for (int ks = 0; ks < BK / 32; ++ks) {
+        bf16x8 bf[FN];
+#pragma unroll
+        for (int jn = 0; jn < FN; ++jn) {
+          const int br = 32 * w + jn * 16 + fr;
+          bf[jn] = *(const bf16x8*)(st + TA + br * ROWB + kc_slot<BK>(ks * 4 + fc, fr) * 16);
+        }
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          const bf16x8 af = *(const bf16x8*)(st + (i * 16 + fr) * ROWB + kc_slot<BK>(ks * 4 + fc, fr) * 16);
+#pragma unroll
+          for (int jn = 0; jn < FN; ++jn) acc[i][jn] = Mfma<bf16>::mma(af, bf[jn], acc[i][jn]);
+        }
+      }
+    }
+    __syncthreads();   // the stages are free for the next pass
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int m = m0 + i * 16 + fc * 4 + rr;
+        const int r = m % RV;
+        if (m < rows && rowbase + r < rend) {
+          bf16* o = a.Gx + ((int64_t)(m / RV) * B + rowbase + r) * 8 * H + (int64_t)d * 4 * H + u0;
+#pragma unroll
+          for (int jn = 0; jn < FN; ++jn) {
+            const int n = 32 * w + jn * 16 + fr;
+            o[(n >> 6) * H + (n & 63)] = (bf16)(acc[i][jn][rr] + bv[jn]);
+          }
+        }
+      }
+  }
+  // the projection stored (the steps read it back through the same CU's
+  // cache) and the LDS free for the W_hh staging
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
 // Forward.
 //
 // RV rows of the batch per workgroup (8 or 16) on 16-row MFMA tiles.  With
@@ -178,6 +323,8 @@ __global__ __launch_bounds__(NTH) void lstm_fwd_persist(const PersistArgs a) {
   const int ub = w & 3, kh = w >> 2;
   const int KH = H / 64;   // 32-deep k-steps per k half
   const bool owner = kh == 0;
+
+  if (a.Xin) gx_prologue<RV>(a, lds_raw, d, u0, a.b0 + s * RV, a.b0 + a.rows);
 
   // W_hh fragments (B operand): gate q of unit u0 + ub*16 + lane%16, k-step
   // kh*KH + i, k = 8*(lane/16) .. +8 within it.  Staged by direct-to-LDS
@@ -741,7 +888,7 @@ __global__ void status_reset_kernel(int* status) {
 size_t persist_lds_bytes(int H, bool backward, int RV) {
   const size_t run = backward ? (size_t)32 * 17 * 16 + (size_t)(NTH / (16 * RV)) * RV * PU * 4
                               : (size_t)(H / 8) * 17 * 16 + (size_t)4 * 4 * 64 * 16 + (size_t)2 * RV * PU * (4 + 2 + 8);
-  return std::max(run, (size_t)STAGE_BYTES);
+  return std::max(std::max(run, (size_t)STAGE_BYTES), backward ? (size_t)0 : gx_lds_bytes);
 }
 
 // Compute units: one persistent workgroup fits per CU (its 8 waves hold

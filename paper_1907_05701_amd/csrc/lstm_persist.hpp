@@ -8,7 +8,19 @@ struct PersistArgs {
   const bf16* W;      // bf16 parameter copy (flat layout)
   int64_t whh0, whh1; // element offsets of W_hh for the two directions
   const bf16* WT;     // unused by the persistent kernels (W_hh^T of the layer, [2][H][4H])
-  const bf16* Gx;     // forward: input projection [M][8H]
+  bf16* Gx;           // forward: input projection incl. both biases [M][8H] (written by the
+                      // kernel itself when Xin is set, else read only)
+  // forward, optional: the layer input and W_ih, so that each workgroup
+  // computes the input projection of its own rows and gate columns before
+  // the steps (instead of a separate product launch); null Xin: Gx is given
+  const bf16* Xin;    // layer input [M][ldx] (bf16, 16-byte aligned rows)
+  int64_t ldx;
+  const bf16* Wih;    // W_ih of direction 0 [4H][ldw]; direction 1 at Wih + wih_d
+  int64_t ldw, wih_d;
+  const float* bih;   // b_ih and b_hh of direction 0 [4H]; direction 1 at + b_d
+  const float* bhh;
+  int64_t b_d;
+  int Kin;            // input width (a multiple of 8; zero k past the operands' ends)
   float* C;           // cell states [M][2H] (forward writes, backward reads)
   bf16* G;            // gate pre-activations [M][2][H][4] (direction, unit, gate i/f/g/o; forward writes, backward reads)
   bf16* DA;           // backward: gate pre-activation gradients [M][8H]

@@ -712,3 +712,33 @@ def test_graph_replays_at_benchmark_shape(gpu_lib):
         say(f"[graph bench shape] replay {i} matches, loss {float(eager.loss.cpu()[0]):.6f}")
     replayed.check_recurrence()
     eager.check_recurrence()
+
+
+@pytest.mark.parametrize("shape", [
+    dict(L=6, D=260, H=512, P=256, K=32000, T=21, B=128),   # the benchmark's step
+    dict(L=2, D=260, H=256, P=64, K=3000, T=25, B=44),      # two row passes, a 4-row last slice
+    dict(L=2, D=64, H=512, P=64, K=500, T=11, B=200),       # 16-row slices, unpadded layer-0 W_ih
+], ids=["b128", "ragged", "rows16"])
+def test_fused_input_projection_matches_the_separate_product(gpu_lib, monkeypatch, shape):
+    """The persistent forward computing each workgroup's slice of the input
+    projection itself gives the same step, bit for bit, as the separate
+    product launch (same k order and rounding)."""
+    from paper_1907_05701_amd.step import LearnerStep
+    dims = ref.Dims(**shape)
+    n = ref.param_count(dims)
+    theta = inputs.params(n, seed=5)
+    x = inputs.features(dims.T, dims.B, dims.D, seed=6)
+    lab = inputs.labels(dims.T, dims.B, dims.K, seed=7, dist="zipf")
+    out = {}
+    for fuse in ("1", "0"):
+        monkeypatch.setenv("ADPSGD_BLSTM_FUSE_GX", fuse)
+        st = LearnerStep(**shape, precision="bf16")
+        st.load(theta, x, lab, theta)
+        st.gradient()
+        torch.cuda.synchronize()
+        st.check_recurrence()
+        out[fuse] = {k: getattr(st, k).float().cpu().numpy() for k in ("y_top", "loss", "grad")}
+        del st
+    for k in ("y_top", "loss", "grad"):
+        np.testing.assert_array_equal(out["1"][k], out["0"][k], err_msg=k)
+    say(f"[fused gx] {shape} bit-identical, loss {float(out['1']['loss'][0]):.6f}")
