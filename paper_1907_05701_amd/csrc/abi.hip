@@ -117,7 +117,7 @@ int make_layout(const blstm_dims* d, Layout* lo) {
   // per-step 16-row partials (per-step BPTT) or per-workgroup partials over
   // all steps (persistent BPTT, 8-row workgroups)
   L.dbp_bytes = align256((size_t)std::max<int64_t>((int64_t)d->T * cdiv(d->B, 16), cdiv(d->B, 8)) * 8 * H * 4);
-  L.DBP = a; a += 2 * L.dbp_bytes;
+  L.DBP = a; a += (size_t)std::max(2, d->L) * L.dbp_bytes;   // per layer when the bias sums wait for the last BPTT
   L.CSP = a; a = align256(a + (size_t)COLSUM_MAX_CHUNKS * 8 * H * 4);
   // split-K plans and partial buffers of the backward GEMMs
   const int BMt = es == 2 ? GemmCfg<bf16>::BM : GemmCfg<float>::BM;

@@ -404,6 +404,13 @@ static PersistArgs persist_args(const Layout& lo, const bf16* W, char* ws, int l
   return pa;
 }
 
+// Whether the persistent BPTT adds the split-K partial sums of dX itself
+// (ADPSGD_BLSTM_FUSE_DY=0: a separate reduction launch, for comparisons).
+static bool fuse_dy() {
+  const char* e = getenv("ADPSGD_BLSTM_FUSE_DY");
+  return !(e && e[0] == '0');
+}
+
 // Whether the persistent forward computes the input projection itself
 // (ADPSGD_BLSTM_FUSE_GX=0: a separate product launch, for comparisons).
 static bool fuse_gx() {
@@ -593,11 +600,21 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
   const bool defer = lp && lo.write_dat && !side;
   F32Job deferred[2 * MAX_LAYERS];
   int nd = 0;
+  // with the persistent BPTT, a layer's dX stays as its split-K partial
+  // sums, which the next BPTT adds itself (in the reduction's order) before
+  // its steps; the bias sums of every layer then wait for one reduction
+  // launch after the last BPTT (on per-layer bias partials)
+  const bool dy_parts = defer && fuse_dy() && use_persistent<T>(H, lo.T, true, s) &&
+                        persist_bwd_dy_partials_ok(H, B, lo.T);
+  ReduceGroup pending_dy;   // the held dX reduction the next BPTT takes over
+  pending_dy.n = 0;
+  ColSumJob bias_jobs[MAX_LAYERS];
+  int nbias = 0;
   const float* dY = dytop;
   for (int l = lo.L - 1; l >= 0; --l) {
     const int par = side ? (l & 1) : 0;
     T* DATl = (T*)(ws + lo.DAT + (defer ? l : par) * lo.dat_bytes);
-    float* DBPl = (float*)(ws + lo.DBP + par * lo.dbp_bytes);
+    float* DBPl = (float*)(ws + lo.DBP + (dy_parts ? l : par) * lo.dbp_bytes);
     if (side && l + 2 < lo.L) (void)hipStreamWaitEvent(s, side->dw_done[l + 2], 0);
     const T* Xl = l == 0 ? (const T*)(ws + lo.X0) : (const T*)(ws + lo.Y[l - 1]);
     const int Dl = lo.layer_in(l), Dpl = lo.layer_in_pitch(l);
@@ -614,11 +631,20 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       pa.DAT = lo.write_dat ? (bf16*)DATl : nullptr;
       pa.DBP = DBPl;
       pa.M = M;
+      if (pending_dy.n == 1) {
+        pa.DYP = pending_dy.j[0].part;
+        pa.ndy = pending_dy.j[0].splits;
+        pa.dy_kstride = pending_dy.j[0].kstride;
+      }
       if (!xch_cleared) xch_cleared = persist_clear(true, pa, s) == hipSuccess;
       done = xch_cleared && persist_layer(true, pa, s) == hipSuccess;
       if (!done) (void)hipGetLastError();
+      else pending_dy.n = 0;   // the BPTT summed the partials
       step_fused = done;
     }
+    // partials nobody summed (the persistent launch did not run): reduce them now
+    reduce_group_launch(s, pending_dy);
+    pending_dy.n = 0;
     if (!done) {
       if (!have_wt) make_copies();
       RecBwdArgs<T> rb;
@@ -682,7 +708,22 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
         const ColSumJob cs{DBPl, dbp_rows, 2, 4 * H, 8 * H, 4 * H,
                            grad + lo.bih[l][0], grad + lo.bhh[l][0], lo.bih[l][1] - lo.bih[l][0]};
         const bool with_db = step_fused && colsum_job_ok(cs);
-        if (ng == 0) {
+        if (dy_parts && with_db) {
+          // the bias sums wait for the last BPTT; dX (if any) keeps its
+          // partials for the next BPTT when it is split
+          bias_jobs[nbias++] = cs;
+          db_done = true;
+          ReduceGroup held;
+          if (ng == 0 || gemm_f32_group<true, false>("gemm_bwd_group", ss, ng, g, nullptr, &held)) {
+            if (ng > 0 && held.n == 1) pending_dy = held;
+            else if (ng > 0) reduce_group_launch(ss, held);
+          } else {
+            for (int i = 0; i < ng; ++i)
+              gemm_f32<T, true, false, V, V>(i == ng - 1 && dx_here ? "gemm_dx" : (i == 0 ? "gemm_dwih" : "gemm_dwhh"),
+                                             ss, g[i].A, g[i].B, g[i].M, g[i].N, g[i].K, g[i].batches, g[i].splits,
+                                             g[i].dst, g[i].ld, g[i].dst_zstride, g[i].part);
+          }
+        } else if (ng == 0) {
           // (layer 0, weight gradients deferred: the bias sums alone, by the
           // same reduction)
           db_done = with_db && colsum_job_launch("splitk_reduce_group", ss, cs);
@@ -728,6 +769,22 @@ static int bwd_impl(const Layout& lo, const T* W, char* ws, const T* ytop, const
       gemm_f32<T, true, false, V, V>("gemm_dx", s, A, Bw, M, Dl, 8 * H, 1, lo.sp_dX[l], dst_dx, Dl, 0, part_dx);
     }
     if (l > 0) dY = dst_dx;
+  }
+  // the held bias sums of every layer, one reduction launch
+  if (nbias > 0) {
+    ReduceGroup rg;
+    std::memset((void*)&rg, 0, sizeof rg);
+    int blocks = 0;
+    for (int i = 0; i < nbias; ++i) {
+      if (rg.n == KC_MAX_GROUP) {
+        reduce_group_launch(s, rg);
+        std::memset((void*)&rg, 0, sizeof rg);
+        blocks = 0;
+      }
+      rg.j[rg.n] = colsum_reduce_job(bias_jobs[i], blocks);
+      blocks += (int)cdiv((int64_t)rg.j[rg.n++].count, 256);
+    }
+    reduce_group_launch(s, rg);
   }
   // the deferred weight gradients, KC_MAX_GROUP products per launch (all of
   // them for up to six layers: one launch, so that only its last round of

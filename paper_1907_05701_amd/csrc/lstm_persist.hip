@@ -55,6 +55,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 #define KH_MAX 8              // forward: 32-deep k-steps per k half at H = 512
 #define SPIN_LIMIT (1u << 18)
 #define STAGE_BYTES (128 * 1024)   // W_hh staging buffer (half of a member's slice)
+#define BWD_DY_LDS (16 * 1024)     // backward: LDS offset of the summed dy (past the step buffers)
 
 __device__ __forceinline__ uint64_t ll_load(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -581,6 +582,7 @@ __global__ __launch_bounds__(NTH) void lstm_bwd_persist(const PersistArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int NB = H / 16;                // unit blocks of the partial product
 
+
   // W_hh of the 256 own gate rows as the B operand: k = own row kk (gate
   // (kk>>4)&3, unit u0 + (kk>>6)*16 + (kk&15)), n = unit.  Wave w holds the
   // unit blocks nb = w + 8j (j < 4) for all 8 k-steps.  Staged from W_hh as
@@ -630,9 +632,12 @@ __global__ __launch_bounds__(NTH) void lstm_bwd_persist(const PersistArgs a) {
 
   // LDS during the steps: own da as the A operand [32 k groups][R + 1][8]
   // (k = own row; rows RV..15 stay zero), gathered dh_rec [TPI][RV][64]
-  // (member parts)
+  // (member parts), and with dy given as partial sums, the summed dy of
+  // every step [T][RV][64] from BWD_DY_LDS
   bf16* al = (bf16*)lds_raw;
   float* dhl = (float*)(al + (size_t)32 * (R + 1) * 8);
+  float* dyl = (float*)(lds_raw + BWD_DY_LDS);
+  static_assert((size_t)32 * (R + 1) * 8 * 2 + (size_t)TPI * RV * PU * 4 <= BWD_DY_LDS, "step buffers below dy");
   if constexpr (RV < R) {
     for (int i = tid; i < 32 * (R - RV); i += NTH)
       *(uint4*)&al[((i / (R - RV)) * (R + 1) + RV + i % (R - RV)) * 8] = make_uint4(0u, 0u, 0u, 0u);
@@ -672,6 +677,45 @@ __global__ __launch_bounds__(NTH) void lstm_bwd_persist(const PersistArgs a) {
     og[i] = (uint32_t)(row * 8 * H + d * 4 * H + (u0 + cu) * 4);
   }
   const int64_t fc = (int64_t)B * 2 * H, fg = (int64_t)B * 8 * H;   // elements per frame
+  if (a.ndy > 0) {
+    // dy of the slice at every step, [T][RV][64] in LDS: the partial sums
+    // added in split order, four units per 16-byte load (item = step, row,
+    // unit quad); DYI items per thread at a time with all their loads (up
+    // to three partials each) issued together
+    constexpr int DYI = 3;
+    const int nitems = Tn * RV * (PU / 4);
+    for (int i0 = 0; i0 < nitems; i0 += DYI * NTH) {
+      float4 v[DYI][3];
+#pragma unroll
+      for (int j = 0; j < DYI; ++j) {
+        const int it = min(i0 + j * NTH + tid, nitems - 1);
+        const int rs = it >> 4, t_ = rs / RV, r = rs % RV;
+        const int row = rowbase + r < rend ? rowbase + r : a.b0;
+        const float* p = a.DYP + (int64_t)t_ * fc + (int64_t)row * 2 * H + d * H + u0 + (it & 15) * 4;
+#pragma unroll
+        for (int k = 0; k < 3; ++k) v[j][k] = *(const float4*)(p + (int64_t)min(k, a.ndy - 1) * a.dy_kstride);
+      }
+#pragma unroll
+      for (int j = 0; j < DYI; ++j) {
+        const int it = i0 + j * NTH + tid;
+        if (it >= nitems) break;
+        const int rs = it >> 4, t_ = rs / RV, r = rs % RV;
+        float4 sum = v[j][0];
+#pragma unroll
+        for (int k = 1; k < 3; ++k)
+          if (k < a.ndy) { sum.x += v[j][k].x; sum.y += v[j][k].y; sum.z += v[j][k].z; sum.w += v[j][k].w; }
+        for (int k = 3; k < a.ndy; ++k) {
+          const int row = rowbase + r < rend ? rowbase + r : a.b0;
+          const float4 w4 = *(const float4*)(a.DYP + (int64_t)k * a.dy_kstride + (int64_t)t_ * fc +
+                                             (int64_t)row * 2 * H + d * H + u0 + (it & 15) * 4);
+          sum.x += w4.x; sum.y += w4.y; sum.z += w4.z; sum.w += w4.w;
+        }
+        if (!(rowbase + r < rend)) sum = make_float4(0.f, 0.f, 0.f, 0.f);
+        *(float4*)&dyl[(t_ * RV + r) * PU + (it & 15) * 4] = sum;
+      }
+    }
+    __syncthreads();
+  }
   // DA pieces of this thread (waves 4-7; 8 own gate rows of one row per 16-byte piece)
   constexpr int NDA = 32 * RV / (NTH / 2);
   uint32_t oda[NDA];
@@ -689,7 +733,7 @@ __global__ __launch_bounds__(NTH) void lstm_bwd_persist(const PersistArgs a) {
     const bf16* gt = a.G + t_ * fg;
 #pragma unroll
     for (int i = 0; i < ITEMS; ++i) {
-      dyn[i] = dyt[oc[i]];
+      dyn[i] = a.ndy > 0 ? dyl[(t_ * RV + (tid >> 6) + 8 * i) * PU + cu] : dyt[oc[i]];
       cpn[i] = hp ? cpt[oc[i]] : 0.f;
       gtn[i] = *(const bf16x4*)(gt + og[i]);   // the unit's four gates: one 8-byte load
     }
@@ -991,6 +1035,12 @@ static bool persist_plan(int H, int B, int* RVo, int* chunko) {
 int persist_rows_per_workgroup(int H, int B) {
   int RV, chunk;
   return persist_plan(H, B, &RV, &chunk) ? RV : 16;
+}
+
+bool persist_bwd_dy_partials_ok(int H, int B, int T) {
+  int RV, chunk;
+  if (!persist_plan(H, B, &RV, &chunk)) return false;
+  return (size_t)BWD_DY_LDS + (size_t)T * RV * PU * 4 <= persist_lds_bytes(H, true, RV);
 }
 
 bool persist_bwd_needs_wt(int, int) { return false; }

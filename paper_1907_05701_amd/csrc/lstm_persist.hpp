@@ -21,6 +21,13 @@ struct PersistArgs {
   const float* bhh;
   int64_t b_d;
   int Kin;            // input width (a multiple of 8; zero k past the operands' ends)
+  // backward, optional: dy as ndy split-K partial sums (partial s of frame f,
+  // unit column c at DYP[s * dy_kstride + f * 2H + c]) instead of DY; the
+  // kernel sums its own rows' and units' entries in split order (the order
+  // of the separate reduction) before the steps, into LDS
+  const float* DYP;
+  int ndy;
+  int64_t dy_kstride;
   float* C;           // cell states [M][2H] (forward writes, backward reads)
   bf16* G;            // gate pre-activations [M][2][H][4] (direction, unit, gate i/f/g/o; forward writes, backward reads)
   bf16* DA;           // backward: gate pre-activation gradients [M][8H]
@@ -52,6 +59,9 @@ static inline size_t persist_xch_bytes(int B, int H) {
   return bwd > fwd ? bwd : fwd;
 }
 
+// Whether the backward can take dy as split-K partials (its summed dy of all
+// steps must fit the LDS beside the step buffers).
+bool persist_bwd_dy_partials_ok(int H, int B, int T);
 // True if the persistent kernels handle this H (a multiple of 64, at most
 // 512: a member's 256 W_hh rows fit in its registers); any T.
 bool persist_supported(int H, int T);

@@ -224,6 +224,14 @@ static inline bool colsum_job_ok(const ColSumJob& c) {
          (int64_t)c.batches * c.N / 4 < ((int64_t)1 << 31);
 }
 
+// Launches the jobs of a reduction group (nothing if it has none).
+static inline void reduce_group_launch(hipStream_t s, const ReduceGroup& rg) {
+  if (rg.n < 1) return;
+  const ReduceJob& last = rg.j[rg.n - 1];
+  const unsigned blocks = (unsigned)(last.start + cdiv((int64_t)last.count, 256));
+  BLSTM_LAUNCH("splitk_reduce_group", splitk_reduce_group_kernel, dim3(blocks), dim3(256), 0, s, rg);
+}
+
 // The reduction job of a column sum (rows summed in row order).
 static inline ReduceJob colsum_reduce_job(const ColSumJob& cs, int start) {
   ReduceJob r;
@@ -252,9 +260,11 @@ static inline bool colsum_job_launch(const char* name, hipStream_t s, const ColS
 // bf16 products only (the direct-to-LDS kernel); false and nothing launched
 // if a product cannot take that path or its reduction needs unaligned rows.
 // cs (optional): column sums added to the reduction launch.
+// held (optional): the reduction is not launched but returned there, for
+// the caller to launch later or to leave to a consumer of the partials.
 template <bool AKC, bool BKC>
 static inline bool gemm_f32_group(const char* name, hipStream_t s, int n, const F32Job* jb,
-                                  const ColSumJob* cs = nullptr) {
+                                  const ColSumJob* cs = nullptr, ReduceGroup* held = nullptr) {
   if (n < 1 || n > KC_MAX_GROUP || (cs && (n == KC_MAX_GROUP || !colsum_job_ok(*cs)))) return false;
   KcItem it[KC_MAX_GROUP];
   EpiStore<float> e[KC_MAX_GROUP];
@@ -287,6 +297,7 @@ static inline bool gemm_f32_group(const char* name, hipStream_t s, int n, const 
     rblocks += (int)cdiv((int64_t)rg.j[rg.n++].count, 256);
   }
   if (!gemm_kc_group_launch<AKC, BKC>(name, s, n, it, e)) return false;
-  if (rg.n) BLSTM_LAUNCH("splitk_reduce_group", splitk_reduce_group_kernel, dim3((unsigned)rblocks), dim3(256), 0, s, rg);
+  if (held) *held = rg;
+  else if (rg.n) reduce_group_launch(s, rg);
   return true;
 }

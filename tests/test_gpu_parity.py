@@ -719,10 +719,12 @@ def test_graph_replays_at_benchmark_shape(gpu_lib):
     dict(L=2, D=260, H=256, P=64, K=3000, T=25, B=44),      # two row passes, a 4-row last slice
     dict(L=2, D=64, H=512, P=64, K=500, T=11, B=200),       # 16-row slices, unpadded layer-0 W_ih
 ], ids=["b128", "ragged", "rows16"])
-def test_fused_input_projection_matches_the_separate_product(gpu_lib, monkeypatch, shape):
+def test_fused_products_match_the_separate_launches(gpu_lib, monkeypatch, shape):
     """The persistent forward computing each workgroup's slice of the input
-    projection itself gives the same step, bit for bit, as the separate
-    product launch (same k order and rounding)."""
+    projection itself, and the persistent BPTT adding the split-K partial
+    sums of dX itself (with every layer's bias sums in one reduction after
+    the last BPTT), give the same step, bit for bit, as the separate product
+    and reduction launches (same k order, summation order and rounding)."""
     from paper_1907_05701_amd.step import LearnerStep
     dims = ref.Dims(**shape)
     n = ref.param_count(dims)
@@ -732,6 +734,7 @@ def test_fused_input_projection_matches_the_separate_product(gpu_lib, monkeypatc
     out = {}
     for fuse in ("1", "0"):
         monkeypatch.setenv("ADPSGD_BLSTM_FUSE_GX", fuse)
+        monkeypatch.setenv("ADPSGD_BLSTM_FUSE_DY", fuse)
         st = LearnerStep(**shape, precision="bf16")
         st.load(theta, x, lab, theta)
         st.gradient()
@@ -741,4 +744,4 @@ def test_fused_input_projection_matches_the_separate_product(gpu_lib, monkeypatc
         del st
     for k in ("y_top", "loss", "grad"):
         np.testing.assert_array_equal(out["1"][k], out["0"][k], err_msg=k)
-    say(f"[fused gx] {shape} bit-identical, loss {float(out['1']['loss'][0]):.6f}")
+    say(f"[fused] {shape} bit-identical, loss {float(out['1']['loss'][0]):.6f}")
