@@ -208,8 +208,12 @@ def class_rates(st, cfg, lr, steps):
     for key, cls in (("fwd", "recurrence_fwd"), ("bwd", "recurrence_bwd")):
         if cls in mfma:
             rec[key] = round(mfma[cls]["ms_per_step"] * 1e3 / (L * T), 3)
-    # the forward launches' time includes the input projection when fused
+    # the forward launches' time includes the input projection when fused,
+    # the BPTT launches' the sum of the layer above's dX partials when those
+    # reductions (one per layer above layer 0) are not launched
     rec["fwd_includes_input_projection"] = fused
+    n_red = per.get("splitk_reduce_group", (0, 0.0))[0] / steps
+    rec["bwd_includes_dx_partial_sums"] = "lstm_rec_bwd_persist" in ms and n_red < L - 1
     return {"mfma": mfma, "recurrence_step_us": rec,
             "kernel_ms": {k: round(v, 4) for k, v in sorted(ms.items(), key=lambda kv: -kv[1])}}
 
