@@ -288,6 +288,18 @@ __global__ __launch_bounds__(WM * WN * 64, WM * WN / 2) void gemm_kc_group_kerne
   kc_gemm_tile<BM, BN, WM, WN, STAGES, BK, AKC, BKC, Epi>(g.p[i], g.e[i], (int)blockIdx.x - g.start[i]);
 }
 
+// Two independent products with different operand layouts in one launch
+// (each alone would leave part of its last round of the chip idle): the
+// first owns workgroups [0, n1) (n1 a multiple of 8), the second the rest.
+template <int BM, int BN, int WM, int WN, int STAGES, int BK, bool AKC1, bool BKC1, bool AKC2, bool BKC2, class Epi>
+__global__ __launch_bounds__(WM * WN * 64, WM * WN / 2) void gemm_kc_pair_kernel(const KcArgs p1, const Epi e1,
+                                                                             const KcArgs p2, const Epi e2, int n1) {
+  if ((int)blockIdx.x < n1)
+    kc_gemm_tile<BM, BN, WM, WN, STAGES, BK, AKC1, BKC1, Epi>(p1, e1, (int)blockIdx.x);
+  else
+    kc_gemm_tile<BM, BN, WM, WN, STAGES, BK, AKC2, BKC2, Epi>(p2, e2, (int)blockIdx.x - n1);
+}
+
 // Whether an operand can go through the direct-to-LDS path: no gate
 // interleave, 16-byte aligned rows and batch strides, the whole k range inside
 // the operand; MN-contiguous operands also need an MN extent that is a
@@ -390,6 +402,26 @@ static inline void gemm_launch(const char* name, hipStream_t s, const Opnd& A, c
     }
   }
   gemm_launch_cfg<T, GemmCfg<T>, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits, epi);
+}
+
+// The pair kernel above for two products (128x128 blocks); false and nothing
+// launched if either cannot take the direct-to-LDS path.
+template <bool AKC1, bool BKC1, bool AKC2, bool BKC2, class Epi>
+static inline bool gemm_kc_pair_launch(const char* name, hipStream_t s, const Opnd& A1, const Opnd& B1, int64_t M1,
+                                       int64_t N1, int64_t K1, int splits1, const Epi& e1, const Opnd& A2,
+                                       const Opnd& B2, int64_t M2, int64_t N2, int64_t K2, int splits2,
+                                       const Epi& e2) {
+  typedef KcTile C;
+  if (!kc_eligible(A1, B1, K1, AKC1, BKC1) || !kc_eligible(A2, B2, K2, AKC2, BKC2)) return false;
+  const KcArgs p1 = kc_args<C, AKC1, BKC1>(A1, B1, M1, N1, K1, 1, splits1);
+  const KcArgs p2 = kc_args<C, AKC2, BKC2>(A2, B2, M2, N2, K2, 1, splits2);
+  const int n1 = (int)rup(p1.total, 8);
+  auto fn = gemm_kc_pair_kernel<C::BM, C::BN, C::WM, C::WN, C::STAGES, C::BK, AKC1, BKC1, AKC2, BKC2, Epi>;
+  static std::atomic<uint64_t> lds_raised{0};
+  kc_raise_lds_limit((const void*)fn, C::lds_bytes, lds_raised);
+  BLSTM_LAUNCH(name, fn, dim3((unsigned)(n1 + p2.total)), dim3(C::WM * C::WN * 64), C::lds_bytes, s, p1, e1, p2, e2,
+               n1);
+  return true;
 }
 
 // One product of a grouped launch.

@@ -559,16 +559,26 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
     // db_s = sum over frames of ds
     colsum<T>("colsum_dbs", s, DS, M, K, Kp, csp, K, 0, grad + lo.bs, nullptr);
   }
-  // dW_s = ds^T z
-  gemm_f32<T, false, false, V, V>("gemm_dws", s, opnd(DS, Kp, Kp, M), opnd(Z, P, P, M), K, P, M, 1,
-                                  lo.sp_dWs, grad + lo.Ws, P, 0, part);
-  // bf16: W_s^T and W_l^T copies make dz and dy K-contiguous products
-  // dz = ds W_s (float32 and a low-precision copy for the next products);
-  // W_s [K][P] is the MN-contiguous operand as it lies (the direct-to-LDS
-  // kernel reads it with transposing LDS reads; measured faster than
-  // transposing W_s each step first)
-  gemm_f32<T, true, false, V, V>("gemm_dz", s, opnd(DS, Kp, Kp, M), opnd(W + lo.Ws, P, P, K), M, P,
-                                 K, 1, lo.sp_dz, DZ, P, 0, part, DZT, P);
+  // dW_s = ds^T z, and dz = ds W_s (float32 and a low-precision copy for
+  // the next products); W_s [K][P] is the MN-contiguous operand as it lies
+  // (the direct-to-LDS kernel reads it with transposing LDS reads; measured
+  // faster than transposing W_s each step first).  bf16: the two products
+  // in one launch (dW_s unsplit and stored directly, dz through its split-K
+  // partials and reduction), each alone ending on a partial round of the chip
+  const Opnd As = opnd(DS, Kp, Kp, M), Bs = opnd(Z, P, P, M);
+  const Opnd Az = opnd(DS, Kp, Kp, M), Bz2 = opnd(W + lo.Ws, P, P, K);
+  bool paired = false;
+  if constexpr (lp) {
+    if (lo.sp_dWs == 1 && lo.sp_dz > 1)
+      paired = gemm_kc_pair_launch<false, false, true, false>(
+          "gemm_dws_dz", s, As, Bs, K, P, M, 1, epi_store<float>(grad + lo.Ws, P, K, P, 0), Az, Bz2, M, P, K,
+          lo.sp_dz, epi_store<float>(part, P, M, P, (int64_t)lo.sp_dz * M * P, M * P));
+    if (paired) splitk_reduce_launch<T>(s, part, lo.sp_dz, 1, M, P, DZ, P, 0, DZT, P);
+  }
+  if (!paired) {
+    gemm_f32<T, false, false, V, V>("gemm_dws", s, As, Bs, K, P, M, 1, lo.sp_dWs, grad + lo.Ws, P, 0, part);
+    gemm_f32<T, true, false, V, V>("gemm_dz", s, Az, Bz2, M, P, K, 1, lo.sp_dz, DZ, P, 0, part, DZT, P);
+  }
   // db_l = sum over frames of dz (bf16: already summed with db_s)
   if constexpr (!lp) colsum<float>("colsum_dbl", s, DZ, M, P, P, csp, P, 0, grad + lo.bl, nullptr);
   // dW_l = dz^T y

@@ -123,6 +123,23 @@ __global__ __launch_bounds__(64) void splitk_reduce4_kernel(const float* __restr
   }
 }
 
+// The split-K reduction of a product whose partials gemm_f32 left in part
+// (dst, and a low-precision copy dstc if given).
+template <typename T>
+static inline void splitk_reduce_launch(hipStream_t s, float* part, int splits, int batches, int64_t M, int64_t N,
+                                        float* dst, int64_t ld, int64_t dst_zstride, T* dstc, int64_t ldc) {
+  if (N % 4 == 0 && ld % 4 == 0 && dst_zstride % 4 == 0 && ((uintptr_t)dst & 15) == 0 &&
+      (!dstc || (ldc % 4 == 0 && ((uintptr_t)dstc & 7) == 0))) {
+    BLSTM_LAUNCH("splitk_reduce", splitk_reduce4_kernel<T>, dim3((unsigned)M, (unsigned)cdiv(N, 256), batches),
+                 dim3(64), 0, s, part, splits, M, N, dst, ld, dst_zstride, dstc, ldc, (const float*)nullptr);
+    return;
+  }
+  const int64_t total = (int64_t)batches * M * N;
+  const unsigned grid = (unsigned)std::min<int64_t>(cdiv(total, 256), 8192);
+  BLSTM_LAUNCH("splitk_reduce", splitk_reduce_kernel<T>, dim3(grid), dim3(256), 0, s, part, splits,
+               batches, M, N, dst, ld, dst_zstride, dstc, ldc);
+}
+
 // C = A B with a float32 destination (ld, dst_zstride per batch).  With
 // splits > 1 (or when a low-precision copy dstc is wanted) the product goes
 // through split-K partials and the fixed-order reduction.
@@ -137,16 +154,7 @@ static inline void gemm_f32(const char* name, hipStream_t s, const Opnd& A, cons
   }
   gemm_launch<T, AKC, BKC, VA, VB>(name, s, A, B, M, N, K, batches, splits,
                                    epi_store<float>(part, N, M, N, (int64_t)splits * M * N, M * N));
-  if (N % 4 == 0 && ld % 4 == 0 && dst_zstride % 4 == 0 && ((uintptr_t)dst & 15) == 0 &&
-      (!dstc || (ldc % 4 == 0 && ((uintptr_t)dstc & 7) == 0))) {
-    BLSTM_LAUNCH("splitk_reduce", splitk_reduce4_kernel<T>, dim3((unsigned)M, (unsigned)cdiv(N, 256), batches),
-                 dim3(64), 0, s, part, splits, M, N, dst, ld, dst_zstride, dstc, ldc, (const float*)nullptr);
-    return;
-  }
-  const int64_t total = (int64_t)batches * M * N;
-  const unsigned grid = (unsigned)std::min<int64_t>(cdiv(total, 256), 8192);
-  BLSTM_LAUNCH("splitk_reduce", splitk_reduce_kernel<T>, dim3(grid), dim3(256), 0, s, part, splits,
-               batches, M, N, dst, ld, dst_zstride, dstc, ldc);
+  splitk_reduce_launch<T>(s, part, splits, batches, M, N, dst, ld, dst_zstride, dstc, ldc);
 }
 
 // Several float32-destination products in one launch (see gemm_f32), then
