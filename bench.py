@@ -71,6 +71,8 @@ def kernel_work(name, c, n_params, fused_gx=False):
         return "mfma", 2 * 2 * M * K * P, "flop", 1
     if name in ("gemm_dwl", "gemm_dy"):
         return "mfma", 2 * M * P * 2 * H, "flop", 1
+    if name == "gemm_dwl_dy":
+        return "mfma", 2 * 2 * M * P * 2 * H, "flop", 1
     if name == "softmax_ce_rows":
         Kp = (K + 7) // 8 * 8
         return "hbm", 2 * M * Kp * es + 8 * M, "byte", 1
@@ -174,7 +176,7 @@ CLASSES = {
     "gate_projection": ("gemm_gx",),
     "backward_products": ("gemm_bwd_group", "gemm_dw_group", "gemm_dwih", "gemm_dwhh", "gemm_dx"),
     "head_products": ("gemm_z", "gemm_logits", "gemm_logits_ds", "gemm_dws", "gemm_dz", "gemm_dws_dz", "gemm_dwl",
-                      "gemm_dy"),
+                      "gemm_dy", "gemm_dwl_dy"),
     "recurrence_fwd": ("lstm_rec_fwd_persist", "lstm_rec_fwd"),
     "recurrence_bwd": ("lstm_rec_bwd_persist", "lstm_rec_bwd"),
 }

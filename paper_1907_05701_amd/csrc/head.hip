@@ -581,12 +581,24 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
   }
   // db_l = sum over frames of dz (bf16: already summed with db_s)
   if constexpr (!lp) colsum<float>("colsum_dbl", s, DZ, M, P, P, csp, P, 0, grad + lo.bl, nullptr);
-  // dW_l = dz^T y
-  gemm_f32<T, false, false, V, V>("gemm_dwl", s, opnd(DZT, P, P, M), opnd(ytop, H2, H2, M), P, H2, M,
-                                  1, lo.sp_dWl, grad + lo.Wl, H2, 0, part);
-  // dy = dz W_l (W_l [P][2H] MN-contiguous as it lies)
-  gemm_f32<T, true, false, V, V>("gemm_dy", s, opnd(DZT, P, P, M), opnd(W + lo.Wl, H2, H2, P), M,
-                                 H2, P, 1, lo.sp_dy, dytop, H2, 0, part);
+  // dW_l = dz^T y, and dy = dz W_l (W_l [P][2H] MN-contiguous as it lies);
+  // bf16: one launch for both (dW_l through its split-K partials, dy stored
+  // directly)
+  const Opnd Al = opnd(DZT, P, P, M), Bl = opnd(ytop, H2, H2, M);
+  const Opnd Ay = opnd(DZT, P, P, M), By = opnd(W + lo.Wl, H2, H2, P);
+  bool paired_l = false;
+  if constexpr (lp) {
+    if (lo.sp_dWl > 1 && lo.sp_dy == 1)
+      paired_l = gemm_kc_pair_launch<false, false, true, false>(
+          "gemm_dwl_dy", s, Al, Bl, P, H2, M, lo.sp_dWl,
+          epi_store<float>(part, H2, P, H2, (int64_t)lo.sp_dWl * P * H2, P * H2), Ay, By, M, H2, P, 1,
+          epi_store<float>(dytop, H2, M, H2, 0));
+    if (paired_l) splitk_reduce_launch<T>(s, part, lo.sp_dWl, 1, P, H2, grad + lo.Wl, H2, 0, (T*)nullptr, 0);
+  }
+  if (!paired_l) {
+    gemm_f32<T, false, false, V, V>("gemm_dwl", s, Al, Bl, P, H2, M, 1, lo.sp_dWl, grad + lo.Wl, H2, 0, part);
+    gemm_f32<T, true, false, V, V>("gemm_dy", s, Ay, By, M, H2, P, 1, lo.sp_dy, dytop, H2, 0, part);
+  }
   return blstm_check_launch("softmax_ce_fwd_bwd");
 }
 
