@@ -66,6 +66,9 @@ def kernel_work(name, c, n_params, fused_gx=False):
         return "mfma", 2 * M * P * 2 * H, "flop", 1
     if name in ("gemm_logits", "gemm_logits_ds", "gemm_dws", "gemm_dz"):
         return "mfma", 2 * M * K * P, "flop", 1
+    if name in ("logits_blk", "logits_ds_blk"):
+        # the logits products as class-block kernels (W_s block in registers)
+        return "mfma", 2 * M * K * P, "flop", 1
     if name == "gemm_dws_dz":
         # dW_s and dz in one launch
         return "mfma", 2 * 2 * M * K * P, "flop", 1
@@ -175,8 +178,8 @@ def cpu_baseline(cfg, budget_s=12.0, one_thread_s=6.0):
 CLASSES = {
     "gate_projection": ("gemm_gx",),
     "backward_products": ("gemm_bwd_group", "gemm_dw_group", "gemm_dwih", "gemm_dwhh", "gemm_dx"),
-    "head_products": ("gemm_z", "gemm_logits", "gemm_logits_ds", "gemm_dws", "gemm_dz", "gemm_dws_dz", "gemm_dwl",
-                      "gemm_dy", "gemm_dwl_dy"),
+    "head_products": ("gemm_z", "gemm_logits", "gemm_logits_ds", "logits_blk", "logits_ds_blk", "gemm_dws", "gemm_dz",
+                      "gemm_dws_dz", "gemm_dwl", "gemm_dy", "gemm_dwl_dy"),
     "recurrence_fwd": ("lstm_rec_fwd_persist", "lstm_rec_fwd"),
     "recurrence_bwd": ("lstm_rec_bwd_persist", "lstm_rec_bwd"),
 }
@@ -203,7 +206,7 @@ def class_rates(st, cfg, lr, steps):
             if k not in ms:
                 continue
             w = kernel_work(k, cfg, st.n, fused_gx=fused)
-            if w is not None and not (k == "gemm_logits_ds"):   # the logits count once (recomputed for ds)
+            if w is not None and k not in ("gemm_logits_ds", "logits_ds_blk"):   # the logits count once (recomputed for ds)
                 flop += w[1]
         if t > 0:
             tf = flop / (t * 1e-3) / 1e12

@@ -341,6 +341,429 @@ struct EpiSoftmaxDs {
 
 };
 
+// ---------------------------------------------------------------------------
+// The two logits products with the class block held on chip (bf16, P <= 256).
+// One workgroup of 8 waves per block of LB = 128 classes: each wave keeps
+// the W_s rows of its 32 classes in registers for the whole launch, and all
+// M frames of z pass through an LDS ring in chunks of LF = 64 frames, so W_s
+// is read once per workgroup and z once per workgroup from L2 (instead of
+// both operands once per output tile), and the 250 workgroups of the full
+// model each take one CU for the whole launch.  Wave w = (wm, wn) =
+// (w % 4, w / 4) computes classes 32 wm .. +31 of the block for frames
+// 32 wn .. +31 of each chunk; a lane holds four consecutive classes of one
+// frame, as in the blocked products above.  The bias is the accumulator
+// input of the first k-step, so the products give the logits themselves.
+//   PASS 1: per (frame, block) maximum and sum of exp over the block's
+//     classes (the block is the strip of the statistics, combined per frame
+//     by logit_lse): the maximum over the wave's 32 classes, then the sum of
+//     exp(s - maximum) (lanes exchange by permlane swaps; max and + are
+//     commutative, so all four lane groups hold the same result), then over
+//     the four class waves in order through LDS (one chunk later).
+//   PASS 2: ds = scale (softmax - onehot) in bf16, the frame loss at the
+//     label, and the db_s sums of the block's classes over all frames: per
+//     lane over its frames in chunk order, then over the 16 frame lanes
+//     (DPP, fixed order) and the two frame waves in order; one complete row.
+// Software pipeline: iteration j multiplies chunk j + 1 while it runs the
+// epilogue of chunk j, so the MFMA and the vector ALU work overlap within
+// a wave.  The ring (LSL slots, direct-to-LDS loads; with pass 2 also the
+// chunk's log-sum-exp values and labels, read into registers with the
+// chunk's fragments) runs three chunks ahead: chunk j + 4 is requested right
+// after the barrier that ends every wave's use of chunk j, into its slot.
+// The buffer resources advance by the chunk (scalar arithmetic; their range
+// ends at frame M, so rows past M read as zeros and their stores are
+// dropped) and the per-lane offsets stay fixed.  Every wave issues the same
+// number of memory instructions per chunk (a dummy load into a scratch area
+// where a wave has no row; stores whose unused lanes carry an out-of-range
+// offset), so the wait for a chunk is an exact vmcnt bound: what the wave
+// issued after that chunk's loads.
+// LDS ring rows: frames in pairs of 1 KB blocks at a pitch of 1056 bytes,
+// the second row of a pair with its 16-byte chunks swapped in pairs
+// (chunk c in slot c ^ 1): the 8 (16) lanes of one 16-byte read phase hit
+// distinct banks, and a fragment's address moves by a constant per k-step.
+// ---------------------------------------------------------------------------
+#define LB 128
+#define LF 64
+#define LSL 4
+#define LKS 8                        // 32-deep k-steps (P <= 256)
+#define LBLK 1056                    // LDS bytes per pair of z rows
+#define LSLOT (LF / 2 * LBLK)        // LDS bytes per ring slot
+struct LogitsArgs {
+  const bf16* Ws;      // [K][P]
+  const bf16* Z;       // [M][P]
+  const float* bias;   // b_s [K]
+  int K, M, P;
+  float2* stats;       // PASS 1: [M][nstrip] (nstrip = blocks)
+  int nstrip;
+  const float* lse;    // PASS 2: [M]
+  const int32_t* labels;
+  bf16* ds;            // [M][Kp]
+  int Kp;
+  float* rowloss;      // [M]
+  float* dbs;          // [K]: db_s
+  float scale, l2s;    // as in EpiSoftmaxDs
+};
+static constexpr size_t LG_RING = (size_t)LSL * LSLOT;
+static constexpr size_t LG_LSE = LG_RING, LG_LAB = LG_LSE + LSL * LF * 4, LG_EX = LG_LAB + LSL * LF * 4;
+static constexpr size_t LG_SCRATCH = LG_EX + 2 * 4 * LF * 8;
+static constexpr size_t LG_SIMD = LG_SCRATCH + 256;   // 4 counters
+static constexpr size_t LG_LDS = LG_SIMD + 16;
+static_assert(LG_LDS <= 160 * 1024, "LDS of one CU");
+
+typedef uint32_t v2u32 __attribute__((ext_vector_type(2)));
+typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
+
+// LDS write and reads of the statistics exchange as inline asm: the
+// compiler's own forms are made to wait for every direct-to-LDS load in
+// flight (it cannot tell which LDS bytes they write), which would drain the
+// ring; the exchange area is disjoint from every load's destination.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+__device__ __forceinline__ void lds_write_f2(float2* p, float x, float y) {
+  const v2u32 v{__float_as_uint(x), __float_as_uint(y)};
+  asm volatile("ds_write_b64 %0, %1" ::"v"(lds_addr(p)), "v"(v) : "memory");
+}
+// the four values p[0], p[LF], p[2 LF], p[3 LF] (512 bytes apart)
+__device__ __forceinline__ void lds_read_f2x4(const float2* p, v2u32 (&v)[4]) {
+  asm volatile(
+      "ds_read_b64 %0, %4\n\tds_read_b64 %1, %4 offset:512\n\tds_read_b64 %2, %4 offset:1024\n\t"
+      "ds_read_b64 %3, %4 offset:1536\n\ts_waitcnt lgkmcnt(0)"
+      : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3])
+      : "v"(lds_addr(p))
+      : "memory");
+}
+
+__device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, void* lds_wave_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)lds_wave_base, 4, byte_off, 0, 0, 0);
+}
+// buffer resource over rows [0, rows) of rowbytes bytes from base (none
+// when rows <= 0; the caller keeps rows * rowbytes below 2^31 - 16)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_rows(const void* base, int rows, int rowbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, max(rows, 0) * rowbytes, 0x00020000);
+}
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+// two floats to a bf16 pair (round to nearest even), x in the low half
+__device__ __forceinline__ uint32_t pack_bf16x2(float x, float y) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{x, y}, bf16x2));
+}
+// x and the same register of lane ^ 16 (^ 32), in an order that depends on
+// the lane: for commutative combinations only
+__device__ __forceinline__ v2u32 pair16(float x) {
+  return __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+}
+__device__ __forceinline__ v2u32 pair32(float x) {
+  return __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+}
+// maxima as plain v_max instructions: the compiler's fmaxf first quiets
+// signalling NaNs of operands it cannot prove canonical (every MFMA result
+// and permlane output here), one more instruction per operand; a NaN logit
+// still reaches the sums (and the loss) through the exponentials
+__device__ __forceinline__ float vmax(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ __forceinline__ float vmax3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+__device__ __forceinline__ float max16x32(float x) {
+  v2u32 p = pair16(x);
+  x = vmax(__uint_as_float(p[0]), __uint_as_float(p[1]));
+  p = pair32(x);
+  return vmax(__uint_as_float(p[0]), __uint_as_float(p[1]));
+}
+__device__ __forceinline__ float sum16x32(float x) {
+  v2u32 p = pair16(x);
+  x = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  p = pair32(x);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+
+// s_getreg operand: HW_ID (register 4), bits 4-5 (the SIMD)
+#define HWREG_HW_ID_SIMD ((1 << 11) | (4 << 6) | 4)
+
+template <int PASS, bool FOLD>
+__global__ __launch_bounds__(512) void logits_block_kernel(const LogitsArgs a) {
+  extern __shared__ __attribute__((aligned(1024))) char lds[];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w & 3, wn = w >> 2;
+  const int fr = lane & 15, fc = lane >> 4;
+  const int K = a.K, M = a.M, P = a.P;
+  const int c0 = blockIdx.x * LB;
+  const int cl = c0 + 32 * wm + 4 * fc;   // the lane's first class (+16 i + r)
+  const int nch = (M + LF - 1) / LF;
+  constexpr int NLD = PASS == 2 ? 5 : 4;  // loads per wave and chunk
+  constexpr int NST = PASS == 2 ? 4 : 1;  // stores per wave and chunk
+  // the waves that share a SIMD take the product and the epilogue of a
+  // step in alternating orders, so that one's MFMAs run beside the other's
+  // vector ALU work: rank among the workgroup's waves on this SIMD (SIMD
+  // from the wave's hardware id), by an LDS counter per SIMD.  Only the
+  // timing depends on it.
+  bool product_first;
+  {
+    int* cnt = (int*)(lds + LG_SIMD);
+    if (tid < 4) cnt[tid] = 0;
+    __syncthreads();
+    const int simd = (__builtin_amdgcn_s_getreg(HWREG_HW_ID_SIMD) & 3);
+    const int rank = __builtin_amdgcn_readfirstlane(lane == 0 ? atomicAdd(&cnt[simd], 1) : 0);
+    product_first = (rank & 1) == 0;
+  }
+  // the wave's W_s rows (A operand): class c0 + 32 wm + 16 i + fr, k = 32 ks + 8 fc
+  bf16x8 af[2][LKS];
+  {
+    const __amdgpu_buffer_rsrc_t rw = dma_rsrc(a.Ws);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int ks = 0; ks < LKS; ++ks) {
+        const int row = c0 + 32 * wm + 16 * i + fr, k = 32 * ks + 8 * fc;
+        const uint32_t off = row < K && k < P ? (uint32_t)(((int64_t)row * P + k) * 2) : DMA_OFF_NONE;
+        af[i][ks] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)off, 0, 0));
+      }
+  }
+  // the lane's classes cl + 16 i + r: bias, -inf past K (clamped loads)
+  f32x4 bv[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) bv[i][r] = a.bias[min(cl + 16 * i + r, K - 1)];
+  // A fragments and biases in registers before the ring loads (a wait the
+  // compiler sees, so it adds none of its own for them in the chunk loop)
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (cl + 16 * i + r >= K) bv[i][r] = -INFINITY;
+
+  // ring loads: instruction q of wave w fills rows 2 b, 2 b + 1 of the
+  // chunk (b = 8 q + w); lane (parity p = lane / 32, slot s = lane % 32)
+  // reads chunk s ^ p of its row
+  uint32_t zoff[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int p = lane >> 5, row = 2 * (q * 8 + w) + p, c = (lane & 31) ^ p;
+    zoff[q] = c * 8 < P ? (uint32_t)((row * P + c * 8) * 2) : DMA_OFF_NONE;
+  }
+  auto issue = [&](int j) {
+    const int f0 = j * LF, left = M - f0;
+    char* st = lds + (j % LSL) * LSLOT;
+    const __amdgpu_buffer_rsrc_t rz = rsrc_rows(a.Z + (int64_t)f0 * P, left, P * 2);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) dma16(rz, zoff[q], st + (q * 8 + w) * LBLK);
+    if constexpr (PASS == 2) {
+      if (w == 0) dma4(rsrc_rows(a.lse + f0, left, 4), lane * 4, lds + LG_LSE + (j % LSL) * LF * 4);
+      else if (w == 1) dma4(rsrc_rows(a.labels + f0, left, 4), lane * 4, lds + LG_LAB + (j % LSL) * LF * 4);
+      else dma4(rz, DMA_OFF_NONE, lds + LG_SCRATCH);
+    }
+  };
+  // fragment reads: row 32 wn + 16 jn + fr of the chunk, 16-byte chunk
+  // 4 ks + fc; jn = 1 is 8 blocks further, ks 64 bytes
+  const int rrow = 32 * wn + fr;
+  const uint32_t rbase = (rrow >> 1) * LBLK + (rrow & 1) * 512 + ((fc ^ (rrow & 1)) * 16);
+  auto product = [&](int j, f32x4 (&o)[2][2]) {
+    const char* st = lds + (j % LSL) * LSLOT + rbase;
+#pragma unroll
+    for (int ks = 0; ks < LKS; ++ks) {
+      bf16x8 b[2];
+#pragma unroll
+      for (int jn = 0; jn < 2; ++jn) b[jn] = *(const bf16x8*)(st + jn * 8 * LBLK + ks * 64);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int jn = 0; jn < 2; ++jn) o[i][jn] = Mfma<bf16>::mma(af[i][ks], b[jn], ks == 0 ? bv[i] : o[i][jn]);
+    }
+  };
+  // the frames' log-sum-exp and labels (+inf and -1 past M)
+  auto frame_data = [&](int j, float (&L)[2], int (&lab)[2]) {
+    const float* sl = (const float*)(lds + LG_LSE + (j % LSL) * LF * 4);
+    const int32_t* sb = (const int32_t*)(lds + LG_LAB + (j % LSL) * LF * 4);
+#pragma unroll
+    for (int jn = 0; jn < 2; ++jn) {
+      const int fl = 32 * wn + 16 * jn + fr;
+      const bool fok = j * LF + fl < M;
+      L[jn] = fok ? sl[fl] : INFINITY;
+      const int lb = sb[fl];
+      lab[jn] = fok && lb < K ? lb : -1;
+    }
+  };
+
+  float2* ex = (float2*)(lds + LG_EX);   // [2 chunks][4 class waves][LF frames]
+  // PASS 1: combine chunk j's four class-wave statistics (wave 0) and store
+  // them; one store instruction in every wave (none valid for j < 0)
+  auto combine = [&](int j) {
+    float2 v = make_float2(0.f, 0.f);
+    if (w == 0) {
+      // maximum of the four, then the sums scaled to it in wave order (a
+      // wave whose classes are all past K holds (-inf, 0) and adds zero)
+      v2u32 e4[4];
+      lds_read_f2x4(ex + (j & 1) * 4 * LF + lane, e4);
+      const float m = vmax(vmax3(__uint_as_float(e4[0].x), __uint_as_float(e4[1].x), __uint_as_float(e4[2].x)),
+                           __uint_as_float(e4[3].x));
+      const float nm = m == -INFINITY ? 0.f : -m * LOG2E_F;
+      float sm = 0.f;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        sm = fmaf(__uint_as_float(e4[q].y), exp2_hw(fmaf(__uint_as_float(e4[q].x), LOG2E_F, nm)), sm);
+      v = make_float2(m, sm);
+    }
+    const int f0 = j * LF;
+    const __amdgpu_buffer_rsrc_t rs = rsrc_rows(a.stats + (int64_t)f0 * a.nstrip, M - f0, a.nstrip * 8);
+    const uint32_t off = w == 0 && j >= 0 ? (uint32_t)((lane * a.nstrip + (int)blockIdx.x) * 8) : DMA_OFF_NONE;
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(v2u32, v), rs, (int)off, 0, 0);
+  };
+  // PASS 2 store offsets within a chunk: 8 consecutive classes per lane
+  // (lane groups g and g ^ 1 swap halves: even groups classes 8 (g / 2) ..
+  // of row tile 0, odd groups those of row tile 1)
+  const int k0 = c0 + 32 * wm + (fc & 1) * 16 + (fc >> 1) * 8;
+  uint32_t dsoff[2];
+#pragma unroll
+  for (int jn = 0; jn < 2; ++jn)
+    dsoff[jn] = k0 < a.Kp ? (uint32_t)(((32 * wn + 16 * jn + fr) * a.Kp + k0) * 2) : DMA_OFF_NONE;
+  float csum[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) csum[i][r] = 0.f;
+
+  auto epilogue = [&](int j, const f32x4 (&acc)[2][2], const float (&L)[2], const int (&lab)[2]) {
+    if constexpr (PASS == 1) {
+#pragma unroll
+      for (int jn = 0; jn < 2; ++jn) {
+        float mx = vmax3(vmax3(acc[0][jn][0], acc[0][jn][1], acc[0][jn][2]),
+                         vmax3(acc[0][jn][3], acc[1][jn][0], acc[1][jn][1]), vmax(acc[1][jn][2], acc[1][jn][3]));
+        mx = max16x32(mx);
+        const float nm = mx == -INFINITY ? 0.f : -mx * LOG2E_F;
+        float sm = exp2_hw(fmaf(acc[0][jn][0], LOG2E_F, nm));
+#pragma unroll
+        for (int e = 1; e < 8; ++e) sm += exp2_hw(fmaf(acc[e >> 2][jn][e & 3], LOG2E_F, nm));
+        sm = sum16x32(sm);
+        if (fc == 0) lds_write_f2(ex + ((j & 1) * 4 + wm) * LF + 32 * wn + 16 * jn + fr, mx, sm);
+      }
+    } else {
+      const int f0 = j * LF;
+      const __amdgpu_buffer_rsrc_t rd = rsrc_rows(a.ds + (int64_t)f0 * a.Kp, M - f0, a.Kp * 2);
+      const __amdgpu_buffer_rsrc_t rr = rsrc_rows(a.rowloss + f0, M - f0, 4);
+#pragma unroll
+      for (int jn = 0; jn < 2; ++jn) {
+        const float Lc = FOLD ? fmaf(L[jn], LOG2E_F, -a.l2s) : L[jn] * LOG2E_F;
+        float lv = 0.f;
+        bool has = false;
+        uint32_t pk[2][2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          float v[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            v[r] = exp2_hw(fmaf(acc[i][jn][r], LOG2E_F, -Lc));
+            if constexpr (!FOLD) v[r] *= a.scale;
+          }
+          const int kb = cl + 16 * i;
+          if ((unsigned)(lab[jn] - kb) < 4u) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (lab[jn] - kb == r) {
+                lv = L[jn] - acc[i][jn][r];
+                has = true;
+                v[r] -= a.scale;
+              }
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) csum[i][r] += v[r];
+          pk[i][0] = pack_bf16x2(v[0], v[1]);
+          pk[i][1] = pack_bf16x2(v[2], v[3]);
+        }
+        // odd lane groups take the even partner's row tile 1 classes, even
+        // groups the odd partner's row tile 0 classes
+        const v2u32 sx = __builtin_amdgcn_permlane16_swap(pk[0][0], pk[1][0], false, false);
+        const v2u32 sy = __builtin_amdgcn_permlane16_swap(pk[0][1], pk[1][1], false, false);
+        const v4u32 v4{sx[0], sy[0], sx[1], sy[1]};
+        __builtin_amdgcn_raw_buffer_store_b128(v4, rd, (int)dsoff[jn], 0, 0);
+        const uint32_t loff = has ? (uint32_t)((32 * wn + 16 * jn + fr) * 4) : DMA_OFF_NONE;
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(lv), rr, (int)loff, 0, 0);
+      }
+    }
+  };
+
+  // one iteration: wait for chunk j + 1, request chunk j + 4, pass 1's
+  // combine of chunk j - 1, the product of chunk j + 1 and the epilogue of
+  // chunk j
+  // NST store instructions that write nothing (every offset out of range)
+  auto no_stores = [&]() {
+    const __amdgpu_buffer_rsrc_t rr = rsrc_rows(a.rowloss, 0, 4);
+#pragma unroll
+    for (int q = 0; q < NST; ++q) __builtin_amdgcn_raw_buffer_store_b32(0u, rr, (int)DMA_OFF_NONE, 0, 0);
+  };
+  auto step = [&](int j, const f32x4 (&cur)[2][2], f32x4 (&nxt)[2][2], const float (&Lc)[2], const int (&lc)[2],
+                  float (&Ln)[2], int (&ln)[2]) {
+    // issued after chunk j + 1's loads: chunks j + 2, j + 3 and three
+    // chunks' stores (the prologue's empty ones standing in for chunks
+    // before the first)
+    kc_wait_vm<2 * NLD + 3 * NST>();
+    if constexpr (PASS == 1) asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // exchange writes
+    // chunk j + 1 in the ring; every wave is done with chunk j's slot (a
+    // bare barrier: the fence of __syncthreads would wait for every load)
+    kc_barrier();
+    issue(j + 4);
+    if constexpr (PASS == 1) combine(j - 1);
+    if (product_first) {
+      product(j + 1, nxt);
+      if constexpr (PASS == 2) frame_data(j + 1, Ln, ln);
+      epilogue(j, cur, Lc, lc);
+    } else {
+      epilogue(j, cur, Lc, lc);
+      product(j + 1, nxt);
+      if constexpr (PASS == 2) frame_data(j + 1, Ln, ln);
+    }
+  };
+
+  f32x4 accA[2][2], accB[2][2];
+  float LA[2], LB_[2];
+  int labA[2], labB[2];
+#pragma unroll
+  for (int j = 0; j < LSL - 1; ++j) {
+    no_stores();
+    issue(j);
+  }
+  no_stores();
+  kc_wait_vm<2 * NLD + 3 * NST>();
+  kc_barrier();
+  issue(LSL - 1);
+  no_stores();
+  product(0, accA);
+  if constexpr (PASS == 2) frame_data(0, LA, labA);
+  for (int j = 0; j < nch; j += 2) {
+    step(j, accA, accB, LA, labA, LB_, labB);
+    if (j + 1 < nch) step(j + 1, accB, accA, LB_, labB, LA, labA);
+  }
+  if constexpr (PASS == 1) {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    kc_barrier();
+    combine(nch - 1);
+  } else {
+    // db_s: over the 16 frame lanes of each lane group, then the two frame
+    // waves in order
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) csum[i][r] = row16_sum(csum[i][r]);
+    float* red = (float*)(lds + LG_EX);   // [2 frame waves][LB]
+    __syncthreads();
+    if (fr == 0) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[wn * LB + 32 * wm + 16 * i + 4 * fc + r] = csum[i][r];
+    }
+    __syncthreads();
+    if (tid < LB && c0 + tid < K) a.dbs[c0 + tid] = red[tid] + red[LB + tid];
+  }
+  dma_wait_all();   // the ring's last (zero) loads land before the workgroup leaves its LDS
+}
+
 // Bias gradients and loss from the second product's outputs, one workgroup
 // of 1024 threads per strip of 128 classes plus one for the loss:
 //   db_s[k] = sum of the column-sum partial rows of class k (four row
@@ -487,6 +910,14 @@ __global__ __launch_bounds__(256) void loss_sum_kernel(const float* __restrict__
   if (threadIdx.x == 0) *loss = scale * buf[0];
 }
 
+// Whether the logits products run as the class-block kernels
+// (ADPSGD_LOGITS_BLOCK=0: the tiled products with their epilogues, for
+// comparisons).
+static bool logits_block() {
+  const char* e = getenv("ADPSGD_LOGITS_BLOCK");
+  return !(e && e[0] == '0');
+}
+
 template <typename T> struct VecH { static constexpr int v = 8; };
 template <> struct VecH<float> { static constexpr int v = 4; };
 
@@ -528,23 +959,50 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
     const int ftile = kc ? KcTile::BN : GemmCfgK32::BN;
     static_assert(KcTile::BM / KcTile::WM == GemmCfgK32::BM / GemmCfgK32::WM, "strip rows of the fallback tiles");
     static_assert(KcTile::BN == KcTileTall::BN, "frame columns of the kc tiles");
-    const int nstrip = (int)cdiv(K, srows);
     float2* stats = (float2*)(hws + lo.LST);
     float* lse = (float*)(hws + lo.LSE);
     float* dbp = (float*)(hws + lo.LDB);
-    EpiLogitStats e1{theta + lo.bs, stats, K, (int)M, nstrip, srows};
-    gemm_launch<T, true, true, V, V>("gemm_logits", s, Aw, Bz, K, M, P, 1, 1, e1);
-    BLSTM_LAUNCH("logit_lse", logit_lse_kernel, dim3((unsigned)cdiv(M, 4)), dim3(256), 0, s, stats, nstrip, M, labels,
-                 K, lse, RL);
     const float l2s = (scale > 0.f && std::isnormal(scale)) ? std::log2(scale) : NAN;
-    EpiSoftmaxDs e2{theta + lo.bs, lse, labels, (bf16*)DS, RL, dbp, scale, l2s, K, Kp, (int)M};
-    gemm_launch<T, true, true, V, V>("gemm_logits_ds", s, Aw, Bz, K, M, P, 1, 1, e2);
+    // the class-block kernels: every byte offset they form within 31 bits
+    // (the buffer resource's range), 16-byte aligned rows
+    const int nblk = (int)cdiv(K, LB);
+    const bool blk = logits_block() && P % 8 == 0 && P <= 8 * LKS * 4 && M > 0 &&
+                     (int64_t)rup(K, LB) * P * 2 < 0x7ffffff0 && M * P * 2 < 0x7ffffff0 &&
+                     M * Kp * 2 < 0x7ffffff0 && M * nblk * 8 < 0x7ffffff0 && M * 4 < 0x7ffffff0 &&
+                     ((uintptr_t)(W + lo.Ws) & 15) == 0 && ((uintptr_t)Z & 15) == 0 && ((uintptr_t)DS & 15) == 0;
+    int nrows_dbp;
+    if (blk) {
+      static std::atomic<uint64_t> raised1{0}, raised2{0}, raised3{0};
+      const bool fold = l2s == l2s;
+      const void* k2 = fold ? (const void*)logits_block_kernel<2, true> : (const void*)logits_block_kernel<2, false>;
+      kc_raise_lds_limit((const void*)logits_block_kernel<1, true>, LG_LDS, raised1);
+      kc_raise_lds_limit(k2, LG_LDS, fold ? raised2 : raised3);
+      LogitsArgs la{(const bf16*)(W + lo.Ws), (const bf16*)Z, theta + lo.bs, K, (int)M, P, stats, nblk, lse, labels,
+                    (bf16*)DS, Kp, RL, dbp, scale, l2s};
+      BLSTM_LAUNCH("logits_blk", (logits_block_kernel<1, true>), dim3((unsigned)nblk), dim3(512), LG_LDS, s, la);
+      BLSTM_LAUNCH("logit_lse", logit_lse_kernel, dim3((unsigned)cdiv(M, 4)), dim3(256), 0, s, stats, nblk, M, labels,
+                   K, lse, RL);
+      if (fold)
+        BLSTM_LAUNCH("logits_ds_blk", (logits_block_kernel<2, true>), dim3((unsigned)nblk), dim3(512), LG_LDS, s, la);
+      else
+        BLSTM_LAUNCH("logits_ds_blk", (logits_block_kernel<2, false>), dim3((unsigned)nblk), dim3(512), LG_LDS, s, la);
+      nrows_dbp = 1;
+    } else {
+      const int nstrip = (int)cdiv(K, srows);
+      EpiLogitStats e1{theta + lo.bs, stats, K, (int)M, nstrip, srows};
+      gemm_launch<T, true, true, V, V>("gemm_logits", s, Aw, Bz, K, M, P, 1, 1, e1);
+      BLSTM_LAUNCH("logit_lse", logit_lse_kernel, dim3((unsigned)cdiv(M, 4)), dim3(256), 0, s, stats, nstrip, M,
+                   labels, K, lse, RL);
+      EpiSoftmaxDs e2{theta + lo.bs, lse, labels, (bf16*)DS, RL, dbp, scale, l2s, K, Kp, (int)M};
+      gemm_launch<T, true, true, V, V>("gemm_logits_ds", s, Aw, Bz, K, M, P, 1, 1, e2);
+      nrows_dbp = (int)cdiv(M, ftile);
+    }
     // db_s, db_l and the loss
     const int nbs = (int)cdiv(K, HB_STRIP);
     float* share = (float*)(hws + lo.DBLP);
     // W_s rows read 8 columns at a time when they are 16-byte aligned
     const bool hb_vec = P % 8 == 0 && P <= 256 && ((uintptr_t)(W + lo.Ws) & 15) == 0;
-    BLSTM_LAUNCH("head_bias", head_bias_kernel, dim3((unsigned)nbs + 1), dim3(1024), 0, s, dbp, (int)cdiv(M, ftile),
+    BLSTM_LAUNCH("head_bias", head_bias_kernel, dim3((unsigned)nbs + 1), dim3(1024), 0, s, dbp, nrows_dbp,
                  K, P, (const bf16*)(W + lo.Ws), share, grad + lo.bs, RL, (int)M, scale, loss, hb_vec);
     BLSTM_LAUNCH("head_bias_final", head_bias_final_kernel, dim3((unsigned)cdiv(P, 16)), dim3(1024), 0, s, share,
                  nbs, P, grad + lo.bl);

@@ -549,6 +549,41 @@ def test_head_alone_on_given_hidden_states(gpu_lib, prec, tol):
         assert rel(g[off:off + int(np.prod(shp))], grads[key].reshape(-1)) <= tol, key
 
 
+@pytest.mark.parametrize("sign", [1.0, -1.0], ids=["scale_pos", "scale_neg"])
+@pytest.mark.parametrize("shape", [
+    dict(L=1, D=8, H=64, P=64, K=1000, T=7, B=24),   # 8 class blocks, the last one partial; 3 frame chunks, ragged
+    dict(L=1, D=8, H=32, P=24, K=50, T=1, B=5),      # one partial class block, one partial frame chunk
+], ids=["blocks", "one_block"])
+@pytest.mark.parametrize("blk", ["1", "0"], ids=["class_block", "tiled"])
+def test_logits_forms_on_given_hidden_states(gpu_lib, monkeypatch, blk, shape, sign):
+    """Both forms of the two logits products (the class-block kernels, and
+    the tiled products with the statistics and softmax epilogues) give the
+    head's loss and gradients.  A negative loss scale takes the form that
+    multiplies by the scale after the exponential (log2 of the scale cannot
+    be folded into the exponent); loss and gradients change sign."""
+    from paper_1907_05701_amd.step import LearnerStep
+    monkeypatch.setenv("ADPSGD_LOGITS_BLOCK", blk)
+    dims = ref.Dims(**shape)
+    n = ref.param_count(dims)
+    theta = inputs.params(n, seed=60)
+    y = inputs.hidden_states(dims.T, dims.B, 2 * dims.H, seed=61)
+    lab = inputs.labels(dims.T, dims.B, dims.K, seed=62, dist="zipf")
+    st = LearnerStep(**shape, precision="bf16")
+    st.load(theta, np.zeros((dims.T, dims.B, dims.D), np.float32), lab)
+    st.loss_scale = sign / (dims.T * dims.B)
+    st.y_top.copy_(torch.from_numpy(y).to(st.act_dtype))
+    st.head()
+    torch.cuda.synchronize()
+    loss, _, dy, grads = ref.head_forward_backward(theta, dims, y, lab)
+    assert abs(float(st.loss.cpu()[0]) - sign * loss) / loss <= BF16_TOL
+    assert rel(st.dy_top.cpu().numpy(), sign * dy) <= BF16_TOL
+    g = st.grad.cpu().numpy()
+    blocks, _ = ref.param_layout(dims)
+    for key in ("W_l", "b_l", "W_s", "b_s"):
+        off, shp = blocks[key]
+        assert rel(g[off:off + int(np.prod(shp))], sign * grads[key].reshape(-1)) <= BF16_TOL, key
+
+
 def test_deterministic_across_runs(gpu_lib):
     from paper_1907_05701_amd.step import LearnerStep
     shape = dict(L=2, D=260, H=128, P=64, K=3000, T=9, B=40)
