@@ -360,9 +360,11 @@ struct EpiSoftmaxDs {
 //     commutative, so all four lane groups hold the same result), then over
 //     the four class waves in order through LDS (one chunk later).
 //   PASS 2: ds = scale (softmax - onehot) in bf16, the frame loss at the
-//     label, and the db_s sums of the block's classes over all frames: per
-//     lane over its frames in chunk order, then over the 16 frame lanes
-//     (DPP, fixed order) and the two frame waves in order; one complete row.
+//     label, and db_s of the block's classes over all frames (per lane over
+//     its frames in chunk order, then over the 16 frame lanes (DPP, fixed
+//     order) and the two frame waves in order), written as the gradient of
+//     b_s; then the block's share of db_l = W_s^T db_s from the W_s rows in
+//     registers (the shares are summed over blocks by head_bias_final).
 // Software pipeline: iteration j multiplies chunk j + 1 while it runs the
 // epilogue of chunk j, so the MFMA and the vector ALU work overlap within
 // a wave.  The ring (LSL slots, direct-to-LDS loads; with pass 2 also the
@@ -399,7 +401,8 @@ struct LogitsArgs {
   bf16* ds;            // [M][Kp]
   int Kp;
   float* rowloss;      // [M]
-  float* dbs;          // [K]: db_s
+  float* dbs;          // [K]: db_s (the gradient of b_s)
+  float* share;        // [blocks][P]: W_s^T db_s over each block's classes
   float scale, l2s;    // as in EpiSoftmaxDs
 };
 static constexpr size_t LG_RING = (size_t)LSL * LSLOT;
@@ -511,34 +514,8 @@ __global__ __launch_bounds__(512) void logits_block_kernel(const LogitsArgs a) {
     const int rank = __builtin_amdgcn_readfirstlane(lane == 0 ? atomicAdd(&cnt[simd], 1) : 0);
     product_first = (rank & 1) == 0;
   }
-  // the wave's W_s rows (A operand): class c0 + 32 wm + 16 i + fr, k = 32 ks + 8 fc
-  bf16x8 af[2][LKS];
-  {
-    const __amdgpu_buffer_rsrc_t rw = dma_rsrc(a.Ws);
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int ks = 0; ks < LKS; ++ks) {
-        const int row = c0 + 32 * wm + 16 * i + fr, k = 32 * ks + 8 * fc;
-        const uint32_t off = row < K && k < P ? (uint32_t)(((int64_t)row * P + k) * 2) : DMA_OFF_NONE;
-        af[i][ks] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)off, 0, 0));
-      }
-  }
-  // the lane's classes cl + 16 i + r: bias, -inf past K (clamped loads)
-  f32x4 bv[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) bv[i][r] = a.bias[min(cl + 16 * i + r, K - 1)];
-  // A fragments and biases in registers before the ring loads (a wait the
-  // compiler sees, so it adds none of its own for them in the chunk loop)
-  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (cl + 16 * i + r >= K) bv[i][r] = -INFINITY;
-
+  bf16x8 af[2][LKS];   // W_s rows of the wave's classes (loaded after the ring's first chunks)
+  f32x4 bv[2];         // their biases: the first k-step's accumulator input
   // ring loads: instruction q of wave w fills rows 2 b, 2 b + 1 of the
   // chunk (b = 8 q + w); lane (parity p = lane / 32, slot s = lane % 32)
   // reads chunk s ^ p of its row
@@ -723,13 +700,40 @@ __global__ __launch_bounds__(512) void logits_block_kernel(const LogitsArgs a) {
   f32x4 accA[2][2], accB[2][2];
   float LA[2], LB_[2];
   int labA[2], labB[2];
+  // the ring's first chunks, then the fragments and biases (their latencies
+  // overlap; the fragments' wait covers the chunks)
 #pragma unroll
   for (int j = 0; j < LSL - 1; ++j) {
     no_stores();
     issue(j);
   }
   no_stores();
-  kc_wait_vm<2 * NLD + 3 * NST>();
+  // the wave's W_s rows (A operand): class c0 + 32 wm + 16 i + fr, k = 32 ks + 8 fc
+  {
+    const __amdgpu_buffer_rsrc_t rw = dma_rsrc(a.Ws);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int ks = 0; ks < LKS; ++ks) {
+        const int row = c0 + 32 * wm + 16 * i + fr, k = 32 * ks + 8 * fc;
+        const uint32_t off = row < K && k < P ? (uint32_t)(((int64_t)row * P + k) * 2) : DMA_OFF_NONE;
+        af[i][ks] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)off, 0, 0));
+      }
+  }
+  // the lane's classes cl + 16 i + r: bias, -inf past K (clamped loads)
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) bv[i][r] = a.bias[min(cl + 16 * i + r, K - 1)];
+  // fragments, biases and the first chunks in place (a wait the compiler
+  // sees, so it adds none of its own for them in the chunk loop)
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (cl + 16 * i + r >= K) bv[i][r] = -INFINITY;
+
   kc_barrier();
   issue(LSL - 1);
   no_stores();
@@ -759,7 +763,34 @@ __global__ __launch_bounds__(512) void logits_block_kernel(const LogitsArgs a) {
         for (int r = 0; r < 4; ++r) red[wn * LB + 32 * wm + 16 * i + 4 * fc + r] = csum[i][r];
     }
     __syncthreads();
-    if (tid < LB && c0 + tid < K) a.dbs[c0 + tid] = red[tid] + red[LB + tid];
+    float* dbl = red + 2 * LB;   // [LB]: the block's db_s, zero past K
+    if (tid < LB) {
+      const float v = red[tid] + red[LB + tid];
+      if (c0 + tid < K) a.dbs[c0 + tid] = v;
+      dbl[tid] = c0 + tid < K ? v : 0.f;
+    }
+    dma_wait_all();   // the ring's last (zero) loads have landed: slot 0 holds the share partials
+    __syncthreads();
+    // the block's share of db_l = W_s^T db_s, from the W_s fragments in
+    // registers (the frame-half waves wn = 1 hold the same rows): per lane
+    // its two classes, then the 16 class lanes of its lane group (DPP, fixed
+    // order), then the four class waves in order
+    float* sp = (float*)lds;   // [4 class waves][256 columns]
+    if (wn == 0) {
+      const float d0 = dbl[32 * wm + fr], d1 = dbl[32 * wm + 16 + fr];
+#pragma unroll
+      for (int ks = 0; ks < LKS; ++ks) {
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = row16_sum(fmaf(d1, (float)af[1][ks][e], d0 * (float)af[0][ks][e]));
+        if (fr == 0) {
+          *(float4*)&sp[wm * 256 + 32 * ks + 8 * fc] = make_float4(v[0], v[1], v[2], v[3]);
+          *(float4*)&sp[wm * 256 + 32 * ks + 8 * fc + 4] = make_float4(v[4], v[5], v[6], v[7]);
+        }
+      }
+    }
+    __syncthreads();
+    if (tid < P) a.share[(int64_t)blockIdx.x * P + tid] = ((sp[tid] + sp[256 + tid]) + sp[512 + tid]) + sp[768 + tid];
   }
   dma_wait_all();   // the ring's last (zero) loads land before the workgroup leaves its LDS
 }
@@ -875,9 +906,28 @@ __global__ __launch_bounds__(1024) void head_bias_kernel(const float* __restrict
 // db_l[p] for 16 columns per workgroup: thread (g, column) sums the shares
 // of strip range g (64 contiguous ranges) in order; the ranges are added in
 // order.
+// With rowloss given, one more workgroup (the last) writes
+// loss = scale * sum of the frame losses (1024 strided partial sums, then a
+// fixed tree), for launches without head_bias_kernel.
 __global__ __launch_bounds__(1024) void head_bias_final_kernel(const float* __restrict__ share, int nstrip, int P,
-                                                               float* __restrict__ grad_bl) {
+                                                               float* __restrict__ grad_bl,
+                                                               const float* __restrict__ rowloss, int M, float scale,
+                                                               float* __restrict__ loss) {
   __shared__ float sh[64][16];
+  if (rowloss && (int)blockIdx.x == (int)gridDim.x - 1) {
+    float* t = &sh[0][0];
+    const int tid = threadIdx.x;
+    float sum = 0.f;
+    for (int f = tid; f < M; f += 1024) sum += rowloss[f];
+    t[tid] = sum;
+    __syncthreads();
+    for (int w = 512; w > 0; w >>= 1) {
+      if (tid < w) t[tid] += t[tid + w];
+      __syncthreads();
+    }
+    if (tid == 0) *loss = scale * t[0];
+    return;
+  }
   const int pl = threadIdx.x & 15, g = threadIdx.x >> 4;
   const int p = blockIdx.x * 16 + pl;
   const int per = (nstrip + 63) / 64, t0 = g * per, t1 = min(nstrip, t0 + per);
@@ -977,8 +1027,9 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
       const void* k2 = fold ? (const void*)logits_block_kernel<2, true> : (const void*)logits_block_kernel<2, false>;
       kc_raise_lds_limit((const void*)logits_block_kernel<1, true>, LG_LDS, raised1);
       kc_raise_lds_limit(k2, LG_LDS, fold ? raised2 : raised3);
+      static_assert(LB == HB_STRIP, "one share row per class block");
       LogitsArgs la{(const bf16*)(W + lo.Ws), (const bf16*)Z, theta + lo.bs, K, (int)M, P, stats, nblk, lse, labels,
-                    (bf16*)DS, Kp, RL, dbp, scale, l2s};
+                    (bf16*)DS, Kp, RL, grad + lo.bs, (float*)(hws + lo.DBLP), scale, l2s};
       BLSTM_LAUNCH("logits_blk", (logits_block_kernel<1, true>), dim3((unsigned)nblk), dim3(512), LG_LDS, s, la);
       BLSTM_LAUNCH("logit_lse", logit_lse_kernel, dim3((unsigned)cdiv(M, 4)), dim3(256), 0, s, stats, nblk, M, labels,
                    K, lse, RL);
@@ -1002,10 +1053,16 @@ static int head_impl(const Layout& lo, const float* theta, const T* W, const T* 
     float* share = (float*)(hws + lo.DBLP);
     // W_s rows read 8 columns at a time when they are 16-byte aligned
     const bool hb_vec = P % 8 == 0 && P <= 256 && ((uintptr_t)(W + lo.Ws) & 15) == 0;
-    BLSTM_LAUNCH("head_bias", head_bias_kernel, dim3((unsigned)nbs + 1), dim3(1024), 0, s, dbp, nrows_dbp,
-                 K, P, (const bf16*)(W + lo.Ws), share, grad + lo.bs, RL, (int)M, scale, loss, hb_vec);
-    BLSTM_LAUNCH("head_bias_final", head_bias_final_kernel, dim3((unsigned)cdiv(P, 16)), dim3(1024), 0, s, share,
-                 nbs, P, grad + lo.bl);
+    if (blk) {
+      // the second class-block pass wrote db_s and the shares itself
+      BLSTM_LAUNCH("head_bias_final", head_bias_final_kernel, dim3((unsigned)cdiv(P, 16) + 1), dim3(1024), 0, s,
+                   share, nbs, P, grad + lo.bl, (const float*)RL, (int)M, scale, loss);
+    } else {
+      BLSTM_LAUNCH("head_bias", head_bias_kernel, dim3((unsigned)nbs + 1), dim3(1024), 0, s, dbp, nrows_dbp,
+                   K, P, (const bf16*)(W + lo.Ws), share, grad + lo.bs, RL, (int)M, scale, loss, hb_vec);
+      BLSTM_LAUNCH("head_bias_final", head_bias_final_kernel, dim3((unsigned)cdiv(P, 16)), dim3(1024), 0, s, share,
+                   nbs, P, grad + lo.bl, (const float*)nullptr, 0, 0.f, (float*)nullptr);
+    }
   } else {
     // s = z W_s^T + b_s, then loss and ds in place
     float* S = (float*)(hws + lo.S);
