@@ -313,21 +313,57 @@ __global__ __launch_bounds__(256) void lstm_rec_bwd_step(const RecBwdArgs<T> a) 
 // The input in the operand precision, rows padded from D to Dp columns
 // (zeros).  bf16 with D not a multiple of 8 also gets a copy of the layer-0
 // W_ih of both directions padded the same way (wp non-null), so that the
-// gate projection's k range (Dp) takes the direct-to-LDS product.
+// gate projection's k range (Dp) takes the direct-to-LDS product.  Dp is a
+// multiple of 8: each thread writes 8 consecutive columns of one row (one
+// 16-byte store for bf16), from vector loads where its 8 columns lie inside
+// D and the source is aligned for them.
 template <typename T>
 __global__ __launch_bounds__(256) void convert_input_kernel(const float* __restrict__ x, int64_t M,
                                                             int D, int Dp, T* __restrict__ X,
                                                             const bf16* __restrict__ w0, int64_t wz, int wrows,
                                                             bf16* __restrict__ wp) {
-  // one row per workgroup: the M frames, then (with wp) the 2*wrows rows of
-  // both directions' W_ih
-  const int64_t row = blockIdx.x;
+  const int cpr = Dp / 8;
+  const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t row = g / cpr;
+  const int k0 = (int)(g % cpr) * 8;
+  if (row >= M + (wp ? 2 * (int64_t)wrows : 0)) return;
   if (row < M) {
-    for (int k = threadIdx.x; k < Dp; k += 256) X[row * Dp + k] = from_f32<T>(k < D ? x[row * D + k] : 0.f);
+    const float* src = x + row * D + k0;
+    float v[8];
+    if (k0 + 8 <= D && (D & 3) == 0 && ((uintptr_t)x & 15) == 0) {
+      const float4 p = *(const float4*)src, q = *(const float4*)(src + 4);
+      v[0] = p.x; v[1] = p.y; v[2] = p.z; v[3] = p.w; v[4] = q.x; v[5] = q.y; v[6] = q.z; v[7] = q.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = x[row * D + min(k0 + e, D - 1)];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = k0 + e < D ? v[e] : 0.f;
+    }
+    T o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = from_f32<T>(v[e]);
+    T* dst = X + row * Dp + k0;
+    if constexpr (sizeof(T) == 2) {
+      *(uint4*)dst = *(const uint4*)o;
+    } else {
+      *(uint4*)dst = *(const uint4*)o;
+      *(uint4*)(dst + 4) = *(const uint4*)(o + 4);
+    }
   } else {
     const int zr = (int)(row - M), z = zr / wrows, r = zr % wrows;
-    for (int k = threadIdx.x; k < Dp; k += 256)
-      wp[(int64_t)zr * Dp + k] = k < D ? w0[z * wz + (int64_t)r * D + k] : (bf16)0.f;
+    const bf16* src = w0 + z * wz + (int64_t)r * D;
+    bf16 o[8];
+    if (k0 + 8 <= D && ((D | (int)(wz & 3)) & 3) == 0 && ((uintptr_t)w0 & 7) == 0) {
+      const uint2 p = *(const uint2*)(src + k0), q = *(const uint2*)(src + k0 + 4);
+      *(uint2*)o = p;
+      *(uint2*)(o + 4) = q;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = src[min(k0 + e, D - 1)];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = k0 + e < D ? o[e] : (bf16)0.f;
+    }
+    *(uint4*)(wp + (int64_t)zr * Dp + k0) = *(const uint4*)o;
   }
 }
 
@@ -438,7 +474,8 @@ static int fwd_impl(const Layout& lo, const float* theta, const T* W, const floa
   T* GX = (T*)(ws + lo.GX);
   bf16* WP0 = lo.WP0_bytes ? (bf16*)(ws + lo.WP0) : nullptr;
   {
-    const unsigned grid = (unsigned)(M + (WP0 ? 2 * 4 * H : 0));
+    const int64_t rows = M + (WP0 ? 2 * 4 * H : 0);
+    const unsigned grid = (unsigned)cdiv(rows * (lo.Dp0 / 8), 256);
     BLSTM_LAUNCH("convert_input", convert_input_kernel<T>, dim3(grid), dim3(256), 0, s, x, M, lo.D,
                  lo.Dp0, X0, (const bf16*)W + lo.Wih[0][0], lo.Wih[0][1] - lo.Wih[0][0], 4 * H, WP0);
   }
