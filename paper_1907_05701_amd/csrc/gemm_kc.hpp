@@ -433,9 +433,9 @@ struct KcItem {
 
 // Launches products with the same operand layouts as one grid; false (and
 // nothing launched) if any of them cannot take the direct-to-LDS path.
-template <bool AKC, bool BKC, class Epi>
-static inline bool gemm_kc_group_launch(const char* name, hipStream_t s, int n, const KcItem* it, const Epi* epi) {
-  typedef KcTile C;
+template <class C, bool AKC, bool BKC, class Epi>
+static inline bool gemm_kc_group_launch_cfg(const char* name, hipStream_t s, int n, const KcItem* it,
+                                            const Epi* epi) {
   if (n < 1 || n > KC_MAX_GROUP) return false;
   KcGroup<Epi> g;
   std::memset((void*)&g, 0, sizeof g);
@@ -455,4 +455,19 @@ static inline bool gemm_kc_group_launch(const char* name, hipStream_t s, int n, 
   kc_raise_lds_limit((const void*)fn, C::lds_bytes, lds_raised);
   BLSTM_LAUNCH(name, fn, dim3((unsigned)start), dim3(C::WM * C::WN * 64), C::lds_bytes, s, g);
   return true;
+}
+
+// A grouped launch with more 128x128 blocks than one round of two per CU
+// takes 192-row blocks when every product has at least 192 rows (as a
+// single product does).
+template <bool AKC, bool BKC, class Epi>
+static inline bool gemm_kc_group_launch(const char* name, hipStream_t s, int n, const KcItem* it, const Epi* epi) {
+  int64_t blocks = 0;
+  bool tall = n >= 1 && n <= KC_MAX_GROUP;
+  for (int i = 0; tall && i < n; ++i) {
+    blocks += cdiv(it[i].M, 128) * cdiv(it[i].N, 128) * it[i].batches * it[i].splits;
+    tall = it[i].M >= KcTileTall::BM;
+  }
+  if (tall && blocks > kc_round_blocks) return gemm_kc_group_launch_cfg<KcTileTall, AKC, BKC>(name, s, n, it, epi);
+  return gemm_kc_group_launch_cfg<KcTile, AKC, BKC>(name, s, n, it, epi);
 }
