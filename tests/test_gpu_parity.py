@@ -584,6 +584,35 @@ def test_logits_forms_on_given_hidden_states(gpu_lib, monkeypatch, blk, shape, s
         assert rel(g[off:off + int(np.prod(shp))], sign * grads[key].reshape(-1)) <= BF16_TOL, key
 
 
+@pytest.mark.parametrize("blk", ["1", "0"], ids=["class_block", "tiled"])
+def test_logits_forms_zero_loss_scale(gpu_lib, monkeypatch, blk):
+    """A zero loss scale (no log2 of it to fold into the exponent) gives a
+    zero loss and exactly zero head gradients and dy_top in both forms of
+    the logits products; 128 frames, two whole 64-frame chunks."""
+    from paper_1907_05701_amd.step import LearnerStep
+    monkeypatch.setenv("ADPSGD_LOGITS_BLOCK", blk)
+    shape = dict(L=1, D=8, H=64, P=64, K=1000, T=8, B=16)
+    dims = ref.Dims(**shape)
+    n = ref.param_count(dims)
+    theta = inputs.params(n, seed=63)
+    y = inputs.hidden_states(dims.T, dims.B, 2 * dims.H, seed=64)
+    lab = inputs.labels(dims.T, dims.B, dims.K, seed=65, dist="zipf")
+    st = LearnerStep(**shape, precision="bf16")
+    st.load(theta, np.zeros((dims.T, dims.B, dims.D), np.float32), lab)
+    st.loss_scale = 0.0
+    st.y_top.copy_(torch.from_numpy(y).to(st.act_dtype))
+    st.grad.fill_(1.0)
+    st.head()
+    torch.cuda.synchronize()
+    assert float(st.loss.cpu()[0]) == 0.0
+    assert not st.dy_top.abs().max().item()
+    g = st.grad.cpu().numpy()
+    blocks, _ = ref.param_layout(dims)
+    for key in ("W_l", "b_l", "W_s", "b_s"):
+        off, shp = blocks[key]
+        assert not np.abs(g[off:off + int(np.prod(shp))]).max(), key
+
+
 def test_deterministic_across_runs(gpu_lib):
     from paper_1907_05701_amd.step import LearnerStep
     shape = dict(L=2, D=260, H=128, P=64, K=3000, T=9, B=40)
